@@ -1,0 +1,211 @@
+/*
+ * librq -- RateQuant hot path on AMD Instinct MI355X (gfx950).
+ *
+ * RateQuant (arXiv 2605.06675) gives every KV head its own bit-width: it
+ * fits a distortion curve D(b) = alpha * beta^-b per quantizer and component
+ * (Alg. 1 Stage 2; Sec. 3.4), allocates integer bits under an average budget
+ * (eq. 1; Theorem 1; Alg. 1 Stage 3 / Alg. 2), and then quantizes each head
+ * of the KV cache at its own width; decode attention reads the packed cache
+ * back (Sec. 3.4 "Pipeline summary"; Appendix "Runtime Analysis").
+ *
+ * Conventions for every call
+ *  - Plain C types only.  "device" pointers are HIP device memory owned by
+ *    the caller; "host" pointers are ordinary host memory owned by the
+ *    caller.  The library allocates no device memory and keeps no state
+ *    between calls.
+ *  - Asynchronous calls enqueue kernels on the given stream and return
+ *    without waiting.  Synchronous calls say so.
+ *  - Every argument is validated on the host before anything is enqueued;
+ *    a call that returns an error has written nothing.  rq_last_error()
+ *    then describes the problem (thread-local, valid until the next call
+ *    on the same thread).
+ *  - head_dim is 128.  Bit-widths are 1..8 (QuaRot needs >= 2).
+ *
+ * Numeric formats (bit-exact contract shared with the test oracle)
+ *  - K/V inputs are fp16 or bf16 (rq_dtype).  Metadata (scale, zero) is
+ *    fp16, rounded to nearest-even from fp32 and saturated at +-65504.
+ *  - A code is decided by correctly-rounded fp32 steps, rint half-to-even:
+ *      KIVI   z = fp16(min), s = fp16(max(max - z, 0) / (2^b - 1)),
+ *             code = rint(clamp((x - z) * fp32(1/s), 0, 2^b - 1)),
+ *             all codes 0 when s == 0; groups: keys = one channel over 32
+ *             consecutive tokens, values = 32 consecutive channels of one
+ *             token.
+ *      QuaRot y = fp32(FWHT(x) * fp32(1/sqrt(128))) with the butterfly
+ *             stages h = 1, 2, ..., 64 in that order; s = fp16(max|y| /
+ *             (2^(b-1) - 1)); code = rint(clamp(y * fp32(1/s), -q, q)) +
+ *             2^(b-1), q = 2^(b-1) - 1 (all codes 2^(b-1) when s == 0).
+ *  - Packed chunk: 32 codes of one stream in exactly b uint32 words.  The
+ *    code bits are split into planes of widths equal to the binary digits
+ *    of b, widest first (3 -> 2+1, 5 -> 4+1, 6 -> 4+2, 7 -> 4+2+1); plane
+ *    width w occupies w words, and its word d holds the field of code
+ *    d*16/w + k at bit k*w and that of code 16 + d*16/w + k at bit
+ *    16 + k*w, for k = 0 .. 16/w - 1.
+ *  - Pair order of 32 entries: 0,16,1,17,...,15,31.
+ *
+ * Cache layout (one buffer each; the caller allocates the sizes reported by
+ * rq_cache_sizes).  A "unit" is one (layer, batch entry, kv-head).  T_cap is
+ * rq_cache.capacity (a multiple of 32), R = rq_cache.residual.
+ *  codes  regions in order layer, head, K then V; region (l,h,kind) holds
+ *         batch * T_cap * 16 * b bytes, b = bits[l][h][kind]:
+ *           K: [batch][token][chunk q: channels 32q..32q+31][b words]
+ *           V: [batch][block of 32 tokens][channel][b words]  (a chunk is
+ *              the 32 tokens of the block)
+ *  meta   KIVI:   [l][h][kind][batch][block][4][s(32), z(32)] fp16, pair
+ *                 order; K: group index = chunk q, entries = channels;
+ *                 V: group index = channel group cg, entries = tokens.
+ *         QuaRot: [l][h][kind][batch][block][s(32 tokens)] fp16, pair order.
+ *  resid  [l][batch][h][kind][R + 32][128] in the input dtype; token t of
+ *         the 16-bit window lives in slot t mod (R + 32).
+ *  Residual rule: with T tokens cached the quantized prefix is
+ *  nq = max(0, floor((T - R) / 32) * 32); tokens nq .. T-1 stay 16-bit.
+ */
+#ifndef RQ_H
+#define RQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t rq_status;
+#define RQ_OK 0
+#define RQ_EINVAL (-1)        /* bad argument                               */
+#define RQ_EINFEASIBLE (-2)   /* budget outside [n*bmin, n*bmax]            */
+#define RQ_EUNSUPPORTED (-3)  /* valid but not implemented (head_dim, ...)  */
+#define RQ_EDEVICE (-4)       /* a HIP runtime call failed                  */
+#define RQ_ESMALLWS (-5)      /* workspace smaller than required            */
+
+#define RQ_KIVI 0
+#define RQ_QUAROT 1
+#define RQ_TURBO 2
+
+#define RQ_F16 0
+#define RQ_BF16 1
+
+#define RQ_MAX_KV_HEADS 32
+
+/* HIP stream handle, passed through as an opaque pointer. */
+typedef void* rq_stream;
+
+/* Cache descriptor.  Plain data filled by the caller; the library only
+ * reads it.  bits is the per-(layer, kv-head) bit table of the paper (its
+ * "static lookup table", Appendix "Runtime Analysis"): host int8
+ * [n_layers][n_kv_heads][2], K then V. */
+typedef struct rq_cache {
+  int32_t family;        /* RQ_KIVI or RQ_QUAROT                          */
+  int32_t dtype;         /* RQ_F16 or RQ_BF16: K/V/q input type           */
+  int32_t n_layers;
+  int32_t batch;
+  int32_t n_kv_heads;    /* <= RQ_MAX_KV_HEADS                            */
+  int32_t n_q_heads;     /* multiple of n_kv_heads, ratio <= 16           */
+  int32_t head_dim;      /* 128                                           */
+  int32_t capacity;      /* max cached tokens per sequence, % 32 == 0     */
+  int32_t residual;      /* R >= 0: 16-bit window length in tokens        */
+  const int8_t* bits;    /* host [n_layers][n_kv_heads][2]                */
+  void* codes;           /* device, >= codes_bytes                        */
+  void* meta;            /* device, >= meta_bytes                         */
+  void* resid;           /* device, >= resid_bytes                        */
+} rq_cache;
+
+/* Library version (major*10000 + minor*100 + patch). */
+int32_t rq_version(void);
+
+/* Thread-local text for the last non-OK status (never NULL). */
+const char* rq_last_error(void);
+
+/* Validate a descriptor (device pointers may be NULL here) and report the
+ * buffer sizes in bytes.  Any output pointer may be NULL.  Host only. */
+rq_status rq_cache_sizes(const rq_cache* c, uint64_t* codes_bytes,
+                         uint64_t* meta_bytes, uint64_t* resid_bytes);
+
+/* Byte offset of the code region (layer, head, kind) inside codes, i.e. the
+ * prefix sum of region sizes in (layer, head, K-then-V) order: the O(1)
+ * lookup of the bit table.  Host only. */
+rq_status rq_region_offset(const rq_cache* c, int32_t layer, int32_t head,
+                           int32_t kind, uint64_t* offset);
+
+/* Append n_new >= 1 tokens to one layer that already holds n_past tokens
+ * (0 <= n_past, n_past + n_new <= capacity).  k, v: device
+ * [batch][n_kv_heads][n_new][128] in dtype, contiguous.  Quantizes every
+ * 32-token block that leaves the residual window (reading older tokens
+ * from the window and newer ones from k, v) and stores the newest tokens
+ * in the window.  Asynchronous.  Sec. 3.4 / Appendix "Quantizer
+ * Implementation" (the base quantizers), Appendix "Runtime Analysis" (the
+ * per-head bit lookup). */
+rq_status rq_quantize_kv(const rq_cache* c, int32_t layer, int32_t n_past,
+                         const void* k, const void* v, int32_t n_new,
+                         rq_stream stream);
+
+/* Workspace bytes rq_decode_attention needs for n_tokens cached tokens. */
+rq_status rq_decode_workspace(const rq_cache* c, int32_t n_tokens,
+                              uint64_t* bytes);
+
+/* Decode attention of one new query per sequence over the n_tokens cached
+ * tokens of one layer (1 <= n_tokens <= capacity):
+ *   out[b][j] = softmax(scale * q[b][j] . K_hat^T) V_hat,
+ * K_hat/V_hat the dequantized prefix plus the 16-bit window, query head j
+ * reading kv-head j / (n_q_heads / n_kv_heads).  q: device
+ * [batch][n_q_heads][128] in dtype; out: device fp32, same shape; ws:
+ * device scratch of at least rq_decode_workspace bytes (contents on entry
+ * do not matter).  Asynchronous. */
+rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
+                              int32_t n_tokens, const void* q, float* out,
+                              float scale, void* ws, uint64_t ws_bytes,
+                              rq_stream stream);
+
+/* Workspace bytes rq_calibrate_distortion needs. */
+rq_status rq_calibrate_workspace(int32_t n_comp, int32_t n_tokens,
+                                 int32_t n_bits, uint64_t* bytes);
+
+/* Distortion sweep + fit (Alg. 1 Stage 2; Sec. 3.4 "Distortion
+ * calibration").  x: device [n_comp][n_tokens][128] in dtype, the
+ * calibration vectors of each component (n_tokens % 32 == 0).  For every
+ * component i and bit-width bits[j]:
+ *   mse[i][j] = mean over tokens and channels of (x - dequant(quant(x)))^2
+ * with the key grouping (is_value = 0) or value grouping (is_value = 1) of
+ * the family, measured in the unrotated domain; then alpha, beta, r2 as in
+ * rq_fit_distortion.  mse, alpha, beta, r2: host arrays ([n_comp][n_bits]
+ * and [n_comp]); alpha/beta/r2 may be NULL to skip the fit.  ws: device
+ * scratch of rq_calibrate_workspace bytes.  Synchronous: waits for the
+ * stream and copies the results to the host. */
+rq_status rq_calibrate_distortion(int32_t family, int32_t dtype,
+                                  const void* x, int32_t n_comp,
+                                  int32_t n_tokens, int32_t is_value,
+                                  const int32_t* bits, int32_t n_bits,
+                                  double* mse, double* alpha, double* beta,
+                                  double* r2, void* ws, uint64_t ws_bytes,
+                                  rq_stream stream);
+
+/* Least-squares fit of ln D = ln alpha - b ln beta per component
+ * (Alg. 1 Stage 2).  mse: host [n_comp][n_bits] (all > 0), n_bits >= 2
+ * distinct widths.  Outputs host [n_comp]; r2 = 1 - SS_res/SS_tot (1 when
+ * SS_tot = 0).  Host only. */
+rq_status rq_fit_distortion(const double* mse, int32_t n_comp,
+                            const int32_t* bits, int32_t n_bits,
+                            double* alpha, double* beta, double* r2);
+
+/* Integer bit allocation over n components (eq. 1 with per-component
+ * alpha_i, beta_i; Theorem 1 and its bound handling; Alg. 1 Stage 3 /
+ * Alg. 2).  Budget B = round(avg_bits * n) (halves away from zero).
+ * bits_out[i] (host int32 [n]) is the greedy max-marginal-gain allocation:
+ * start at bmin and give each of the B - n*bmin remaining bits to the
+ * component with the largest log-gain
+ *   log(w) + log(alpha) - b*log(beta) + log1p(-1/beta)
+ * (IEEE double, left to right; ties to the lowest index), never above bmax.
+ * bits_cont_out (nullable, host double [n]) receives the continuous optimum
+ * (the KKT point of eq. 1, reverse waterfilling with the box bounds) and
+ * J_out (nullable) the weighted distortion sum w_i alpha_i beta_i^-b_i of
+ * bits_out.  Requires w, alpha > 0, beta > 1, 1 <= bmin <= bmax <= 8 and
+ * n*bmin <= B <= n*bmax (else RQ_EINFEASIBLE).  Host only. */
+rq_status rq_allocate_bits(int32_t n, const double* w, const double* alpha,
+                           const double* beta, double avg_bits, int32_t bmin,
+                           int32_t bmax, int32_t* bits_out,
+                           double* bits_cont_out, double* J_out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RQ_H */

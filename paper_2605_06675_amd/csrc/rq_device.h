@@ -1,0 +1,135 @@
+// Device helpers: number conversions, the quantizer arithmetic that decides
+// codes, and the packed-chunk format (32 codes in b words, bit planes whose
+// widths are the binary digits of b, codes i and i+16 sharing the two
+// half-words of a word).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rq {
+
+typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float widen(uint32_t bits16, int is_bf16) {
+  if (is_bf16) return __uint_as_float(bits16 << 16);
+  _Float16 h = __builtin_bit_cast(_Float16, (uint16_t)bits16);
+  return (float)h;
+}
+
+// fp32 -> fp16, nearest-even, saturated at +-65504.  Returns raw bits.
+__device__ __forceinline__ uint16_t f16_sat(float x) {
+  x = __builtin_fminf(__builtin_fmaxf(x, -65504.0f), 65504.0f);
+  return __builtin_bit_cast(uint16_t, (_Float16)x);
+}
+
+__device__ __forceinline__ float f16_to_f32(uint16_t b) {
+  return (float)__builtin_bit_cast(_Float16, b);
+}
+
+// rint half-to-even of a value already clamped to [lo, hi] (|v| < 2^22).
+__device__ __forceinline__ int rint_i(float v) {
+  return (int)__builtin_rintf(v);
+}
+
+// Asymmetric group parameters from (min, max): zero = fp16(min), scale =
+// fp16(max(max - zero, 0) / qmax); inv = 1/scale (0 when scale == 0, which
+// sends every code to 0).
+struct AsymParams {
+  uint16_t s16, z16;
+  float zf, inv;
+};
+
+__device__ __forceinline__ AsymParams asym_params(float mn, float mx,
+                                                  float qmax) {
+  AsymParams p;
+  p.z16 = f16_sat(mn);
+  p.zf = f16_to_f32(p.z16);
+  float rng = __builtin_fmaxf(mx - p.zf, 0.0f);
+  p.s16 = f16_sat(rng / qmax);
+  float sf = f16_to_f32(p.s16);
+  p.inv = (sf != 0.0f) ? 1.0f / sf : 0.0f;
+  return p;
+}
+
+__device__ __forceinline__ int asym_code(float x, const AsymParams& p,
+                                         float qmax) {
+  float r = (x - p.zf) * p.inv;  // two roundings: built with fp-contract off
+  r = __builtin_fminf(__builtin_fmaxf(r, 0.0f), qmax);
+  return rint_i(r);
+}
+
+// Bit planes of a b-bit code, widest first.
+template <int B> struct Planes;
+template <> struct Planes<1> { static constexpr int n = 1; static constexpr int w[1] = {1}; };
+template <> struct Planes<2> { static constexpr int n = 1; static constexpr int w[1] = {2}; };
+template <> struct Planes<3> { static constexpr int n = 2; static constexpr int w[2] = {2, 1}; };
+template <> struct Planes<4> { static constexpr int n = 1; static constexpr int w[1] = {4}; };
+template <> struct Planes<5> { static constexpr int n = 2; static constexpr int w[2] = {4, 1}; };
+template <> struct Planes<6> { static constexpr int n = 2; static constexpr int w[2] = {4, 2}; };
+template <> struct Planes<7> { static constexpr int n = 3; static constexpr int w[3] = {4, 2, 1}; };
+template <> struct Planes<8> { static constexpr int n = 1; static constexpr int w[1] = {8}; };
+
+// Pack 32 codes (bytes, code i = byte i of c[i/4]) into B words.
+template <int B>
+__device__ __forceinline__ void pack_chunk(const uint32_t c[8], uint32_t out[B]) {
+  int word = 0, shift = 0;
+#pragma unroll
+  for (int p = 0; p < Planes<B>::n; ++p) {
+    const int w = Planes<B>::w[p];
+    const int per = 16 / w;
+    const uint32_t m = (1u << w) - 1u;
+#pragma unroll
+    for (int d = 0; d < w; ++d) {
+      uint32_t acc = 0;
+#pragma unroll
+      for (int k = 0; k < per; ++k) {
+        const int i0 = d * per + k, i1 = 16 + d * per + k;
+        uint32_t c0 = (c[i0 >> 2] >> (8 * (i0 & 3))) & 0xffu;
+        uint32_t c1 = (c[i1 >> 2] >> (8 * (i1 & 3))) & 0xffu;
+        acc |= ((c0 >> shift) & m) << (k * w);
+        acc |= ((c1 >> shift) & m) << (16 + k * w);
+      }
+      out[word++] = acc;
+    }
+    shift += w;
+  }
+}
+
+// Codes i and i+16 of a chunk (0 <= i < 16) as the two half-words of a
+// uint32, read from the chunk's B words (i must fold to a constant after
+// unrolling).
+template <int B>
+__device__ __forceinline__ uint32_t pair_bits(const uint32_t* wds, int I) {
+  uint32_t v = 0;
+  int word = 0, shift = 0;
+#pragma unroll
+  for (int p = 0; p < Planes<B>::n; ++p) {
+    const int w = Planes<B>::w[p];
+    const int per = 16 / w;
+    const uint32_t m = ((1u << w) - 1u) * 0x00010001u;
+    const int d = I / per, k = I % per;
+    v |= ((wds[word + d] >> (k * w)) & m) << shift;
+    word += w;
+    shift += w;
+  }
+  return v;
+}
+
+__device__ __forceinline__ h2 as_h2(uint32_t x) {
+  return __builtin_bit_cast(h2, x);
+}
+__device__ __forceinline__ uint32_t as_u32(h2 x) {
+  return __builtin_bit_cast(uint32_t, x);
+}
+
+// Two codes (half-words) -> the fp16 pair (code0, code1), exactly:
+// 0x6400 | c is 1024 + c in fp16, and 1024 is then subtracted.
+__device__ __forceinline__ h2 codes_to_h2(uint32_t pair, h2 off) {
+  return as_h2(pair | 0x64006400u) - off;
+}
+
+}  // namespace rq

@@ -1,0 +1,403 @@
+// C-ABI entry points: validation, cache layout, launch set-up.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <string>
+#include <vector>
+
+#include "rq_host.h"
+#include "rq_internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+rq_status fail(rq_status code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+rq_status ok() {
+  g_err.clear();
+  return RQ_OK;
+}
+
+rq_status hip_fail(hipError_t e, const char* what) {
+  return fail(RQ_EDEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+int n_quantized(int T, int R) {
+  const int x = T - R;
+  return x <= 0 ? 0 : (x / rq::kChunk) * rq::kChunk;
+}
+
+int meta_per_block(const rq_cache* c) {
+  return c->family == RQ_KIVI ? rq::kMetaBlockKivi : rq::kMetaBlockTok;
+}
+
+rq_status check_cache(const rq_cache* c) {
+  if (!c) return fail(RQ_EINVAL, "cache descriptor is NULL");
+  if (c->family != RQ_KIVI && c->family != RQ_QUAROT) {
+    if (c->family == RQ_TURBO)
+      return fail(RQ_EUNSUPPORTED, "TurboQuant family is not built in this library");
+    return fail(RQ_EINVAL, "unknown family %d", c->family);
+  }
+  if (c->dtype != RQ_F16 && c->dtype != RQ_BF16)
+    return fail(RQ_EINVAL, "unknown dtype %d", c->dtype);
+  if (c->head_dim != rq::kD)
+    return fail(RQ_EUNSUPPORTED, "head_dim %d (only 128 is supported)", c->head_dim);
+  if (c->n_layers < 1 || c->batch < 1)
+    return fail(RQ_EINVAL, "n_layers and batch must be >= 1");
+  if (c->n_kv_heads < 1 || c->n_kv_heads > RQ_MAX_KV_HEADS)
+    return fail(RQ_EINVAL, "n_kv_heads %d outside 1..%d", c->n_kv_heads,
+                RQ_MAX_KV_HEADS);
+  if (c->n_q_heads < c->n_kv_heads || c->n_q_heads % c->n_kv_heads)
+    return fail(RQ_EINVAL, "n_q_heads %d is not a multiple of n_kv_heads %d",
+                c->n_q_heads, c->n_kv_heads);
+  if (c->n_q_heads / c->n_kv_heads > 16)
+    return fail(RQ_EUNSUPPORTED, "more than 16 query heads per kv-head");
+  if (c->capacity < rq::kChunk || c->capacity % rq::kChunk)
+    return fail(RQ_EINVAL, "capacity %d must be a positive multiple of 32",
+                c->capacity);
+  if (c->residual < 0) return fail(RQ_EINVAL, "residual window must be >= 0");
+  if (!c->bits) return fail(RQ_EINVAL, "bit table is NULL");
+  const int lo = c->family == RQ_QUAROT ? 2 : 1;
+  for (int i = 0; i < c->n_layers * c->n_kv_heads * 2; ++i) {
+    const int b = c->bits[i];
+    if (b < lo || b > 8)
+      return fail(RQ_EINVAL, "bit table entry %d is %d (allowed %d..8)", i, b, lo);
+  }
+  const double codes = (double)c->n_layers * c->n_kv_heads * 2 * c->batch *
+                       c->capacity * 16.0 * 8;
+  if (codes > 9.0e18) return fail(RQ_EINVAL, "cache too large");
+  return RQ_OK;
+}
+
+uint64_t region_bytes(const rq_cache* c, int b) {
+  return (uint64_t)c->batch * c->capacity * 16 * b;
+}
+
+uint64_t region_offset(const rq_cache* c, int layer, int head, int kind) {
+  uint64_t off = 0;
+  const int H = c->n_kv_heads;
+  const int stop = (layer * H + head) * 2 + kind;
+  for (int i = 0; i < stop; ++i) off += region_bytes(c, c->bits[i]);
+  return off;
+}
+
+uint64_t meta_layer_bytes(const rq_cache* c) {
+  return (uint64_t)c->n_kv_heads * 2 * c->batch * (c->capacity / rq::kChunk) *
+         meta_per_block(c);
+}
+
+uint64_t resid_layer_elems(const rq_cache* c) {
+  return (uint64_t)c->batch * c->n_kv_heads * 2 * (c->residual + rq::kChunk) *
+         rq::kD;
+}
+
+rq::LayerTable layer_table(const rq_cache* c, int layer) {
+  rq::LayerTable t{};
+  uint64_t off = region_offset(c, layer, 0, 0);
+  for (int h = 0; h < c->n_kv_heads; ++h)
+    for (int kind = 0; kind < 2; ++kind) {
+      const int b = c->bits[(layer * c->n_kv_heads + h) * 2 + kind];
+      t.code_off[h][kind] = off;
+      t.bits[h][kind] = (uint8_t)b;
+      off += region_bytes(c, b);
+    }
+  return t;
+}
+
+struct SplitPlan {
+  int nq, n_split, blk_per_split;
+};
+
+SplitPlan plan_splits(const rq_cache* c, int n_tokens) {
+  SplitPlan p;
+  p.nq = n_quantized(n_tokens, c->residual);
+  const int nblk = p.nq / rq::kChunk;
+  const long units = (long)c->batch * c->n_kv_heads;
+  long want = 4;
+  const char* env = std::getenv("RQ_ATTN_BLOCKS_PER_SPLIT");
+  if (env && std::atoi(env) > 0) {
+    want = std::atoi(env);
+  } else {
+    const long total = units * nblk;
+    const long per = (total + 6143) / 6144;
+    if (per > want) want = per;
+  }
+  p.blk_per_split = (int)want;
+  p.n_split = nblk == 0 ? 0 : (nblk + p.blk_per_split - 1) / p.blk_per_split;
+  return p;
+}
+
+uint64_t attn_ws_bytes(const rq_cache* c, const SplitPlan& p) {
+  const uint64_t G = c->n_q_heads / c->n_kv_heads;
+  const uint64_t parts = (uint64_t)c->batch * c->n_kv_heads * (p.n_split + 1);
+  return parts * G * (2 + rq::kD) * sizeof(float);
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t rq_version(void) { return 100; }
+
+const char* rq_last_error(void) { return g_err.c_str(); }
+
+rq_status rq_cache_sizes(const rq_cache* c, uint64_t* codes_bytes,
+                         uint64_t* meta_bytes, uint64_t* resid_bytes) {
+  rq_status st = check_cache(c);
+  if (st != RQ_OK) return st;
+  if (codes_bytes) *codes_bytes = region_offset(c, c->n_layers, 0, 0);
+  if (meta_bytes) *meta_bytes = meta_layer_bytes(c) * c->n_layers;
+  if (resid_bytes)
+    *resid_bytes = resid_layer_elems(c) * c->n_layers * sizeof(uint16_t);
+  return ok();
+}
+
+rq_status rq_region_offset(const rq_cache* c, int32_t layer, int32_t head,
+                           int32_t kind, uint64_t* offset) {
+  rq_status st = check_cache(c);
+  if (st != RQ_OK) return st;
+  if (layer < 0 || layer >= c->n_layers || head < 0 || head >= c->n_kv_heads ||
+      kind < 0 || kind > 1 || !offset)
+    return fail(RQ_EINVAL, "region (%d, %d, %d) out of range", layer, head, kind);
+  *offset = region_offset(c, layer, head, kind);
+  return ok();
+}
+
+rq_status rq_quantize_kv(const rq_cache* c, int32_t layer, int32_t n_past,
+                         const void* k, const void* v, int32_t n_new,
+                         rq_stream stream) {
+  rq_status st = check_cache(c);
+  if (st != RQ_OK) return st;
+  if (layer < 0 || layer >= c->n_layers)
+    return fail(RQ_EINVAL, "layer %d out of range", layer);
+  if (n_past < 0 || n_new < 1 || (int64_t)n_past + n_new > c->capacity)
+    return fail(RQ_EINVAL, "tokens %d + %d exceed capacity %d", n_past, n_new,
+                c->capacity);
+  if (!k || !v || !c->codes || !c->meta || !c->resid)
+    return fail(RQ_EINVAL, "NULL device pointer");
+  const int T_new = n_past + n_new;
+  const int nq_old = n_quantized(n_past, c->residual);
+  const int nq_new = n_quantized(T_new, c->residual);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+
+  rq::QuantLaunch q{};
+  q.k = static_cast<const uint16_t*>(k);
+  q.v = static_cast<const uint16_t*>(v);
+  q.codes = static_cast<uint8_t*>(c->codes);
+  q.meta = static_cast<uint8_t*>(c->meta) + meta_layer_bytes(c) * layer;
+  q.resid = static_cast<uint16_t*>(c->resid) + resid_layer_elems(c) * layer;
+  q.B = c->batch;
+  q.H = c->n_kv_heads;
+  q.n_new = n_new;
+  q.n_past = n_past;
+  q.cap = c->capacity;
+  q.R = c->residual;
+  q.blk0 = nq_old / rq::kChunk;
+  q.nblk = (nq_new - nq_old) / rq::kChunk;
+  q.is_bf16 = c->dtype == RQ_BF16;
+  q.family = c->family;
+  q.tab = layer_table(c, layer);
+  hipError_t e = rq::launch_quantize(q, s);
+  if (e != hipSuccess) return hip_fail(e, "quantize launch");
+
+  rq::RingLaunch r{};
+  r.k = q.k;
+  r.v = q.v;
+  r.resid = q.resid;
+  r.B = c->batch;
+  r.H = c->n_kv_heads;
+  r.n_new = n_new;
+  r.n_past = n_past;
+  r.R = c->residual;
+  r.t_lo = nq_new > n_past ? nq_new : n_past;
+  r.t_hi = T_new;
+  e = rq::launch_ring(r, s);
+  if (e != hipSuccess) return hip_fail(e, "window launch");
+  return ok();
+}
+
+rq_status rq_decode_workspace(const rq_cache* c, int32_t n_tokens,
+                              uint64_t* bytes) {
+  rq_status st = check_cache(c);
+  if (st != RQ_OK) return st;
+  if (n_tokens < 1 || n_tokens > c->capacity)
+    return fail(RQ_EINVAL, "n_tokens %d outside 1..%d", n_tokens, c->capacity);
+  if (!bytes) return fail(RQ_EINVAL, "bytes is NULL");
+  *bytes = attn_ws_bytes(c, plan_splits(c, n_tokens));
+  return ok();
+}
+
+rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
+                              int32_t n_tokens, const void* q, float* out,
+                              float scale, void* ws, uint64_t ws_bytes,
+                              rq_stream stream) {
+  rq_status st = check_cache(c);
+  if (st != RQ_OK) return st;
+  if (layer < 0 || layer >= c->n_layers)
+    return fail(RQ_EINVAL, "layer %d out of range", layer);
+  if (n_tokens < 1 || n_tokens > c->capacity)
+    return fail(RQ_EINVAL, "n_tokens %d outside 1..%d", n_tokens, c->capacity);
+  if (!q || !out || !ws || !c->codes || !c->meta || !c->resid)
+    return fail(RQ_EINVAL, "NULL device pointer");
+  if (!std::isfinite(scale)) return fail(RQ_EINVAL, "scale is not finite");
+  const SplitPlan p = plan_splits(c, n_tokens);
+  const uint64_t need = attn_ws_bytes(c, p);
+  if (ws_bytes < need)
+    return fail(RQ_ESMALLWS, "workspace %llu bytes < %llu needed",
+                (unsigned long long)ws_bytes, (unsigned long long)need);
+  const int G = c->n_q_heads / c->n_kv_heads;
+  rq::AttnLaunch a{};
+  a.q = static_cast<const uint16_t*>(q);
+  a.codes = static_cast<const uint8_t*>(c->codes);
+  a.meta = static_cast<const uint8_t*>(c->meta) + meta_layer_bytes(c) * layer;
+  a.resid = static_cast<const uint16_t*>(c->resid) + resid_layer_elems(c) * layer;
+  a.out = out;
+  a.ws_ml = static_cast<float*>(ws);
+  a.ws_acc = a.ws_ml + (uint64_t)c->batch * c->n_kv_heads * (p.n_split + 1) * G * 2;
+  a.B = c->batch;
+  a.H = c->n_kv_heads;
+  a.G = G;
+  a.cap = c->capacity;
+  a.R = c->residual;
+  a.nq = p.nq;
+  a.n_tokens = n_tokens;
+  a.n_split = p.n_split;
+  a.blk_per_split = p.blk_per_split;
+  a.is_bf16 = c->dtype == RQ_BF16;
+  a.family = c->family;
+  a.qscale = scale * 1.4426950408889634f;
+  a.tab = layer_table(c, layer);
+  hipError_t e = rq::launch_attention(a, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "attention launch");
+  return ok();
+}
+
+rq_status rq_calibrate_workspace(int32_t n_comp, int32_t n_tokens,
+                                 int32_t n_bits, uint64_t* bytes) {
+  if (n_comp < 1 || n_tokens < rq::kChunk || n_tokens % rq::kChunk ||
+      n_bits < 1 || n_bits > 16 || !bytes)
+    return fail(RQ_EINVAL, "bad calibration shape (%d, %d, %d)", n_comp,
+                n_tokens, n_bits);
+  *bytes = (uint64_t)n_comp * n_bits * sizeof(double) *
+           ((uint64_t)n_tokens / rq::kChunk + 1);
+  return ok();
+}
+
+rq_status rq_calibrate_distortion(int32_t family, int32_t dtype, const void* x,
+                                  int32_t n_comp, int32_t n_tokens,
+                                  int32_t is_value, const int32_t* bits,
+                                  int32_t n_bits, double* mse, double* alpha,
+                                  double* beta, double* r2, void* ws,
+                                  uint64_t ws_bytes, rq_stream stream) {
+  if (family == RQ_TURBO)
+    return fail(RQ_EUNSUPPORTED, "TurboQuant family is not built in this library");
+  if (family != RQ_KIVI && family != RQ_QUAROT)
+    return fail(RQ_EINVAL, "unknown family %d", family);
+  if (dtype != RQ_F16 && dtype != RQ_BF16)
+    return fail(RQ_EINVAL, "unknown dtype %d", dtype);
+  uint64_t need = 0;
+  rq_status st = rq_calibrate_workspace(n_comp, n_tokens, n_bits, &need);
+  if (st != RQ_OK) return st;
+  if (!x || !bits || !mse || !ws) return fail(RQ_EINVAL, "NULL pointer");
+  if ((alpha || beta || r2) && n_bits < 2)
+    return fail(RQ_EINVAL, "the fit needs at least two bit-widths");
+  const int lo = family == RQ_QUAROT ? 2 : 1;
+  for (int j = 0; j < n_bits; ++j) {
+    if (bits[j] < lo || bits[j] > 8)
+      return fail(RQ_EINVAL, "bit-width %d outside %d..8", bits[j], lo);
+    for (int i = 0; i < j; ++i)
+      if (bits[i] == bits[j]) return fail(RQ_EINVAL, "repeated bit-width %d", bits[j]);
+  }
+  if (ws_bytes < need)
+    return fail(RQ_ESMALLWS, "workspace %llu bytes < %llu needed",
+                (unsigned long long)ws_bytes, (unsigned long long)need);
+  rq::CalibLaunch a{};
+  a.x = static_cast<const uint16_t*>(x);
+  a.mse = static_cast<double*>(ws);
+  a.partial = a.mse + (uint64_t)n_comp * n_bits;
+  a.n_comp = n_comp;
+  a.T = n_tokens;
+  a.n_bits = n_bits;
+  a.is_value = is_value != 0;
+  a.is_bf16 = dtype == RQ_BF16;
+  a.family = family;
+  for (int j = 0; j < n_bits; ++j) a.bits[j] = (uint8_t)bits[j];
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = rq::launch_calibrate(a, s);
+  if (e != hipSuccess) return hip_fail(e, "calibration launch");
+  e = hipMemcpyAsync(mse, a.mse, sizeof(double) * n_comp * n_bits,
+                     hipMemcpyDeviceToHost, s);
+  if (e != hipSuccess) return hip_fail(e, "calibration copy");
+  e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "calibration sync");
+  if (alpha || beta || r2) {
+    std::vector<double> al(n_comp), be(n_comp), rr(n_comp);
+    rq::fit_distortion(mse, n_comp, bits, n_bits, al.data(), be.data(), rr.data());
+    for (int i = 0; i < n_comp; ++i) {
+      bool pos = true;
+      for (int j = 0; j < n_bits; ++j) pos = pos && mse[(size_t)i * n_bits + j] > 0;
+      if (!pos) al[i] = be[i] = rr[i] = NAN;
+      if (alpha) alpha[i] = al[i];
+      if (beta) beta[i] = be[i];
+      if (r2) r2[i] = rr[i];
+    }
+  }
+  return ok();
+}
+
+rq_status rq_fit_distortion(const double* mse, int32_t n_comp,
+                            const int32_t* bits, int32_t n_bits, double* alpha,
+                            double* beta, double* r2) {
+  if (!mse || !bits || n_comp < 1 || n_bits < 2)
+    return fail(RQ_EINVAL, "need mse, bits, n_comp >= 1 and n_bits >= 2");
+  bool distinct = false;
+  for (int j = 1; j < n_bits; ++j) distinct = distinct || bits[j] != bits[0];
+  if (!distinct) return fail(RQ_EINVAL, "bit-widths must not all be equal");
+  for (int64_t i = 0; i < (int64_t)n_comp * n_bits; ++i)
+    if (!(mse[i] > 0) || !std::isfinite(mse[i]))
+      return fail(RQ_EINVAL, "mse[%lld] = %g is not a positive finite number",
+                  (long long)i, mse[i]);
+  rq::fit_distortion(mse, n_comp, bits, n_bits, alpha, beta, r2);
+  return ok();
+}
+
+rq_status rq_allocate_bits(int32_t n, const double* w, const double* alpha,
+                           const double* beta, double avg_bits, int32_t bmin,
+                           int32_t bmax, int32_t* bits_out,
+                           double* bits_cont_out, double* J_out) {
+  if (n < 1 || !w || !alpha || !beta || !bits_out)
+    return fail(RQ_EINVAL, "need n >= 1 and w, alpha, beta, bits_out");
+  if (bmin < 1 || bmax > 8 || bmin > bmax)
+    return fail(RQ_EINVAL, "bounds [%d, %d] must satisfy 1 <= bmin <= bmax <= 8",
+                bmin, bmax);
+  if (!std::isfinite(avg_bits)) return fail(RQ_EINVAL, "avg_bits not finite");
+  for (int i = 0; i < n; ++i) {
+    if (!(w[i] > 0) || !std::isfinite(w[i]) || !(alpha[i] > 0) ||
+        !std::isfinite(alpha[i]) || !(beta[i] > 1) || !std::isfinite(beta[i]))
+      return fail(RQ_EINVAL, "component %d: need w > 0, alpha > 0, beta > 1", i);
+  }
+  const int64_t B = rq::budget(n, avg_bits);
+  if (B < (int64_t)n * bmin || B > (int64_t)n * bmax)
+    return fail(RQ_EINFEASIBLE, "budget %lld outside [%lld, %lld]", (long long)B,
+                (long long)n * bmin, (long long)n * bmax);
+  rq::greedy(n, w, alpha, beta, B, bmin, bmax, bits_out);
+  if (bits_cont_out) rq::waterfill(n, w, alpha, beta, B, bmin, bmax, bits_cont_out);
+  if (J_out) {
+    double J = 0;
+    for (int i = 0; i < n; ++i) J += w[i] * alpha[i] * std::pow(beta[i], -(double)bits_out[i]);
+    *J_out = J;
+  }
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,74 @@
+// Internal declarations shared by the host library and the HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/rq.h"
+
+namespace rq {
+
+constexpr int kD = 128;          // head_dim
+constexpr int kChunk = 32;       // codes per packed chunk = tokens per block
+constexpr int kMetaBlockKivi = 512;   // bytes of KIVI metadata per block
+constexpr int kMetaBlockTok = 64;     // bytes of per-token metadata per block
+
+// Per-layer view of the bit table: byte offsets of each (head, kind) code
+// region and its bit-width.  Passed by value as a kernel argument, so a
+// kernel finds its head's width and region in O(1).
+struct LayerTable {
+  uint64_t code_off[RQ_MAX_KV_HEADS][2];
+  uint8_t bits[RQ_MAX_KV_HEADS][2];
+};
+
+struct QuantLaunch {
+  const uint16_t* k;      // [B][H][n_new][128]
+  const uint16_t* v;
+  uint8_t* codes;
+  uint8_t* meta;          // start of this layer's metadata
+  uint16_t* resid;        // start of this layer's residual rings
+  int B, H, n_new, n_past, cap, R;
+  int blk0, nblk;         // blocks [blk0, blk0 + nblk) get quantized
+  int is_bf16;
+  int family;
+  LayerTable tab;
+};
+
+struct RingLaunch {
+  const uint16_t* k;
+  const uint16_t* v;
+  uint16_t* resid;        // this layer's rings
+  int B, H, n_new, n_past, R;
+  int t_lo, t_hi;         // tokens [t_lo, t_hi) go to the window
+};
+
+struct AttnLaunch {
+  const uint16_t* q;      // [B][Hq][128]
+  const uint8_t* codes;
+  const uint8_t* meta;    // this layer
+  const uint16_t* resid;  // this layer
+  float* out;             // [B][Hq][128]
+  float* ws_ml;           // [B][H][S+1][G][2]   (max, sum)
+  float* ws_acc;          // [B][H][S+1][G][128]
+  int B, H, G, cap, R;
+  int nq, n_tokens;
+  int n_split, blk_per_split;
+  int is_bf16, family;
+  float qscale;           // scale * log2(e)
+  LayerTable tab;
+};
+
+struct CalibLaunch {
+  const uint16_t* x;      // [n_comp][T][128]
+  double* partial;        // [n_comp][n_blk][n_bits]
+  double* mse;            // [n_comp][n_bits]
+  int n_comp, T, n_bits, is_value, is_bf16, family;
+  uint8_t bits[16];
+};
+
+hipError_t launch_quantize(const QuantLaunch& a, hipStream_t s);
+hipError_t launch_ring(const RingLaunch& a, hipStream_t s);
+hipError_t launch_attention(const AttnLaunch& a, hipStream_t s);
+hipError_t launch_calibrate(const CalibLaunch& a, hipStream_t s);
+
+}  // namespace rq
