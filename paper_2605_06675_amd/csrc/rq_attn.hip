@@ -1,19 +1,20 @@
 // Decode attention over the packed mixed-bit cache.
 //
-// Grid (split group, kv-head, batch), four waves per workgroup sharing the
-// query rows in LDS; each wave is one split, a run of 32-token blocks of its
-// (batch, kv-head) unit:
+// Grid (workgroup slot, kv-head, batch), four waves per workgroup.  Slots
+// 0 .. n_wg-1 stream the quantized 32-token blocks of their (batch, kv-head)
+// unit; slot n_wg handles the 16-bit residual window.  Per block a wave:
 //   QK^T on MFMA 16x16x32 f16: A = dequantized keys (16 tokens x 32
-//   channels per lane-quarter), B = the G query rows of this kv-head;
+//   channels per lane quarter), B = the G query rows of this kv-head;
 //   online softmax in the log2 domain (scale * log2(e) folded into q);
 //   PV on MFMA 16x16x32 f16: A = probabilities (G rows x 32 tokens),
 //   B = dequantized values (32 tokens x 16 channels).
 // The packed format keeps codes i and i+16 of a chunk in one word, so a
 // word yields an fp16 pair with one mask, and the QK result registers are
-// already in the A layout PV needs (no shuffles between the two products).
-// The extra split index n_split handles the 16-bit residual window on VALU.
-// Each split writes (max, sum, acc) partials; a second kernel combines them
-// (and, for QuaRot, rotates the output back).
+// already in the A layout PV needs.  The next block's codes and metadata
+// are loaded while the current one is computed; metadata goes through LDS.
+// A workgroup merges its four waves in LDS and writes one partial
+// (max, sum, acc); the last workgroup of a unit (atomic ticket) merges the
+// unit's partials and writes the output (QuaRot: rotated back).
 #include "rq_device.h"
 #include "rq_internal.h"
 
@@ -22,6 +23,8 @@ namespace rq {
 namespace {
 
 constexpr int kWave = 64;
+constexpr int kWaves = 4;
+constexpr int kThreads = kWave * kWaves;
 constexpr float kInvSqrtD = 0.08838834764831845f;
 
 __device__ __forceinline__ h8 make_h8(uint32_t a, uint32_t b, uint32_t c,
@@ -34,213 +37,305 @@ __device__ __forceinline__ f4 mfma(h8 a, h8 b, f4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
 }
 
-template <int B>
-__device__ __forceinline__ void load_words(const uint32_t* p, uint32_t w[B]) {
-#pragma unroll
-  for (int i = 0; i < B; ++i) w[i] = p[i];
-}
-
-// Pairs i' = 0..3 (codes 4r+i' and 16+4r+i') of a chunk, reading only the
-// words lane-quarter r needs.
-template <int B>
-__device__ __forceinline__ void value_pairs(const uint32_t* chunk, int r,
-                                            uint32_t out[4]) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) out[i] = 0;
-  int wb = 0, o = 0;
-#pragma unroll
-  for (int p = 0; p < Planes<B>::n; ++p) {
-    const int w = Planes<B>::w[p];
-    const uint32_t m = ((1u << w) - 1u) * 0x00010001u;
-    if (w == 8) {
-      const uint32_t a = chunk[wb + 2 * r], b = chunk[wb + 2 * r + 1];
-      out[0] |= (a & m) << o;
-      out[1] |= ((a >> 8) & m) << o;
-      out[2] |= (b & m) << o;
-      out[3] |= ((b >> 8) & m) << o;
-    } else if (w == 4) {
-      const uint32_t a = chunk[wb + r];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) out[i] |= ((a >> (4 * i)) & m) << o;
-    } else if (w == 2) {
-      const uint32_t a = chunk[wb + (r >> 1)] >> (8 * (r & 1));
-#pragma unroll
-      for (int i = 0; i < 4; ++i) out[i] |= ((a >> (2 * i)) & m) << o;
-    } else {
-      const uint32_t a = chunk[wb] >> (4 * r);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) out[i] |= ((a >> i) & m) << o;
-    }
-    wb += w;
-    o += w;
-  }
-}
-
-struct KCtx {
-  const uint32_t* region;   // K code region of this (head), batch applied
-  const uint8_t* meta;      // K metadata of this unit
-  int r, m;                 // lane quarter, lane row
-};
-
-// QK^T of one 32-token block, KIVI keys: K_hat = u * s + z per channel.
-template <int B>
-__device__ __forceinline__ void qk_kivi(const KCtx& k, int blk, const h8 qb[4],
-                                        f4& S0, f4& S1) {
-  const u4* mp = reinterpret_cast<const u4*>(k.meta + (size_t)blk * kMetaBlockKivi +
-                                             k.r * 128);
-  uint32_t sp[16], zp[16];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const u4 a = mp[i], c = mp[4 + i];
-    sp[4 * i] = a.x; sp[4 * i + 1] = a.y; sp[4 * i + 2] = a.z; sp[4 * i + 3] = a.w;
-    zp[4 * i] = c.x; zp[4 * i + 1] = c.y; zp[4 * i + 2] = c.z; zp[4 * i + 3] = c.w;
-  }
-  const h2 off = {(_Float16)1024.0f, (_Float16)1024.0f};
-#pragma unroll
-  for (int tile = 0; tile < 2; ++tile) {
-    const int t = blk * kChunk + 16 * tile + k.m;
-    uint32_t w[B];
-    load_words<B>(k.region + ((size_t)t * 4 + k.r) * B, w);
-    f4 S = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      uint32_t x[4];
-#define RQ_KP(KK)                                                        \
-      {                                                                  \
-        const h2 u = codes_to_h2(pair_bits<B>(w, 4 * kb + KK), off);     \
-        x[KK] = as_u32(__builtin_elementwise_fma(                        \
-            u, as_h2(sp[4 * kb + KK]), as_h2(zp[4 * kb + KK])));         \
-      }
-      RQ_KP(0) RQ_KP(1) RQ_KP(2) RQ_KP(3)
-#undef RQ_KP
-      S = mfma(make_h8(x[0], x[1], x[2], x[3]), qb[kb], S);
-    }
-    if (tile == 0) S0 = S; else S1 = S;
-  }
-}
-
-// QK^T of one block, QuaRot keys: scores of token t scaled by s_t after the
-// product of q_rot with the integer levels (u - 2^(b-1)).
-template <int B>
-__device__ __forceinline__ void qk_quarot(const KCtx& k, int blk, const h8 qb[4],
-                                          f4& S0, f4& S1) {
-  const _Float16 o = (_Float16)(1024.0f + (float)(1 << (B - 1)));
-  const h2 off = {o, o};
-#pragma unroll
-  for (int tile = 0; tile < 2; ++tile) {
-    const int t = blk * kChunk + 16 * tile + k.m;
-    uint32_t w[B];
-    load_words<B>(k.region + ((size_t)t * 4 + k.r) * B, w);
-    f4 S = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      const uint32_t x0 = as_u32(codes_to_h2(pair_bits<B>(w, 4 * kb + 0), off));
-      const uint32_t x1 = as_u32(codes_to_h2(pair_bits<B>(w, 4 * kb + 1), off));
-      const uint32_t x2 = as_u32(codes_to_h2(pair_bits<B>(w, 4 * kb + 2), off));
-      const uint32_t x3 = as_u32(codes_to_h2(pair_bits<B>(w, 4 * kb + 3), off));
-      S = mfma(make_h8(x0, x1, x2, x3), qb[kb], S);
-    }
-    if (tile == 0) S0 = S; else S1 = S;
-  }
-  // per-token scales: dword (4r + i) of the block's pair-ordered scales
-  // holds (s[4r + i], s[16 + 4r + i])
-  const u4 sv = *reinterpret_cast<const u4*>(k.meta + (size_t)blk * kMetaBlockTok +
-                                             k.r * 16);
-  const uint32_t ss[4] = {sv.x, sv.y, sv.z, sv.w};
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const h2 s = as_h2(ss[i]);
-    S0[i] *= (float)s.x;
-    S1[i] *= (float)s.y;
-  }
-}
-
-struct VCtx {
-  const uint32_t* region;   // V code region of this head, batch applied
-  const uint8_t* meta;      // V metadata of this unit
-  int r, n;
-};
-
-template <int B>
-__device__ __forceinline__ void pv_kivi(const VCtx& v, int blk, const h8& P,
-                                        f4 acc[8]) {
-  const h2 off = {(_Float16)1024.0f, (_Float16)1024.0f};
-  const uint32_t* cb = v.region + (size_t)blk * kD * B;
-  const uint8_t* mb = v.meta + (size_t)blk * kMetaBlockKivi;
-#pragma unroll
-  for (int nt = 0; nt < 8; ++nt) {
-    const int c = 16 * nt + v.n, cg = nt >> 1;
-    const u4 s4 = *reinterpret_cast<const u4*>(mb + cg * 128 + v.r * 16);
-    const u4 z4 = *reinterpret_cast<const u4*>(mb + cg * 128 + 64 + v.r * 16);
-    const uint32_t sp[4] = {s4.x, s4.y, s4.z, s4.w};
-    const uint32_t zp[4] = {z4.x, z4.y, z4.z, z4.w};
-    uint32_t pr[4];
-    value_pairs<B>(cb + (size_t)c * B, v.r, pr);
-    uint32_t x[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const h2 u = codes_to_h2(pr[i], off);
-      x[i] = as_u32(__builtin_elementwise_fma(u, as_h2(sp[i]), as_h2(zp[i])));
-    }
-    acc[nt] = mfma(P, make_h8(x[0], x[1], x[2], x[3]), acc[nt]);
-  }
-}
-
-template <int B>
-__device__ __forceinline__ void pv_quarot(const VCtx& v, int blk, const h8& P,
-                                          f4 acc[8]) {
-  const _Float16 o = (_Float16)(1024.0f + (float)(1 << (B - 1)));
-  const h2 off = {o, o};
-  const uint32_t* cb = v.region + (size_t)blk * kD * B;
-#pragma unroll
-  for (int nt = 0; nt < 8; ++nt) {
-    const int c = 16 * nt + v.n;
-    uint32_t pr[4];
-    value_pairs<B>(cb + (size_t)c * B, v.r, pr);
-    acc[nt] = mfma(P,
-                   make_h8(as_u32(codes_to_h2(pr[0], off)),
-                           as_u32(codes_to_h2(pr[1], off)),
-                           as_u32(codes_to_h2(pr[2], off)),
-                           as_u32(codes_to_h2(pr[3], off))),
-                   acc[nt]);
-  }
-}
-
-#define RQ_DISPATCH8(bits, F, ...)          \
-  switch (bits) {                           \
-    case 1: F<1>(__VA_ARGS__); break;       \
-    case 2: F<2>(__VA_ARGS__); break;       \
-    case 3: F<3>(__VA_ARGS__); break;       \
-    case 4: F<4>(__VA_ARGS__); break;       \
-    case 5: F<5>(__VA_ARGS__); break;       \
-    case 6: F<6>(__VA_ARGS__); break;       \
-    case 7: F<7>(__VA_ARGS__); break;       \
-    default: F<8>(__VA_ARGS__); break;      \
-  }
-
 __device__ __forceinline__ float xor_shfl(float v, int mask) {
   return __shfl_xor(v, mask, kWave);
 }
 
-// Fills qs[j][c] (fp32, LDS) with the scaled (and, for QuaRot, rotated)
-// query rows of this kv-head; rows >= G are zero.  All threads of the
-// workgroup take part.
+// Words of a V chunk that lane quarter r needs, per plane: 2 for the 8-bit
+// plane, 1 otherwise.
+template <int B> struct VWords {
+  static constexpr int n = (B == 8) ? 2 : Planes<B>::n;
+};
+
+template <int BK> struct KStage {
+  uint32_t kw[2][BK];
+  u4 meta;
+};
+
+template <int BV> struct VStage {
+  uint32_t vw[8][VWords<BV>::n];
+};
+
+struct Ctx {
+  const uint32_t* kreg;   // K codes of this unit
+  const uint32_t* vreg;   // V codes of this unit
+  const uint8_t* kmeta;   // K metadata of this unit
+  const uint8_t* vmeta;   // V metadata of this unit
+  int per_blk;            // metadata bytes per block and kind
+  int r, col, lane;
+};
+
+// K words of the block (tiles 0/1: token 16*tile + col, chunk r) and this
+// lane's 16 bytes of the block metadata (lanes 0..31: K, 32..63: V).
+template <int BK>
+__device__ __forceinline__ void fetch_k(const Ctx& c, int blk, KStage<BK>& s) {
+#pragma unroll
+  for (int tile = 0; tile < 2; ++tile) {
+    const uint32_t* p = c.kreg + ((size_t)(blk * kChunk + 16 * tile + c.col) * 4 + c.r) * BK;
+#pragma unroll
+    for (int i = 0; i < BK; ++i) s.kw[tile][i] = p[i];
+  }
+  const int half = c.lane >> 5, i = c.lane & 31;
+  if (i * 16 < c.per_blk) {
+    const uint8_t* m = (half ? c.vmeta : c.kmeta) + (size_t)blk * c.per_blk + i * 16;
+    s.meta = *reinterpret_cast<const u4*>(m);
+  }
+}
+
+// V words lane quarter r needs from the chunks of channels 16*nt + col.
+template <int BV>
+__device__ __forceinline__ void fetch_v(const Ctx& c, int blk, VStage<BV>& s) {
+  const uint32_t* base = c.vreg + ((size_t)blk * kD + c.col) * BV;
+#pragma unroll
+  for (int nt = 0; nt < 8; ++nt) {
+    const uint32_t* ch = base + 16 * nt * BV;
+    int wb = 0, k = 0;
+#pragma unroll
+    for (int p = 0; p < Planes<BV>::n; ++p) {
+      const int w = Planes<BV>::w[p];
+      if (w == 8) {
+        s.vw[nt][k++] = ch[wb + 2 * c.r];
+        s.vw[nt][k++] = ch[wb + 2 * c.r + 1];
+      } else if (w == 4) {
+        s.vw[nt][k++] = ch[wb + c.r];
+      } else if (w == 2) {
+        s.vw[nt][k++] = ch[wb + (c.r >> 1)];
+      } else {
+        s.vw[nt][k++] = ch[wb];
+      }
+      wb += w;
+    }
+  }
+}
+
+// pairs i' = 0..3 (codes 4r+i' and 16+4r+i') of the lane's V chunk words
+template <int BV>
+__device__ __forceinline__ void vpairs(const uint32_t* vw, int r, uint32_t out[4]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) out[i] = 0;
+  int k = 0, o = 0;
+#pragma unroll
+  for (int p = 0; p < Planes<BV>::n; ++p) {
+    const int w = Planes<BV>::w[p];
+    const uint32_t m = ((1u << w) - 1u) * 0x00010001u;
+    if (w == 8) {
+      const uint32_t a = vw[k], b = vw[k + 1];
+      out[0] |= (a & m) << o;
+      out[1] |= ((a >> 8) & m) << o;
+      out[2] |= (b & m) << o;
+      out[3] |= ((b >> 8) & m) << o;
+      k += 2;
+    } else if (w == 4) {
+      const uint32_t a = vw[k++];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) out[i] |= ((a >> (4 * i)) & m) << o;
+    } else if (w == 2) {
+      const uint32_t a = vw[k++] >> (8 * (r & 1));
+#pragma unroll
+      for (int i = 0; i < 4; ++i) out[i] |= ((a >> (2 * i)) & m) << o;
+    } else {
+      const uint32_t a = vw[k++] >> (4 * r);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) out[i] |= ((a >> i) & m) << o;
+    }
+    o += w;
+  }
+}
+
+struct WaveState {
+  f4 acc[8];
+  float m_run, l_run;
+};
+
+// One block: QK^T, online softmax, PV.  mb = this wave's metadata in LDS
+// (u4 index 0.. = K metadata, 32.. = V metadata).
+template <int BK, int BV, bool QUAROT>
+__device__ __forceinline__ void block_step(const Ctx& c, KStage<BK>& s,
+                                           VStage<BV>& sv_, const u4* mb,
+                                           const u4* qb, WaveState& ws,
+                                           bool more, int nb) {
+  const int r = c.r;
+  f4 S0 = {0.f, 0.f, 0.f, 0.f}, S1 = {0.f, 0.f, 0.f, 0.f};
+  if (QUAROT) {
+    const _Float16 o = (_Float16)(1024.0f + (float)(1 << (BK - 1)));
+    const h2 off = {o, o};
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+#pragma unroll
+      for (int tile = 0; tile < 2; ++tile) {
+        uint32_t x[4];
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk)
+          x[kk] = as_u32(codes_to_h2(pair_bits<BK>(s.kw[tile], 4 * kb + kk), off));
+        const h8 qv = __builtin_bit_cast(h8, qb[kb * kWave]);
+        if (tile == 0) S0 = mfma(make_h8(x[0], x[1], x[2], x[3]), qv, S0);
+        else S1 = mfma(make_h8(x[0], x[1], x[2], x[3]), qv, S1);
+      }
+    }
+    const u4 sv = mb[r];
+    const uint32_t ss[4] = {sv.x, sv.y, sv.z, sv.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const h2 sc = as_h2(ss[i]);
+      S0[i] *= (float)sc.x;
+      S1[i] *= (float)sc.y;
+    }
+  } else {
+    const h2 off = {(_Float16)1024.0f, (_Float16)1024.0f};
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      const u4 s4 = mb[r * 8 + kb], z4 = mb[r * 8 + 4 + kb];
+      const uint32_t sp[4] = {s4.x, s4.y, s4.z, s4.w};
+      const uint32_t zp[4] = {z4.x, z4.y, z4.z, z4.w};
+#pragma unroll
+      for (int tile = 0; tile < 2; ++tile) {
+        uint32_t x[4];
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+          const h2 u = codes_to_h2(pair_bits<BK>(s.kw[tile], 4 * kb + kk), off);
+          x[kk] = as_u32(__builtin_elementwise_fma(u, as_h2(sp[kk]), as_h2(zp[kk])));
+        }
+        const h8 qv = __builtin_bit_cast(h8, qb[kb * kWave]);
+        if (tile == 0) S0 = mfma(make_h8(x[0], x[1], x[2], x[3]), qv, S0);
+        else S1 = mfma(make_h8(x[0], x[1], x[2], x[3]), qv, S1);
+      }
+    }
+  }
+  if (more) fetch_k<BK>(c, nb, s);
+  // online softmax, column col = query row j, tokens 4r+i and 16+4r+i
+  float mx = __builtin_fmaxf(S0[0], S1[0]);
+#pragma unroll
+  for (int i = 1; i < 4; ++i) mx = __builtin_fmaxf(mx, __builtin_fmaxf(S0[i], S1[i]));
+  mx = __builtin_fmaxf(mx, xor_shfl(mx, 16));
+  mx = __builtin_fmaxf(mx, xor_shfl(mx, 32));
+  const float mnew = __builtin_fmaxf(ws.m_run, mx);
+  const float alpha = __builtin_amdgcn_exp2f(ws.m_run - mnew);
+  ws.m_run = mnew;
+  float p0[4], p1[4], psum = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    p0[i] = __builtin_amdgcn_exp2f(S0[i] - mnew);
+    p1[i] = __builtin_amdgcn_exp2f(S1[i] - mnew);
+    psum += p0[i] + p1[i];
+  }
+  ws.l_run = ws.l_run * alpha + psum;
+  // rows 4r + i of the accumulator belong to query 4r + i
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float ar = __shfl(alpha, 4 * r + i, kWave);
+#pragma unroll
+    for (int nt = 0; nt < 8; ++nt) ws.acc[nt][i] *= ar;
+  }
+  uint32_t pp[4];
+  if (QUAROT) {
+    const u4 sv = mb[32 + r];
+    const uint32_t ss[4] = {sv.x, sv.y, sv.z, sv.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const h2 sc = as_h2(ss[i]);
+      const h2 pv = {(_Float16)(p0[i] * (float)sc.x), (_Float16)(p1[i] * (float)sc.y)};
+      pp[i] = as_u32(pv);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const h2 pv = {(_Float16)p0[i], (_Float16)p1[i]};
+      pp[i] = as_u32(pv);
+    }
+  }
+  const h8 P = make_h8(pp[0], pp[1], pp[2], pp[3]);
+  if (QUAROT) {
+    const _Float16 o = (_Float16)(1024.0f + (float)(1 << (BV - 1)));
+    const h2 off = {o, o};
+#pragma unroll
+    for (int nt = 0; nt < 8; ++nt) {
+      uint32_t pr[4];
+      vpairs<BV>(sv_.vw[nt], r, pr);
+      ws.acc[nt] = mfma(P,
+                        make_h8(as_u32(codes_to_h2(pr[0], off)),
+                                as_u32(codes_to_h2(pr[1], off)),
+                                as_u32(codes_to_h2(pr[2], off)),
+                                as_u32(codes_to_h2(pr[3], off))),
+                        ws.acc[nt]);
+    }
+  } else {
+    const h2 off = {(_Float16)1024.0f, (_Float16)1024.0f};
+#pragma unroll
+    for (int cg = 0; cg < 4; ++cg) {
+      const u4 s4 = mb[32 + cg * 8 + r], z4 = mb[32 + cg * 8 + 4 + r];
+      const uint32_t sp[4] = {s4.x, s4.y, s4.z, s4.w};
+      const uint32_t zp[4] = {z4.x, z4.y, z4.z, z4.w};
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const int nt = 2 * cg + half;
+        uint32_t pr[4], x[4];
+        vpairs<BV>(sv_.vw[nt], r, pr);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const h2 u = codes_to_h2(pr[i], off);
+          x[i] = as_u32(__builtin_elementwise_fma(u, as_h2(sp[i]), as_h2(zp[i])));
+        }
+        ws.acc[nt] = mfma(P, make_h8(x[0], x[1], x[2], x[3]), ws.acc[nt]);
+      }
+    }
+  }
+  if (more) fetch_v<BV>(c, nb, sv_);
+}
+
+template <int BK, int BV, bool QUAROT>
+__device__ __forceinline__ void stream_blocks(const Ctx& c, int blk_lo, int blk_hi,
+                                              u4* mb, const u4* qb, WaveState& ws) {
+  if (blk_lo >= blk_hi) return;
+  // Single-buffered pipeline: the next block's K words (+ metadata) are
+  // requested as soon as QK^T has consumed this block's, and its V words
+  // as soon as PV has consumed this block's.
+  KStage<BK> ks;
+  VStage<BV> vs;
+  fetch_k<BK>(c, blk_lo, ks);
+  fetch_v<BV>(c, blk_lo, vs);
+  for (int blk = blk_lo; blk < blk_hi; blk += kWaves) {
+    mb[c.lane] = ks.meta;
+    const int nb = blk + kWaves;
+    block_step<BK, BV, QUAROT>(c, ks, vs, mb, qb, ws, nb < blk_hi, nb);
+  }
+}
+
+template <bool QUAROT, int MAXB>
+__device__ void dispatch(int bk, int bv, const Ctx& c, int lo, int hi, u4* mb,
+                         const u4* qb, WaveState& ws) {
+#define RQ_CASE(K, V)                                                   \
+  case (K - 1) * 8 + (V - 1):                                           \
+    if (K <= MAXB && V <= MAXB)                                         \
+      stream_blocks<(K <= MAXB ? K : 1), (V <= MAXB ? V : 1), QUAROT>(   \
+          c, lo, hi, mb, qb, ws);                                       \
+    break;
+#define RQ_ROW(K) RQ_CASE(K, 1) RQ_CASE(K, 2) RQ_CASE(K, 3) RQ_CASE(K, 4) \
+                  RQ_CASE(K, 5) RQ_CASE(K, 6) RQ_CASE(K, 7) RQ_CASE(K, 8)
+  switch ((bk - 1) * 8 + (bv - 1)) {
+    RQ_ROW(1) RQ_ROW(2) RQ_ROW(3) RQ_ROW(4) RQ_ROW(5) RQ_ROW(6) RQ_ROW(7) RQ_ROW(8)
+    default: break;
+  }
+#undef RQ_ROW
+#undef RQ_CASE
+}
+
+// Scaled query rows of this kv-head into qs (rows >= G zero), rotated for
+// QuaRot.  Whole workgroup.
 __device__ void load_queries(const AttnLaunch& a, int b, int h, bool rotate,
                              float (*qs)[kD]) {
-  const int tid = threadIdx.x, nthr = blockDim.x;
-  for (int e = tid; e < 16 * kD; e += nthr) {
-    const int j = e / kD, c = e % kD;
+  const int tid = threadIdx.x;
+  for (int e = tid; e < 16 * kD; e += kThreads) {
+    const int j = e / kD, cc = e % kD;
     float v = 0.0f;
     if (j < a.G)
-      v = widen(a.q[((size_t)b * a.H * a.G + h * a.G + j) * kD + c], a.is_bf16);
-    qs[j][c] = v;
+      v = widen(a.q[((size_t)b * a.H * a.G + h * a.G + j) * kD + cc], a.is_bf16);
+    qs[j][cc] = v;
   }
   __syncthreads();
   float f = a.qscale;
   if (rotate) {
-    // q_rot = (1/sqrt(128)) H q (any butterfly order: attention tolerance)
     for (int hh = 1; hh < kD; hh *= 2) {
-      for (int e = tid; e < a.G * (kD / 2); e += nthr) {
+      for (int e = tid; e < a.G * (kD / 2); e += kThreads) {
         const int j = e / (kD / 2), i = e % (kD / 2);
         const int base = (i / hh) * 2 * hh + (i % hh);
         const float x = qs[j][base], y = qs[j][base + hh];
@@ -251,282 +346,241 @@ __device__ void load_queries(const AttnLaunch& a, int b, int h, bool rotate,
     }
     f *= kInvSqrtD;
   }
-  for (int e = tid; e < a.G * kD; e += nthr) qs[e / kD][e % kD] *= f;
+  for (int e = tid; e < a.G * kD; e += kThreads) qs[e / kD][e % kD] *= f;
   __syncthreads();
 }
 
-// 16-bit residual window on VALU, one wave: lane = token for the scores,
-// lane = channel pair for PV; probabilities move between lanes by shuffles.
-// qs holds the unrotated scaled queries.
-__device__ void residual_split(const AttnLaunch& a, int b, int h,
-                               const float (*qs)[kD], float* ml, float* accw) {
-  const int lane = threadIdx.x & (kWave - 1);
+// Partial of (unit, slot): float [G][2 + 128] = (max, sum, acc[128]).
+__device__ __forceinline__ float* part_ptr(const AttnLaunch& a, size_t unit,
+                                           int slot) {
+  return a.part + (unit * (a.n_wg + 1) + slot) * (size_t)a.G * (2 + kD);
+}
+
+// 16-bit residual window of one unit, original domain; wave w takes query
+// rows w, w+4, ...; lane = token for scores, lane = channel pair for PV.
+__device__ void residual_slot(const AttnLaunch& a, int b, int h,
+                              const float (*qs)[kD], float* dst) {
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x & (kWave - 1);
   const int cap = a.R + kChunk;
-  float m_run[16], l_run[16], ac[16][2];
-#pragma unroll
-  for (int j = 0; j < 16; ++j) {
-    m_run[j] = -INFINITY;
-    l_run[j] = 0.0f;
-    ac[j][0] = ac[j][1] = 0.0f;
-  }
-  const uint16_t* kbase = a.resid + (((size_t)b * a.H + h) * 2 + 0) * cap * kD;
-  const uint16_t* vbase = a.resid + (((size_t)b * a.H + h) * 2 + 1) * cap * kD;
-  for (int t0 = a.nq; t0 < a.n_tokens; t0 += kWave) {
-    const int t = t0 + lane;
-    const bool ok = t < a.n_tokens;
-    float s[16];
-#pragma unroll
-    for (int j = 0; j < 16; ++j) s[j] = 0.0f;
-    if (ok) {
-      const uint16_t* kr = kbase + (size_t)(t % cap) * kD;
-      for (int c = 0; c < kD; c += 2) {
-        const uint32_t w = *reinterpret_cast<const uint32_t*>(kr + c);
-        const float k0 = widen(w & 0xffffu, a.is_bf16);
-        const float k1 = widen(w >> 16, a.is_bf16);
-#pragma unroll
-        for (int j = 0; j < 16; ++j)
-          s[j] = __builtin_fmaf(qs[j][c + 1], k1, __builtin_fmaf(qs[j][c], k0, s[j]));
-      }
-    }
-    float p[16];
-#pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      p[j] = 0.0f;
-      if (j < a.G) {
-        float mx = ok ? s[j] : -INFINITY;
-        for (int d = 32; d >= 1; d >>= 1) mx = __builtin_fmaxf(mx, xor_shfl(mx, d));
-        const float mn = __builtin_fmaxf(m_run[j], mx);
-        const float al = __builtin_amdgcn_exp2f(m_run[j] - mn);
-        p[j] = ok ? __builtin_amdgcn_exp2f(s[j] - mn) : 0.0f;
-        float sum = p[j];
-        for (int d = 32; d >= 1; d >>= 1) sum += xor_shfl(sum, d);
-        l_run[j] = l_run[j] * al + sum;
-        m_run[j] = mn;
-        ac[j][0] *= al;
-        ac[j][1] *= al;
-      }
-    }
-    const int n = (a.n_tokens - t0) < kWave ? (a.n_tokens - t0) : kWave;
-    for (int i = 0; i < n; ++i) {
-      const uint16_t* vr = vbase + (size_t)((t0 + i) % cap) * kD;
-      const uint32_t w = *reinterpret_cast<const uint32_t*>(vr + 2 * lane);
-      const float v0 = widen(w & 0xffffu, a.is_bf16);
-      const float v1 = widen(w >> 16, a.is_bf16);
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        if (j < a.G) {
-          const float pj = __shfl(p[j], i, kWave);
-          ac[j][0] = __builtin_fmaf(pj, v0, ac[j][0]);
-          ac[j][1] = __builtin_fmaf(pj, v1, ac[j][1]);
+  const uint16_t* kb = a.resid + (((size_t)b * a.H + h) * 2 + 0) * cap * kD;
+  const uint16_t* vb = a.resid + (((size_t)b * a.H + h) * 2 + 1) * cap * kD;
+  for (int j = wave; j < a.G; j += kWaves) {
+    float m_run = -INFINITY, l_run = 0.0f, ac0 = 0.0f, ac1 = 0.0f;
+    for (int t0 = a.nq; t0 < a.n_tokens; t0 += kWave) {
+      const int t = t0 + lane;
+      const bool ok = t < a.n_tokens;
+      float s = -INFINITY;
+      if (ok) {
+        const uint16_t* kr = kb + (size_t)(t % cap) * kD;
+        s = 0.0f;
+        for (int cc = 0; cc < kD; cc += 2) {
+          const uint32_t w = *reinterpret_cast<const uint32_t*>(kr + cc);
+          s = __builtin_fmaf(qs[j][cc], widen(w & 0xffffu, a.is_bf16), s);
+          s = __builtin_fmaf(qs[j][cc + 1], widen(w >> 16, a.is_bf16), s);
         }
       }
-    }
-  }
-#pragma unroll
-  for (int j = 0; j < 16; ++j) {
-    if (j < a.G) {
-      accw[j * kD + 2 * lane] = ac[j][0];
-      accw[j * kD + 2 * lane + 1] = ac[j][1];
-      if (lane == 0) {
-        ml[2 * j] = m_run[j];
-        ml[2 * j + 1] = l_run[j];
+      float mx = s;
+      for (int d = 32; d >= 1; d >>= 1) mx = __builtin_fmaxf(mx, xor_shfl(mx, d));
+      const float mn = __builtin_fmaxf(m_run, mx);
+      const float al = __builtin_amdgcn_exp2f(m_run - mn);
+      const float p = ok ? __builtin_amdgcn_exp2f(s - mn) : 0.0f;
+      float sum = p;
+      for (int d = 32; d >= 1; d >>= 1) sum += xor_shfl(sum, d);
+      l_run = l_run * al + sum;
+      m_run = mn;
+      ac0 *= al;
+      ac1 *= al;
+      const int n = (a.n_tokens - t0) < kWave ? (a.n_tokens - t0) : kWave;
+      for (int i = 0; i < n; ++i) {
+        const uint32_t w = *reinterpret_cast<const uint32_t*>(
+            vb + (size_t)((t0 + i) % cap) * kD + 2 * lane);
+        const float pi = __shfl(p, i, kWave);
+        ac0 = __builtin_fmaf(pi, widen(w & 0xffffu, a.is_bf16), ac0);
+        ac1 = __builtin_fmaf(pi, widen(w >> 16, a.is_bf16), ac1);
       }
     }
+    float* d = dst + (size_t)j * (2 + kD);
+    if (lane == 0) {
+      d[0] = m_run;
+      d[1] = l_run;
+    }
+    d[2 + 2 * lane] = ac0;
+    d[2 + 2 * lane + 1] = ac1;
   }
 }
 
-constexpr int kWavesPerBlock = 4;
-
-__global__ void __launch_bounds__(kWave * kWavesPerBlock)
+// MAXB: largest bit-width the kernel handles (4: the common {1..4} range,
+// compiled for four resident waves per SIMD; 8: every width).
+template <int MAXB>
+__global__ void __launch_bounds__(kThreads, MAXB <= 4 ? 4 : 2)
 attn_kernel(AttnLaunch a) {
   __shared__ float qs[16][kD];
-  const int h = blockIdx.y, b = blockIdx.z;
-  const int wave = threadIdx.x / kWave, lane = threadIdx.x & (kWave - 1);
-  const int split = blockIdx.x * kWavesPerBlock + wave;
+  __shared__ u4 mbuf[kWaves][kWave];
+  __shared__ u4 qbuf[4][kWave];      // QK B operand per (K-block, lane)
+  __shared__ int last_flag;
+  extern __shared__ float merge[];   // [kWaves][G][2 + 128]
+  const int slot = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid & (kWave - 1);
   const size_t unit = (size_t)b * a.H + h;
-  const size_t part = unit * (a.n_split + 1) + split;
-  float* ml = a.ws_ml + part * a.G * 2;
-  float* accw = a.ws_acc + part * a.G * kD;
-
-  // Only the workgroup holding the residual split needs plain queries; the
-  // window holds unrotated tokens.
-  const int last_wg = a.n_split / kWavesPerBlock;
-  const bool has_resid = (int)blockIdx.x == last_wg;
   const bool quarot = a.family == RQ_QUAROT;
-  if (has_resid && quarot) {
+  const int G = a.G;
+
+  if (slot == a.n_wg) {
     load_queries(a, b, h, false, qs);
-    if (split == a.n_split) residual_split(a, b, h, qs, ml, accw);
-    __syncthreads();
-    load_queries(a, b, h, true, qs);
+    residual_slot(a, b, h, qs, part_ptr(a, unit, slot));
   } else {
     load_queries(a, b, h, quarot, qs);
-    if (split == a.n_split) residual_split(a, b, h, qs, ml, accw);
-  }
-  if (split >= a.n_split) return;
-
-  const int r = lane >> 4, col = lane & 15;
-  // B operand of QK: column j = col, k-slots of quarter r, K-block kb:
-  // channels 32r + (4kb + k') and 32r + 16 + (4kb + k'), k' = 0..3.
-  h8 qb[4];
+    const int r = lane >> 4, col = lane & 15;
+    // B operand of QK: column j = col, k-slots of quarter r, K-block kb:
+    // channels 32r + 4kb + k' and 32r + 16 + 4kb + k', k' = 0..3
+    if (wave == 0) {
 #pragma unroll
-  for (int kb = 0; kb < 4; ++kb) {
-    uint32_t x[4];
+      for (int kb = 0; kb < 4; ++kb) {
+        uint32_t x[4];
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const int c0 = 32 * r + 4 * kb + kk;
-      const h2 v = {(_Float16)qs[col][c0], (_Float16)qs[col][c0 + 16]};
-      x[kk] = as_u32(v);
-    }
-    qb[kb] = make_h8(x[0], x[1], x[2], x[3]);
-  }
-
-  const int bk = a.tab.bits[h][0], bv = a.tab.bits[h][1];
-  const int nblk_cap = a.cap / kChunk;
-  const int per_blk = quarot ? kMetaBlockTok : kMetaBlockKivi;
-  KCtx kc;
-  kc.region = reinterpret_cast<const uint32_t*>(a.codes + a.tab.code_off[h][0]) +
-              (size_t)b * a.cap * 4 * bk;
-  kc.meta = a.meta + (((size_t)h * 2 + 0) * a.B + b) * nblk_cap * per_blk;
-  kc.r = r;
-  kc.m = col;
-  VCtx vc;
-  vc.region = reinterpret_cast<const uint32_t*>(a.codes + a.tab.code_off[h][1]) +
-              (size_t)b * nblk_cap * kD * bv;
-  vc.meta = a.meta + (((size_t)h * 2 + 1) * a.B + b) * nblk_cap * per_blk;
-  vc.r = r;
-  vc.n = col;
-
-  f4 acc[8];
-#pragma unroll
-  for (int nt = 0; nt < 8; ++nt) acc[nt] = (f4){0.f, 0.f, 0.f, 0.f};
-  float m_run = -INFINITY, l_run = 0.0f;
-
-  const int nblk = a.nq / kChunk;
-  const int blk_lo = split * a.blk_per_split;
-  int blk_hi = blk_lo + a.blk_per_split;
-  if (blk_hi > nblk) blk_hi = nblk;
-
-  for (int blk = blk_lo; blk < blk_hi; ++blk) {
-    f4 S0, S1;
-    if (quarot) {
-      RQ_DISPATCH8(bk, qk_quarot, kc, blk, qb, S0, S1)
-    } else {
-      RQ_DISPATCH8(bk, qk_kivi, kc, blk, qb, S0, S1)
-    }
-    // online softmax for column col (query j = col), tokens 4r+i, 16+4r+i
-    float mx = S0[0];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) mx = __builtin_fmaxf(mx, __builtin_fmaxf(S0[i], S1[i]));
-    mx = __builtin_fmaxf(mx, xor_shfl(mx, 16));
-    mx = __builtin_fmaxf(mx, xor_shfl(mx, 32));
-    const float mnew = __builtin_fmaxf(m_run, mx);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - mnew);
-    m_run = mnew;
-    float p0[4], p1[4], psum = 0.0f;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      p0[i] = __builtin_amdgcn_exp2f(S0[i] - mnew);
-      p1[i] = __builtin_amdgcn_exp2f(S1[i] - mnew);
-      psum += p0[i] + p1[i];
-    }
-    l_run = l_run * alpha + psum;
-    // rescale accumulator rows 4r + i by alpha of column 4r + i
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float ar = __shfl(alpha, 4 * r + i, kWave);
-#pragma unroll
-      for (int nt = 0; nt < 8; ++nt) acc[nt][i] *= ar;
-    }
-    uint32_t pp[4];
-    if (quarot) {
-      const u4 sv = *reinterpret_cast<const u4*>(vc.meta + (size_t)blk * kMetaBlockTok +
-                                                 r * 16);
-      const uint32_t ss[4] = {sv.x, sv.y, sv.z, sv.w};
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const h2 s = as_h2(ss[i]);
-        const h2 pv = {(_Float16)(p0[i] * (float)s.x), (_Float16)(p1[i] * (float)s.y)};
-        pp[i] = as_u32(pv);
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const h2 pv = {(_Float16)p0[i], (_Float16)p1[i]};
-        pp[i] = as_u32(pv);
+        for (int kk = 0; kk < 4; ++kk) {
+          const int c0 = 32 * r + 4 * kb + kk;
+          const h2 v = {(_Float16)qs[col][c0], (_Float16)qs[col][c0 + 16]};
+          x[kk] = as_u32(v);
+        }
+        qbuf[kb][lane] = (u4){x[0], x[1], x[2], x[3]};
       }
     }
-    const h8 P = make_h8(pp[0], pp[1], pp[2], pp[3]);
-    if (quarot) {
-      RQ_DISPATCH8(bv, pv_quarot, vc, blk, P, acc)
-    } else {
-      RQ_DISPATCH8(bv, pv_kivi, vc, blk, P, acc)
-    }
-  }
-  // partial sums of l over the 4 lane quarters
-  l_run += xor_shfl(l_run, 16);
-  l_run += xor_shfl(l_run, 32);
-  if (r == 0 && col < a.G) {
-    ml[2 * col] = m_run;
-    ml[2 * col + 1] = l_run;
-  }
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int j = 4 * r + i;
-    if (j < a.G) {
-#pragma unroll
-      for (int nt = 0; nt < 8; ++nt) accw[j * kD + 16 * nt + col] = acc[nt][i];
-    }
-  }
-}
-
-__global__ void __launch_bounds__(kD)
-combine_kernel(AttnLaunch a) {
-  __shared__ float o[kD];
-  const int bq = blockIdx.x;               // b * Hq + hq
-  const int b = bq / (a.H * a.G), hq = bq % (a.H * a.G);
-  const int h = hq / a.G, j = hq % a.G;
-  const int c = threadIdx.x;
-  const size_t unit = (size_t)b * a.H + h;
-  const int ns = a.n_split + 1;
-  float M = -INFINITY;
-  for (int s = 0; s < ns; ++s) {
-    const float* ml = a.ws_ml + ((unit * ns + s) * a.G + j) * 2;
-    M = __builtin_fmaxf(M, ml[0]);
-  }
-  float num = 0.0f, den = 0.0f, numr = 0.0f;
-  for (int s = 0; s < ns; ++s) {
-    const float* ml = a.ws_ml + ((unit * ns + s) * a.G + j) * 2;
-    const float w = (ml[1] > 0.0f) ? __builtin_amdgcn_exp2f(ml[0] - M) : 0.0f;
-    const float v = a.ws_acc[((unit * ns + s) * a.G + j) * kD + c];
-    if (s == a.n_split) numr += w * v; else num += w * v;
-    den += w * ml[1];
-  }
-  float res = num;
-  if (a.family == RQ_QUAROT) {
-    // quantized part is in the rotated domain: out = (1/sqrt(128)) H acc
-    o[c] = num;
     __syncthreads();
+    const u4* qb = &qbuf[0][lane];
+    const int bk = a.tab.bits[h][0], bv = a.tab.bits[h][1];
+    const int nblk_cap = a.cap / kChunk;
+    Ctx c;
+    c.per_blk = quarot ? kMetaBlockTok : kMetaBlockKivi;
+    c.kreg = reinterpret_cast<const uint32_t*>(a.codes + a.tab.code_off[h][0]) +
+             (size_t)b * a.cap * 4 * bk;
+    c.vreg = reinterpret_cast<const uint32_t*>(a.codes + a.tab.code_off[h][1]) +
+             (size_t)b * nblk_cap * kD * bv;
+    c.kmeta = a.meta + (((size_t)h * 2 + 0) * a.B + b) * nblk_cap * c.per_blk;
+    c.vmeta = a.meta + (((size_t)h * 2 + 1) * a.B + b) * nblk_cap * c.per_blk;
+    c.r = r;
+    c.col = col;
+    c.lane = lane;
+    WaveState ws;
+#pragma unroll
+    for (int nt = 0; nt < 8; ++nt) ws.acc[nt] = (f4){0.f, 0.f, 0.f, 0.f};
+    ws.m_run = -INFINITY;
+    ws.l_run = 0.0f;
+    const int nblk = a.nq / kChunk;
+    const int lo = slot * a.blk_per_wg;
+    int hi = lo + a.blk_per_wg;
+    if (hi > nblk) hi = nblk;
+    if (quarot)
+      dispatch<true, MAXB>(bk, bv, c, lo + wave, hi, mbuf[wave], qb, ws);
+    else
+      dispatch<false, MAXB>(bk, bv, c, lo + wave, hi, mbuf[wave], qb, ws);
+    ws.l_run += xor_shfl(ws.l_run, 16);
+    ws.l_run += xor_shfl(ws.l_run, 32);
+    // merge the four waves in LDS
+    float* mw = merge + (size_t)wave * G * (2 + kD);
+    if (r == 0 && col < G) {
+      mw[col * (2 + kD)] = ws.m_run;
+      mw[col * (2 + kD) + 1] = ws.l_run;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int j = 4 * r + i;
+      if (j < G) {
+#pragma unroll
+        for (int nt = 0; nt < 8; ++nt) mw[j * (2 + kD) + 2 + 16 * nt + col] = ws.acc[nt][i];
+      }
+    }
+    __syncthreads();
+    float* dst = part_ptr(a, unit, slot);
+    for (int e = tid; e < G * kD; e += kThreads) {
+      const int j = e / kD, cc = e % kD;
+      float M = -INFINITY;
+      for (int w = 0; w < kWaves; ++w) M = __builtin_fmaxf(M, merge[(w * G + j) * (2 + kD)]);
+      float acc = 0.0f, l = 0.0f;
+      for (int w = 0; w < kWaves; ++w) {
+        const float* src = merge + (size_t)(w * G + j) * (2 + kD);
+        const float f = (M == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(src[0] - M);
+        acc = __builtin_fmaf(f, src[2 + cc], acc);
+        l = __builtin_fmaf(f, src[1], l);
+      }
+      dst[j * (2 + kD) + 2 + cc] = acc;
+      if (cc == 0) {
+        dst[j * (2 + kD)] = M;
+        dst[j * (2 + kD) + 1] = l;
+      }
+    }
+  }
+
+  // ticket: the last of the n_wg + 1 workgroups of this unit combines
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  __syncthreads();
+  if (tid == 0) {
+    const unsigned t = atomicAdd(a.counters + unit, 1u);
+    last_flag = (t == (unsigned)a.n_wg);
+  }
+  __syncthreads();
+  if (!last_flag) return;
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+
+  float* rot = &qs[0][0];   // [G <= 16][128] scratch for the back-rotation
+  const int ns = a.n_wg + 1;
+  for (int e = tid; e < G * kD; e += kThreads) {
+    const int j = e / kD, cc = e % kD;
+    float M = -INFINITY;
+    for (int s = 0; s < ns; ++s) M = __builtin_fmaxf(M, part_ptr(a, unit, s)[j * (2 + kD)]);
+    float num = 0.0f, numr = 0.0f, den = 0.0f;
+    for (int s = 0; s < ns; ++s) {
+      const float* src = part_ptr(a, unit, s) + j * (2 + kD);
+      const float f = (src[1] > 0.0f) ? __builtin_amdgcn_exp2f(src[0] - M) : 0.0f;
+      if (s == a.n_wg) numr = f * src[2 + cc];
+      else num = __builtin_fmaf(f, src[2 + cc], num);
+      den = __builtin_fmaf(f, src[1], den);
+    }
+    rot[j * kD + cc] = num;
+    merge[j * kD + cc] = numr / den;
+    merge[G * kD + j * kD + cc] = 1.0f / den;
+  }
+  __syncthreads();
+  if (quarot) {
     for (int hh = 1; hh < kD; hh *= 2) {
-      float x = 0.0f;
-      const int partner = c ^ hh;
-      x = (c & hh) ? (o[partner] - o[c]) : (o[c] + o[partner]);
-      __syncthreads();
-      o[c] = x;
+      for (int e = tid; e < G * (kD / 2); e += kThreads) {
+        const int j = e / (kD / 2), i = e % (kD / 2);
+        const int base = (i / hh) * 2 * hh + (i % hh);
+        const float x = rot[j * kD + base], y = rot[j * kD + base + hh];
+        rot[j * kD + base] = x + y;
+        rot[j * kD + base + hh] = x - y;
+      }
       __syncthreads();
     }
-    res = o[c] * kInvSqrtD;
   }
-  a.out[(size_t)bq * kD + c] = (res + numr) / den;
+  const float f = quarot ? kInvSqrtD : 1.0f;
+  for (int e = tid; e < G * kD; e += kThreads) {
+    const int j = e / kD, cc = e % kD;
+    a.out[((size_t)b * a.H * G + h * G + j) * kD + cc] =
+        rot[e] * f * merge[G * kD + e] + merge[e];
+  }
+  if (tid == 0) atomicExch(a.counters + unit, 0u);
 }
 
 }  // namespace
 
+size_t attention_lds_bytes(int G) {
+  size_t merge = (size_t)kWaves * G * (2 + kD) * sizeof(float);
+  size_t fin = (size_t)2 * G * kD * sizeof(float);
+  return merge > fin ? merge : fin;
+}
+
 hipError_t launch_attention(const AttnLaunch& a, hipStream_t s) {
-  dim3 grid((a.n_split + kWavesPerBlock) / kWavesPerBlock, a.H, a.B);
-  hipLaunchKernelGGL(attn_kernel, grid, dim3(kWave * kWavesPerBlock), 0, s, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(combine_kernel, dim3(a.B * a.H * a.G), dim3(kD), 0, s, a);
+  dim3 grid(a.n_wg + 1, a.H, a.B);
+  int maxb = 1;
+  for (int h = 0; h < a.H; ++h)
+    for (int k = 0; k < 2; ++k) maxb = a.tab.bits[h][k] > maxb ? a.tab.bits[h][k] : maxb;
+  if (maxb <= 4)
+    hipLaunchKernelGGL(attn_kernel<4>, grid, dim3(kThreads),
+                       attention_lds_bytes(a.G), s, a);
+  else
+    hipLaunchKernelGGL(attn_kernel<8>, grid, dim3(kThreads),
+                       attention_lds_bytes(a.G), s, a);
   return hipGetLastError();
 }
 

@@ -115,32 +115,44 @@ rq::LayerTable layer_table(const rq_cache* c, int layer) {
 }
 
 struct SplitPlan {
-  int nq, n_split, blk_per_split;
+  int nq, n_wg, blk_per_wg;
 };
 
+// Workgroups (four waves each) per (batch, kv-head) unit: enough to give
+// every CU several resident workgroups, each streaming a contiguous run of
+// 32-token blocks.
 SplitPlan plan_splits(const rq_cache* c, int n_tokens) {
   SplitPlan p;
   p.nq = n_quantized(n_tokens, c->residual);
-  const int nblk = p.nq / rq::kChunk;
+  const long nblk = p.nq / rq::kChunk;
   const long units = (long)c->batch * c->n_kv_heads;
-  long want = 4;
-  const char* env = std::getenv("RQ_ATTN_BLOCKS_PER_SPLIT");
+  long per = 0;
+  const char* env = std::getenv("RQ_ATTN_WG_BLOCKS");
   if (env && std::atoi(env) > 0) {
-    want = std::atoi(env);
+    per = std::atoi(env);
   } else {
+    const long target_wg = 1536;
     const long total = units * nblk;
-    const long per = (total + 6143) / 6144;
-    if (per > want) want = per;
+    per = (total + target_wg - 1) / target_wg;
+    if (per < 16) per = 16;
+    per = (per + 3) / 4 * 4;
   }
-  p.blk_per_split = (int)want;
-  p.n_split = nblk == 0 ? 0 : (nblk + p.blk_per_split - 1) / p.blk_per_split;
+  p.blk_per_wg = (int)per;
+  p.n_wg = nblk == 0 ? 0 : (int)((nblk + per - 1) / per);
   return p;
+}
+
+constexpr uint64_t kCounterBytes = 256;  // alignment of the partials
+
+uint64_t counter_bytes(const rq_cache* c) {
+  const uint64_t n = (uint64_t)c->batch * c->n_kv_heads * sizeof(uint32_t);
+  return (n + kCounterBytes - 1) / kCounterBytes * kCounterBytes;
 }
 
 uint64_t attn_ws_bytes(const rq_cache* c, const SplitPlan& p) {
   const uint64_t G = c->n_q_heads / c->n_kv_heads;
-  const uint64_t parts = (uint64_t)c->batch * c->n_kv_heads * (p.n_split + 1);
-  return parts * G * (2 + rq::kD) * sizeof(float);
+  const uint64_t parts = (uint64_t)c->batch * c->n_kv_heads * (p.n_wg + 1);
+  return counter_bytes(c) + parts * G * (2 + rq::kD) * sizeof(float);
 }
 
 }  // namespace
@@ -262,8 +274,8 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
   a.meta = static_cast<const uint8_t*>(c->meta) + meta_layer_bytes(c) * layer;
   a.resid = static_cast<const uint16_t*>(c->resid) + resid_layer_elems(c) * layer;
   a.out = out;
-  a.ws_ml = static_cast<float*>(ws);
-  a.ws_acc = a.ws_ml + (uint64_t)c->batch * c->n_kv_heads * (p.n_split + 1) * G * 2;
+  a.counters = static_cast<uint32_t*>(ws);
+  a.part = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + counter_bytes(c));
   a.B = c->batch;
   a.H = c->n_kv_heads;
   a.G = G;
@@ -271,8 +283,8 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
   a.R = c->residual;
   a.nq = p.nq;
   a.n_tokens = n_tokens;
-  a.n_split = p.n_split;
-  a.blk_per_split = p.blk_per_split;
+  a.n_wg = p.n_wg;
+  a.blk_per_wg = p.blk_per_wg;
   a.is_bf16 = c->dtype == RQ_BF16;
   a.family = c->family;
   a.qscale = scale * 1.4426950408889634f;

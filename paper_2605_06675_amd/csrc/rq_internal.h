@@ -48,11 +48,11 @@ struct AttnLaunch {
   const uint8_t* meta;    // this layer
   const uint16_t* resid;  // this layer
   float* out;             // [B][Hq][128]
-  float* ws_ml;           // [B][H][S+1][G][2]   (max, sum)
-  float* ws_acc;          // [B][H][S+1][G][128]
+  uint32_t* counters;     // [B][H] tickets, zero between calls
+  float* part;            // [B][H][n_wg + 1][G][2 + 128] (max, sum, acc)
   int B, H, G, cap, R;
   int nq, n_tokens;
-  int n_split, blk_per_split;
+  int n_wg, blk_per_wg;   // workgroups per unit streaming blocks
   int is_bf16, family;
   float qscale;           // scale * log2(e)
   LayerTable tab;
