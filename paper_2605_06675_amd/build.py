@@ -36,11 +36,32 @@ def _compile(src):
     return obj
 
 
+def _check_no_calls(src):
+    """Kernels must be call-free: device functions are force-inlined (a
+    called function that needs long-branch relaxation may reuse its
+    return-address registers).  Compile to device assembly and reject any
+    call instruction."""
+    asm = os.path.join(BUILD, os.path.splitext(src)[0] + ".s")
+    cmd = [HIPCC, *COMMON, "--cuda-device-only", "-S", os.path.join(CSRC, src),
+           "-o", asm]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc -S failed for {src}:\n{r.stderr}")
+    with open(asm) as f:
+        if "s_swappc" in f.read():
+            raise RuntimeError(f"{src}: device code contains a function call")
+    return asm
+
+
 def build(verbose=False):
     """Compile every source and link librq.so (always rebuilds)."""
     os.makedirs(BUILD, exist_ok=True)
-    with concurrent.futures.ThreadPoolExecutor(len(SOURCES)) as ex:
+    hip = [s for s in SOURCES if s.endswith(".hip")]
+    with concurrent.futures.ThreadPoolExecutor(len(SOURCES) + len(hip)) as ex:
+        checks = [ex.submit(_check_no_calls, s) for s in hip]
         objs = list(ex.map(_compile, SOURCES))
+        for c in checks:
+            c.result()
     tmp = OUT + ".tmp"
     cmd = [HIPCC, "-shared", "-fPIC", "--offload-arch=gfx950", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -301,7 +301,7 @@ __device__ __forceinline__ void stream_blocks(const Ctx& c, int blk_lo, int blk_
 }
 
 template <bool QUAROT, int MAXB>
-__device__ void dispatch(int bk, int bv, const Ctx& c, int lo, int hi, u4* mb,
+__device__ __forceinline__ void dispatch(int bk, int bv, const Ctx& c, int lo, int hi, u4* mb,
                          const u4* qb, WaveState& ws) {
 #define RQ_CASE(K, V)                                                   \
   case (K - 1) * 8 + (V - 1):                                           \
@@ -321,7 +321,7 @@ __device__ void dispatch(int bk, int bv, const Ctx& c, int lo, int hi, u4* mb,
 
 // Scaled query rows of this kv-head into qs (rows >= G zero), rotated for
 // QuaRot.  Whole workgroup.
-__device__ void load_queries(const AttnLaunch& a, int b, int h, bool rotate,
+__device__ __forceinline__ void load_queries(const AttnLaunch& a, int b, int h, bool rotate,
                              float (*qs)[kD]) {
   const int tid = threadIdx.x;
   for (int e = tid; e < 16 * kD; e += kThreads) {
@@ -358,7 +358,7 @@ __device__ __forceinline__ float* part_ptr(const AttnLaunch& a, size_t unit,
 
 // 16-bit residual window of one unit, original domain; wave w takes query
 // rows w, w+4, ...; lane = token for scores, lane = channel pair for PV.
-__device__ void residual_slot(const AttnLaunch& a, int b, int h,
+__device__ __forceinline__ void residual_slot(const AttnLaunch& a, int b, int h,
                               const float (*qs)[kD], float* dst) {
   const int wave = threadIdx.x / kWave, lane = threadIdx.x & (kWave - 1);
   const int cap = a.R + kChunk;

@@ -42,7 +42,7 @@ __device__ __forceinline__ void pack_store(const uint32_t c[8], uint32_t* dst) {
   store_words<B>(dst, w);
 }
 
-__device__ void pack_store_dyn(int bits, const uint32_t c[8], uint32_t* dst) {
+__device__ __forceinline__ void pack_store_dyn(int bits, const uint32_t c[8], uint32_t* dst) {
   switch (bits) {
     case 1: pack_store<1>(c, dst); break;
     case 2: pack_store<2>(c, dst); break;
@@ -61,7 +61,7 @@ struct Smem {
 };
 
 // Write this block's packed V chunks: channel c -> b words over 32 tokens.
-__device__ void pack_values_from_smem(const Smem& sm, int bits,
+__device__ __forceinline__ void pack_values_from_smem(const Smem& sm, int bits,
                                       uint32_t* region_blk, int lane) {
   const uint8_t* cb = reinterpret_cast<const uint8_t*>(sm.codes);
 #pragma unroll
@@ -80,7 +80,7 @@ __device__ void pack_values_from_smem(const Smem& sm, int bits,
 }
 
 // ------------------------------------------------------------------ KIVI K
-__device__ void kivi_keys(const QuantLaunch& a, Smem& sm, int b, int h,
+__device__ __forceinline__ void kivi_keys(const QuantLaunch& a, Smem& sm, int b, int h,
                           int blk, int lane) {
   const int bits = a.tab.bits[h][0];
   const float qmax = (float)((1 << bits) - 1);
@@ -129,7 +129,7 @@ __device__ void kivi_keys(const QuantLaunch& a, Smem& sm, int b, int h,
 }
 
 // ------------------------------------------------------------------ KIVI V
-__device__ void kivi_values(const QuantLaunch& a, Smem& sm, int b, int h,
+__device__ __forceinline__ void kivi_values(const QuantLaunch& a, Smem& sm, int b, int h,
                             int blk, int lane) {
   const int bits = a.tab.bits[h][1];
   const float qmax = (float)((1 << bits) - 1);
@@ -188,7 +188,7 @@ __device__ __forceinline__ float dpp_xor1(float v) {
                                       0xF, true));
 }
 
-__device__ void quarot_block(const QuantLaunch& a, Smem& sm, int b, int h,
+__device__ __forceinline__ void quarot_block(const QuantLaunch& a, Smem& sm, int b, int h,
                              int kind, int blk, int lane) {
   const int bits = a.tab.bits[h][kind];
   const int off = 1 << (bits - 1);
