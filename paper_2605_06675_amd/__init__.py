@@ -197,8 +197,7 @@ def rq_quantize_kv(cache, layer, n_past, k, v, stream=None):
 def rq_decode_attention(cache, layer, n_tokens, q, out, ws, scale=None,
                         stream=None):
     """q: torch [batch][n_q_heads][128]; out: fp32 same shape; ws: device
-    byte tensor of at least rq_decode_workspace bytes, zero-filled before
-    its first use (calls leave its ticket counters zero)."""
+    byte tensor of at least rq_decode_workspace bytes."""
     if scale is None:
         scale = 1.0 / np.sqrt(128.0)
     _check(lib().rq_decode_attention(
@@ -255,8 +254,7 @@ class KVCache:
         import torch
         need = rq_decode_workspace(self.desc, n_tokens)
         if self._ws is None or self._ws.numel() < need:
-            # zero-filled: the leading ticket counters must start at zero
-            self._ws = torch.zeros(need, dtype=torch.uint8,
+            self._ws = torch.empty(need, dtype=torch.uint8,
                                    device=self.codes.device)
         return self._ws
 

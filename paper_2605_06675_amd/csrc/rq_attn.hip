@@ -13,8 +13,8 @@
 // already in the A layout PV needs.  The next block's codes and metadata
 // are loaded while the current one is computed; metadata goes through LDS.
 // A workgroup merges its four waves in LDS and writes one partial
-// (max, sum, acc); the last workgroup of a unit (atomic ticket) merges the
-// unit's partials and writes the output (QuaRot: rotated back).
+// (max, sum, acc); a second kernel merges each unit's partials and writes
+// the output (QuaRot: rotated back).
 #include "rq_device.h"
 #include "rq_internal.h"
 
@@ -202,29 +202,33 @@ __device__ __forceinline__ void block_step(const Ctx& c, KStage<BK>& s,
     }
   }
   if (more) fetch_k<BK>(c, nb, s);
-  // online softmax, column col = query row j, tokens 4r+i and 16+4r+i
+  // Online softmax in the log2 domain, column col = query row j, tokens
+  // 4r+i and 16+4r+i.  The running max only moves when a block exceeds it
+  // by more than 2^8 (or on the wave's first block): probabilities stay
+  // <= 256, well inside fp16, and the accumulator rescale is rare.
   float mx = __builtin_fmaxf(S0[0], S1[0]);
 #pragma unroll
   for (int i = 1; i < 4; ++i) mx = __builtin_fmaxf(mx, __builtin_fmaxf(S0[i], S1[i]));
-  mx = __builtin_fmaxf(mx, xor_shfl(mx, 16));
-  mx = __builtin_fmaxf(mx, xor_shfl(mx, 32));
-  const float mnew = __builtin_fmaxf(ws.m_run, mx);
-  const float alpha = __builtin_amdgcn_exp2f(ws.m_run - mnew);
-  ws.m_run = mnew;
-  float p0[4], p1[4], psum = 0.0f;
+  if (__builtin_amdgcn_ballot_w64(!(mx <= ws.m_run + 8.0f))) {
+    mx = __builtin_fmaxf(mx, xor_shfl(mx, 16));
+    mx = __builtin_fmaxf(mx, xor_shfl(mx, 32));
+    const float mnew = __builtin_fmaxf(ws.m_run, mx);
+    const float alpha = __builtin_amdgcn_exp2f(ws.m_run - mnew);
+    ws.m_run = mnew;
+    ws.l_run *= alpha;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    p0[i] = __builtin_amdgcn_exp2f(S0[i] - mnew);
-    p1[i] = __builtin_amdgcn_exp2f(S1[i] - mnew);
-    psum += p0[i] + p1[i];
+    for (int i = 0; i < 4; ++i) {
+      const float ar = __shfl(alpha, 4 * r + i, kWave);
+#pragma unroll
+      for (int nt = 0; nt < 8; ++nt) ws.acc[nt][i] *= ar;
+    }
   }
-  ws.l_run = ws.l_run * alpha + psum;
-  // rows 4r + i of the accumulator belong to query 4r + i
+  float p0[4], p1[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const float ar = __shfl(alpha, 4 * r + i, kWave);
-#pragma unroll
-    for (int nt = 0; nt < 8; ++nt) ws.acc[nt][i] *= ar;
+    p0[i] = __builtin_amdgcn_exp2f(S0[i] - ws.m_run);
+    p1[i] = __builtin_amdgcn_exp2f(S1[i] - ws.m_run);
+    ws.l_run += p0[i] + p1[i];
   }
   uint32_t pp[4];
   if (QUAROT) {
@@ -417,7 +421,6 @@ attn_kernel(AttnLaunch a) {
   __shared__ float qs[16][kD];
   __shared__ u4 mbuf[kWaves][kWave];
   __shared__ u4 qbuf[4][kWave];      // QK B operand per (K-block, lane)
-  __shared__ int last_flag;
   extern __shared__ float merge[];   // [kWaves][G][2 + 128]
   const int slot = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid & (kWave - 1);
@@ -511,23 +514,28 @@ attn_kernel(AttnLaunch a) {
     }
   }
 
-  // ticket: the last of the n_wg + 1 workgroups of this unit combines
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-  __syncthreads();
-  if (tid == 0) {
-    const unsigned t = atomicAdd(a.counters + unit, 1u);
-    last_flag = (t == (unsigned)a.n_wg);
-  }
-  __syncthreads();
-  if (!last_flag) return;
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+}
 
-  float* rot = &qs[0][0];   // [G <= 16][128] scratch for the back-rotation
+// Merge the partials of one (batch, kv-head) unit: one workgroup per unit.
+// Slots 0 .. n_wg-1 hold the quantized blocks (QuaRot: rotated domain),
+// slot n_wg the 16-bit window (original domain).
+__global__ void __launch_bounds__(kThreads)
+combine_kernel(AttnLaunch a) {
+  extern __shared__ float lds[];   // rot[G][128], tail[G][128], inv[G][128]
+  const int unit = blockIdx.x, tid = threadIdx.x;
+  const int G = a.G;
+  const bool quarot = a.family == RQ_QUAROT;
+  float* rot = lds;
+  float* tail = lds + G * kD;
+  float* inv = lds + 2 * G * kD;
   const int ns = a.n_wg + 1;
   for (int e = tid; e < G * kD; e += kThreads) {
     const int j = e / kD, cc = e % kD;
     float M = -INFINITY;
-    for (int s = 0; s < ns; ++s) M = __builtin_fmaxf(M, part_ptr(a, unit, s)[j * (2 + kD)]);
+    for (int s = 0; s < ns; ++s) {
+      const float* src = part_ptr(a, unit, s) + j * (2 + kD);
+      if (src[1] > 0.0f) M = __builtin_fmaxf(M, src[0]);
+    }
     float num = 0.0f, numr = 0.0f, den = 0.0f;
     for (int s = 0; s < ns; ++s) {
       const float* src = part_ptr(a, unit, s) + j * (2 + kD);
@@ -536,9 +544,9 @@ attn_kernel(AttnLaunch a) {
       else num = __builtin_fmaf(f, src[2 + cc], num);
       den = __builtin_fmaf(f, src[1], den);
     }
-    rot[j * kD + cc] = num;
-    merge[j * kD + cc] = numr / den;
-    merge[G * kD + j * kD + cc] = 1.0f / den;
+    rot[e] = num;
+    tail[e] = numr / den;
+    inv[e] = 1.0f / den;
   }
   __syncthreads();
   if (quarot) {
@@ -554,20 +562,14 @@ attn_kernel(AttnLaunch a) {
     }
   }
   const float f = quarot ? kInvSqrtD : 1.0f;
-  for (int e = tid; e < G * kD; e += kThreads) {
-    const int j = e / kD, cc = e % kD;
-    a.out[((size_t)b * a.H * G + h * G + j) * kD + cc] =
-        rot[e] * f * merge[G * kD + e] + merge[e];
-  }
-  if (tid == 0) atomicExch(a.counters + unit, 0u);
+  float* out = a.out + (size_t)unit * G * kD;   // (b, h) -> query rows h*G..
+  for (int e = tid; e < G * kD; e += kThreads) out[e] = rot[e] * f * inv[e] + tail[e];
 }
 
 }  // namespace
 
 size_t attention_lds_bytes(int G) {
-  size_t merge = (size_t)kWaves * G * (2 + kD) * sizeof(float);
-  size_t fin = (size_t)2 * G * kD * sizeof(float);
-  return merge > fin ? merge : fin;
+  return (size_t)kWaves * G * (2 + kD) * sizeof(float);
 }
 
 hipError_t launch_attention(const AttnLaunch& a, hipStream_t s) {
@@ -581,6 +583,10 @@ hipError_t launch_attention(const AttnLaunch& a, hipStream_t s) {
   else
     hipLaunchKernelGGL(attn_kernel<8>, grid, dim3(kThreads),
                        attention_lds_bytes(a.G), s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(combine_kernel, dim3(a.B * a.H), dim3(kThreads),
+                     (size_t)3 * a.G * kD * sizeof(float), s, a);
   return hipGetLastError();
 }
 

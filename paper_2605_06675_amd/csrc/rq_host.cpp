@@ -131,10 +131,10 @@ SplitPlan plan_splits(const rq_cache* c, int n_tokens) {
   if (env && std::atoi(env) > 0) {
     per = std::atoi(env);
   } else {
-    const long target_wg = 1536;
+    const long target_wg = 1024;
     const long total = units * nblk;
     per = (total + target_wg - 1) / target_wg;
-    if (per < 16) per = 16;
+    if (per < 32) per = 32;
     per = (per + 3) / 4 * 4;
   }
   p.blk_per_wg = (int)per;
@@ -142,17 +142,10 @@ SplitPlan plan_splits(const rq_cache* c, int n_tokens) {
   return p;
 }
 
-constexpr uint64_t kCounterBytes = 256;  // alignment of the partials
-
-uint64_t counter_bytes(const rq_cache* c) {
-  const uint64_t n = (uint64_t)c->batch * c->n_kv_heads * sizeof(uint32_t);
-  return (n + kCounterBytes - 1) / kCounterBytes * kCounterBytes;
-}
-
 uint64_t attn_ws_bytes(const rq_cache* c, const SplitPlan& p) {
   const uint64_t G = c->n_q_heads / c->n_kv_heads;
   const uint64_t parts = (uint64_t)c->batch * c->n_kv_heads * (p.n_wg + 1);
-  return counter_bytes(c) + parts * G * (2 + rq::kD) * sizeof(float);
+  return parts * G * (2 + rq::kD) * sizeof(float);
 }
 
 }  // namespace
@@ -274,8 +267,7 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
   a.meta = static_cast<const uint8_t*>(c->meta) + meta_layer_bytes(c) * layer;
   a.resid = static_cast<const uint16_t*>(c->resid) + resid_layer_elems(c) * layer;
   a.out = out;
-  a.counters = static_cast<uint32_t*>(ws);
-  a.part = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + counter_bytes(c));
+  a.part = static_cast<float*>(ws);
   a.B = c->batch;
   a.H = c->n_kv_heads;
   a.G = G;

@@ -48,7 +48,6 @@ struct AttnLaunch {
   const uint8_t* meta;    // this layer
   const uint16_t* resid;  // this layer
   float* out;             // [B][Hq][128]
-  uint32_t* counters;     // [B][H] tickets, zero between calls
   float* part;            // [B][H][n_wg + 1][G][2 + 128] (max, sum, acc)
   int B, H, G, cap, R;
   int nq, n_tokens;
