@@ -108,35 +108,37 @@ __device__ __forceinline__ void fetch_v(const Ctx& c, int blk, VStage<BV>& s) {
   }
 }
 
-// pairs i' = 0..3 (codes 4r+i' and 16+4r+i') of the lane's V chunk words
+// pairs i' = 0..3 (codes 4r+i' and 16+4r+i') of the lane's V chunk words,
+// or'ed into the fp16 exponent pattern mg (see pair_or)
 template <int BV>
-__device__ __forceinline__ void vpairs(const uint32_t* vw, int r, uint32_t out[4]) {
+__device__ __forceinline__ void vpairs(const uint32_t* vw, int r, uint32_t mg,
+                                       uint32_t out[4]) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) out[i] = 0;
+  for (int i = 0; i < 4; ++i) out[i] = mg;
   int k = 0, o = 0;
 #pragma unroll
   for (int p = 0; p < Planes<BV>::n; ++p) {
     const int w = Planes<BV>::w[p];
-    const uint32_t m = ((1u << w) - 1u) * 0x00010001u;
+    const uint32_t m = (((1u << w) - 1u) * 0x00010001u) << o;
     if (w == 8) {
       const uint32_t a = vw[k], b = vw[k + 1];
-      out[0] |= (a & m) << o;
-      out[1] |= ((a >> 8) & m) << o;
-      out[2] |= (b & m) << o;
-      out[3] |= ((b >> 8) & m) << o;
+      out[0] = (shr_signed(a, -o) & m) | out[0];
+      out[1] = (shr_signed(a, 8 - o) & m) | out[1];
+      out[2] = (shr_signed(b, -o) & m) | out[2];
+      out[3] = (shr_signed(b, 8 - o) & m) | out[3];
       k += 2;
     } else if (w == 4) {
       const uint32_t a = vw[k++];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) out[i] |= ((a >> (4 * i)) & m) << o;
+      for (int i = 0; i < 4; ++i) out[i] = (shr_signed(a, 4 * i - o) & m) | out[i];
     } else if (w == 2) {
       const uint32_t a = vw[k++] >> (8 * (r & 1));
 #pragma unroll
-      for (int i = 0; i < 4; ++i) out[i] |= ((a >> (2 * i)) & m) << o;
+      for (int i = 0; i < 4; ++i) out[i] = (shr_signed(a, 2 * i - o) & m) | out[i];
     } else {
       const uint32_t a = vw[k++] >> (4 * r);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) out[i] |= ((a >> i) & m) << o;
+      for (int i = 0; i < 4; ++i) out[i] = (shr_signed(a, i - o) & m) | out[i];
     }
     o += w;
   }
@@ -155,6 +157,7 @@ __device__ __forceinline__ void block_step(const Ctx& c, KStage<BK>& s,
                                            const u4* qb, WaveState& ws,
                                            bool more, int nb) {
   const int r = c.r;
+  const uint32_t mg = opaque_magic();
   f4 S0 = {0.f, 0.f, 0.f, 0.f}, S1 = {0.f, 0.f, 0.f, 0.f};
   if (QUAROT) {
     const _Float16 o = (_Float16)(1024.0f + (float)(1 << (BK - 1)));
@@ -166,7 +169,7 @@ __device__ __forceinline__ void block_step(const Ctx& c, KStage<BK>& s,
         uint32_t x[4];
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk)
-          x[kk] = as_u32(codes_to_h2(pair_bits<BK>(s.kw[tile], 4 * kb + kk), off));
+          x[kk] = as_u32(magic_to_h2(pair_or<BK>(s.kw[tile], 4 * kb + kk, mg), off));
         const h8 qv = __builtin_bit_cast(h8, qb[kb * kWave]);
         if (tile == 0) S0 = mfma(make_h8(x[0], x[1], x[2], x[3]), qv, S0);
         else S1 = mfma(make_h8(x[0], x[1], x[2], x[3]), qv, S1);
@@ -192,7 +195,7 @@ __device__ __forceinline__ void block_step(const Ctx& c, KStage<BK>& s,
         uint32_t x[4];
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
-          const h2 u = codes_to_h2(pair_bits<BK>(s.kw[tile], 4 * kb + kk), off);
+          const h2 u = magic_to_h2(pair_or<BK>(s.kw[tile], 4 * kb + kk, mg), off);
           x[kk] = as_u32(__builtin_elementwise_fma(u, as_h2(sp[kk]), as_h2(zp[kk])));
         }
         const h8 qv = __builtin_bit_cast(h8, qb[kb * kWave]);
@@ -254,12 +257,12 @@ __device__ __forceinline__ void block_step(const Ctx& c, KStage<BK>& s,
 #pragma unroll
     for (int nt = 0; nt < 8; ++nt) {
       uint32_t pr[4];
-      vpairs<BV>(sv_.vw[nt], r, pr);
+      vpairs<BV>(sv_.vw[nt], r, mg, pr);
       ws.acc[nt] = mfma(P,
-                        make_h8(as_u32(codes_to_h2(pr[0], off)),
-                                as_u32(codes_to_h2(pr[1], off)),
-                                as_u32(codes_to_h2(pr[2], off)),
-                                as_u32(codes_to_h2(pr[3], off))),
+                        make_h8(as_u32(magic_to_h2(pr[0], off)),
+                                as_u32(magic_to_h2(pr[1], off)),
+                                as_u32(magic_to_h2(pr[2], off)),
+                                as_u32(magic_to_h2(pr[3], off))),
                         ws.acc[nt]);
     }
   } else {
@@ -273,10 +276,10 @@ __device__ __forceinline__ void block_step(const Ctx& c, KStage<BK>& s,
       for (int half = 0; half < 2; ++half) {
         const int nt = 2 * cg + half;
         uint32_t pr[4], x[4];
-        vpairs<BV>(sv_.vw[nt], r, pr);
+        vpairs<BV>(sv_.vw[nt], r, mg, pr);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const h2 u = codes_to_h2(pr[i], off);
+          const h2 u = magic_to_h2(pr[i], off);
           x[i] = as_u32(__builtin_elementwise_fma(u, as_h2(sp[i]), as_h2(zp[i])));
         }
         ws.acc[nt] = mfma(P, make_h8(x[0], x[1], x[2], x[3]), ws.acc[nt]);
@@ -518,35 +521,50 @@ attn_kernel(AttnLaunch a) {
 
 // Merge the partials of one (batch, kv-head) unit: one workgroup per unit.
 // Slots 0 .. n_wg-1 hold the quantized blocks (QuaRot: rotated domain),
-// slot n_wg the 16-bit window (original domain).
+// slot n_wg the 16-bit window (original domain).  All loads of a stage are
+// independent, so they are in flight together.
 __global__ void __launch_bounds__(kThreads)
 combine_kernel(AttnLaunch a) {
-  extern __shared__ float lds[];   // rot[G][128], tail[G][128], inv[G][128]
+  extern __shared__ float lds[];   // wgt[ns][G], lsum[ns][G], rot[G][128]
   const int unit = blockIdx.x, tid = threadIdx.x;
   const int G = a.G;
   const bool quarot = a.family == RQ_QUAROT;
-  float* rot = lds;
-  float* tail = lds + G * kD;
-  float* inv = lds + 2 * G * kD;
   const int ns = a.n_wg + 1;
-  for (int e = tid; e < G * kD; e += kThreads) {
-    const int j = e / kD, cc = e % kD;
+  float* wgt = lds;
+  float* lsum = lds + ns * G;
+  float* rot = lds + 2 * ns * G;
+  __shared__ float inv_den[16];
+  // per (slot, j): max and sum, then weights relative to the row max
+  for (int e = tid; e < ns * G; e += kThreads) {
+    const float* src = part_ptr(a, unit, e / G) + (e % G) * (2 + kD);
+    wgt[e] = src[1] > 0.0f ? src[0] : -INFINITY;
+    lsum[e] = src[1];
+  }
+  __syncthreads();
+  if (tid < G) {
     float M = -INFINITY;
-    for (int s = 0; s < ns; ++s) {
-      const float* src = part_ptr(a, unit, s) + j * (2 + kD);
-      if (src[1] > 0.0f) M = __builtin_fmaxf(M, src[0]);
+    for (int sl = 0; sl < ns; ++sl) M = __builtin_fmaxf(M, wgt[sl * G + tid]);
+    float den = 0.0f;
+    for (int sl = 0; sl < ns; ++sl) {
+      const float m = wgt[sl * G + tid];
+      const float f = m == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m - M);
+      wgt[sl * G + tid] = f;
+      den = __builtin_fmaf(f, lsum[sl * G + tid], den);
     }
-    float num = 0.0f, numr = 0.0f, den = 0.0f;
-    for (int s = 0; s < ns; ++s) {
-      const float* src = part_ptr(a, unit, s) + j * (2 + kD);
-      const float f = (src[1] > 0.0f) ? __builtin_amdgcn_exp2f(src[0] - M) : 0.0f;
-      if (s == a.n_wg) numr = f * src[2 + cc];
-      else num = __builtin_fmaf(f, src[2 + cc], num);
-      den = __builtin_fmaf(f, src[1], den);
-    }
+    inv_den[tid] = 1.0f / den;
+  }
+  __syncthreads();
+  float tailv[(16 * kD) / kThreads];
+  int n_e = 0;
+  for (int e = tid; e < G * kD; e += kThreads, ++n_e) {
+    const int j = e / kD, cc = e % kD;
+    float num = 0.0f;
+    const float* src = part_ptr(a, unit, 0) + j * (2 + kD) + 2 + cc;
+    const size_t stride = (size_t)G * (2 + kD);
+#pragma unroll 8
+    for (int sl = 0; sl < ns - 1; ++sl) num = __builtin_fmaf(wgt[sl * G + j], src[sl * stride], num);
+    tailv[n_e] = wgt[(ns - 1) * G + j] * src[(ns - 1) * stride];
     rot[e] = num;
-    tail[e] = numr / den;
-    inv[e] = 1.0f / den;
   }
   __syncthreads();
   if (quarot) {
@@ -563,7 +581,9 @@ combine_kernel(AttnLaunch a) {
   }
   const float f = quarot ? kInvSqrtD : 1.0f;
   float* out = a.out + (size_t)unit * G * kD;   // (b, h) -> query rows h*G..
-  for (int e = tid; e < G * kD; e += kThreads) out[e] = rot[e] * f * inv[e] + tail[e];
+  n_e = 0;
+  for (int e = tid; e < G * kD; e += kThreads, ++n_e)
+    out[e] = (rot[e] * f + tailv[n_e]) * inv_den[e / kD];
 }
 
 }  // namespace
@@ -585,8 +605,8 @@ hipError_t launch_attention(const AttnLaunch& a, hipStream_t s) {
                        attention_lds_bytes(a.G), s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(combine_kernel, dim3(a.B * a.H), dim3(kThreads),
-                     (size_t)3 * a.G * kD * sizeof(float), s, a);
+  const size_t lds = ((size_t)2 * (a.n_wg + 1) * a.G + (size_t)a.G * kD) * sizeof(float);
+  hipLaunchKernelGGL(combine_kernel, dim3(a.B * a.H), dim3(kThreads), lds, s, a);
   return hipGetLastError();
 }
 

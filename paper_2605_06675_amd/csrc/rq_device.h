@@ -99,12 +99,27 @@ __device__ __forceinline__ void pack_chunk(const uint32_t c[8], uint32_t out[B])
   }
 }
 
-// Codes i and i+16 of a chunk (0 <= i < 16) as the two half-words of a
-// uint32, read from the chunk's B words (i must fold to a constant after
-// unrolling).
+// 0x64006400 (the fp16 pair 1024, 1024) in a register the compiler cannot
+// see through, so that "(x & mask) | magic" becomes one v_and_or_b32 with
+// the mask in an SGPR (VOP3 has no literal operand on this target).
+__device__ __forceinline__ uint32_t opaque_magic() {
+  uint32_t m = 0x64006400u;
+  asm volatile("" : "+v"(m));
+  return m;
+}
+
+// x shifted right by s bits (left when s < 0); s is a constant after
+// unrolling.
+__device__ __forceinline__ uint32_t shr_signed(uint32_t x, int s) {
+  return s > 0 ? (x >> s) : (s < 0 ? (x << -s) : x);
+}
+
+// Codes i and i+16 of a chunk (0 <= i < 16) placed into the two fp16
+// mantissas of `acc` (which carries the 1024 exponent pattern): returns
+// acc | code_i | code_{i+16} << 16, read from the chunk's B words (i must
+// fold to a constant after unrolling).
 template <int B>
-__device__ __forceinline__ uint32_t pair_bits(const uint32_t* wds, int I) {
-  uint32_t v = 0;
+__device__ __forceinline__ uint32_t pair_or(const uint32_t* wds, int I, uint32_t acc) {
   int word = 0, shift = 0;
 #pragma unroll
   for (int p = 0; p < Planes<B>::n; ++p) {
@@ -112,11 +127,11 @@ __device__ __forceinline__ uint32_t pair_bits(const uint32_t* wds, int I) {
     const int per = 16 / w;
     const uint32_t m = ((1u << w) - 1u) * 0x00010001u;
     const int d = I / per, k = I % per;
-    v |= ((wds[word + d] >> (k * w)) & m) << shift;
+    acc = (shr_signed(wds[word + d], k * w - shift) & (m << shift)) | acc;
     word += w;
     shift += w;
   }
-  return v;
+  return acc;
 }
 
 __device__ __forceinline__ h2 as_h2(uint32_t x) {
@@ -126,10 +141,9 @@ __device__ __forceinline__ uint32_t as_u32(h2 x) {
   return __builtin_bit_cast(uint32_t, x);
 }
 
-// Two codes (half-words) -> the fp16 pair (code0, code1), exactly:
-// 0x6400 | c is 1024 + c in fp16, and 1024 is then subtracted.
-__device__ __forceinline__ h2 codes_to_h2(uint32_t pair, h2 off) {
-  return as_h2(pair | 0x64006400u) - off;
+// fp16 pair (1024 + code0, 1024 + code1) minus off, exactly.
+__device__ __forceinline__ h2 magic_to_h2(uint32_t magic_pair, h2 off) {
+  return as_h2(magic_pair) - off;
 }
 
 }  // namespace rq
