@@ -41,105 +41,88 @@ __device__ __forceinline__ float xor_shfl(float v, int mask) {
   return __shfl_xor(v, mask, kWave);
 }
 
-// Words of a V chunk that lane quarter r needs, per plane: 2 for the 8-bit
-// plane, 1 otherwise.
-template <int B> struct VWords {
-  static constexpr int n = (B == 8) ? 2 : Planes<B>::n;
-};
-
-template <int BK> struct KStage {
-  uint32_t kw[2][BK];
-  u4 meta;
-};
-
-template <int BV> struct VStage {
-  uint32_t vw[8][VWords<BV>::n];
+// A block's data is four contiguous byte ranges: K codes (512*BK), V codes
+// (512*BV), K metadata and V metadata (512 B each for KIVI, 64 B for
+// QuaRot).  A wave moves it global -> registers -> LDS as 16-byte pieces:
+// piece k of lane l covers bytes [16 l + 1024 k, +16) of the concatenation,
+// so every load instruction reads 1 KB of contiguous memory.
+template <int BK, int BV, bool QUAROT> struct Slot {
+  static constexpr int kb = 512 * BK;
+  static constexpr int vb = 512 * BV;
+  static constexpr int mb = QUAROT ? 64 : 512;
+  static constexpr int bytes = kb + vb + 2 * mb;
+  static constexpr int pieces = (bytes + 1023) / 1024;
 };
 
 struct Ctx {
-  const uint32_t* kreg;   // K codes of this unit
-  const uint32_t* vreg;   // V codes of this unit
+  const uint8_t* kreg;    // K codes of this unit
+  const uint8_t* vreg;    // V codes of this unit
   const uint8_t* kmeta;   // K metadata of this unit
   const uint8_t* vmeta;   // V metadata of this unit
-  int per_blk;            // metadata bytes per block and kind
   int r, col, lane;
 };
 
-// K words of the block (tiles 0/1: token 16*tile + col, chunk r) and this
-// lane's 16 bytes of the block metadata (lanes 0..31: K, 32..63: V).
-template <int BK>
-__device__ __forceinline__ void fetch_k(const Ctx& c, int blk, KStage<BK>& s) {
+template <int BK, int BV, bool QUAROT>
+__device__ __forceinline__ void load_block(const Ctx& c, int blk,
+                                           u4 (&reg)[Slot<BK, BV, QUAROT>::pieces]) {
+  using S = Slot<BK, BV, QUAROT>;
 #pragma unroll
-  for (int tile = 0; tile < 2; ++tile) {
-    const uint32_t* p = c.kreg + ((size_t)(blk * kChunk + 16 * tile + c.col) * 4 + c.r) * BK;
-#pragma unroll
-    for (int i = 0; i < BK; ++i) s.kw[tile][i] = p[i];
-  }
-  const int half = c.lane >> 5, i = c.lane & 31;
-  if (i * 16 < c.per_blk) {
-    const uint8_t* m = (half ? c.vmeta : c.kmeta) + (size_t)blk * c.per_blk + i * 16;
-    s.meta = *reinterpret_cast<const u4*>(m);
-  }
-}
-
-// V words lane quarter r needs from the chunks of channels 16*nt + col.
-template <int BV>
-__device__ __forceinline__ void fetch_v(const Ctx& c, int blk, VStage<BV>& s) {
-  const uint32_t* base = c.vreg + ((size_t)blk * kD + c.col) * BV;
-#pragma unroll
-  for (int nt = 0; nt < 8; ++nt) {
-    const uint32_t* ch = base + 16 * nt * BV;
-    int wb = 0, k = 0;
-#pragma unroll
-    for (int p = 0; p < Planes<BV>::n; ++p) {
-      const int w = Planes<BV>::w[p];
-      if (w == 8) {
-        s.vw[nt][k++] = ch[wb + 2 * c.r];
-        s.vw[nt][k++] = ch[wb + 2 * c.r + 1];
-      } else if (w == 4) {
-        s.vw[nt][k++] = ch[wb + c.r];
-      } else if (w == 2) {
-        s.vw[nt][k++] = ch[wb + (c.r >> 1)];
-      } else {
-        s.vw[nt][k++] = ch[wb];
-      }
-      wb += w;
+  for (int k = 0; k < S::pieces; ++k) {
+    const int o = 16 * c.lane + 1024 * k;
+    if (o < S::bytes) {
+      const uint8_t* src;
+      if (o < S::kb) src = c.kreg + (size_t)blk * S::kb + o;
+      else if (o < S::kb + S::vb) src = c.vreg + (size_t)blk * S::vb + (o - S::kb);
+      else if (o < S::kb + S::vb + S::mb) src = c.kmeta + (size_t)blk * S::mb + (o - S::kb - S::vb);
+      else src = c.vmeta + (size_t)blk * S::mb + (o - S::kb - S::vb - S::mb);
+      reg[k] = *reinterpret_cast<const u4*>(src);
     }
   }
 }
 
-// pairs i' = 0..3 (codes 4r+i' and 16+4r+i') of the lane's V chunk words,
-// or'ed into the fp16 exponent pattern mg (see pair_or)
+template <int BK, int BV, bool QUAROT>
+__device__ __forceinline__ void store_block(uint8_t* slot, int lane,
+                                            const u4 (&reg)[Slot<BK, BV, QUAROT>::pieces]) {
+  using S = Slot<BK, BV, QUAROT>;
+#pragma unroll
+  for (int k = 0; k < S::pieces; ++k) {
+    const int o = 16 * lane + 1024 * k;
+    if (o < S::bytes) *reinterpret_cast<u4*>(slot + o) = reg[k];
+  }
+}
+
+// pairs i' = 0..3 (codes 4r+i' and 16+4r+i') of channel chunk `ch` (its B
+// words in LDS), or'ed into the fp16 exponent pattern mg (see pair_or)
 template <int BV>
-__device__ __forceinline__ void vpairs(const uint32_t* vw, int r, uint32_t mg,
+__device__ __forceinline__ void vpairs(const uint32_t* ch, int r, uint32_t mg,
                                        uint32_t out[4]) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) out[i] = mg;
-  int k = 0, o = 0;
+  int wb = 0, o = 0;
 #pragma unroll
   for (int p = 0; p < Planes<BV>::n; ++p) {
     const int w = Planes<BV>::w[p];
     const uint32_t m = (((1u << w) - 1u) * 0x00010001u) << o;
     if (w == 8) {
-      const uint32_t a = vw[k], b = vw[k + 1];
+      const uint32_t a = ch[wb + 2 * r], b = ch[wb + 2 * r + 1];
       out[0] = (shr_signed(a, -o) & m) | out[0];
       out[1] = (shr_signed(a, 8 - o) & m) | out[1];
       out[2] = (shr_signed(b, -o) & m) | out[2];
       out[3] = (shr_signed(b, 8 - o) & m) | out[3];
-      k += 2;
     } else if (w == 4) {
-      const uint32_t a = vw[k++];
+      const uint32_t a = ch[wb + r];
 #pragma unroll
       for (int i = 0; i < 4; ++i) out[i] = (shr_signed(a, 4 * i - o) & m) | out[i];
     } else if (w == 2) {
-      const uint32_t a = vw[k++] >> (8 * (r & 1));
+      const uint32_t a = ch[wb + (r >> 1)] >> (8 * (r & 1));
 #pragma unroll
       for (int i = 0; i < 4; ++i) out[i] = (shr_signed(a, 2 * i - o) & m) | out[i];
     } else {
-      const uint32_t a = vw[k++] >> (4 * r);
+      const uint32_t a = ch[wb] >> (4 * r);
 #pragma unroll
       for (int i = 0; i < 4; ++i) out[i] = (shr_signed(a, i - o) & m) | out[i];
     }
+    wb += w;
     o += w;
   }
 }
@@ -149,33 +132,41 @@ struct WaveState {
   float m_run, l_run;
 };
 
-// One block: QK^T, online softmax, PV.  mb = this wave's metadata in LDS
-// (u4 index 0.. = K metadata, 32.. = V metadata).
+// One block, read from the LDS slot: QK^T, online softmax, PV.
 template <int BK, int BV, bool QUAROT>
-__device__ __forceinline__ void block_step(const Ctx& c, KStage<BK>& s,
-                                           VStage<BV>& sv_, const u4* mb,
-                                           const u4* qb, WaveState& ws,
-                                           bool more, int nb) {
+__device__ __forceinline__ void block_step(const Ctx& c, const uint8_t* slot,
+                                           const u4* qb, WaveState& ws) {
+  using S = Slot<BK, BV, QUAROT>;
   const int r = c.r;
   const uint32_t mg = opaque_magic();
+  const uint32_t* kwb = reinterpret_cast<const uint32_t*>(slot);
+  const uint32_t* vwb = reinterpret_cast<const uint32_t*>(slot + S::kb);
+  const u4* km = reinterpret_cast<const u4*>(slot + S::kb + S::vb);
+  const u4* vm = reinterpret_cast<const u4*>(slot + S::kb + S::vb + S::mb);
+  uint32_t kw[2][BK];
+#pragma unroll
+  for (int tile = 0; tile < 2; ++tile)
+#pragma unroll
+    for (int i = 0; i < BK; ++i) kw[tile][i] = kwb[((16 * tile + c.col) * 4 + r) * BK + i];
   f4 S0 = {0.f, 0.f, 0.f, 0.f}, S1 = {0.f, 0.f, 0.f, 0.f};
   if (QUAROT) {
     const _Float16 o = (_Float16)(1024.0f + (float)(1 << (BK - 1)));
     const h2 off = {o, o};
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
+      const h8 qv = __builtin_bit_cast(h8, qb[kb * kWave]);
 #pragma unroll
       for (int tile = 0; tile < 2; ++tile) {
         uint32_t x[4];
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk)
-          x[kk] = as_u32(magic_to_h2(pair_or<BK>(s.kw[tile], 4 * kb + kk, mg), off));
-        const h8 qv = __builtin_bit_cast(h8, qb[kb * kWave]);
+          x[kk] = as_u32(magic_to_h2(pair_or<BK>(kw[tile], 4 * kb + kk, mg), off));
         if (tile == 0) S0 = mfma(make_h8(x[0], x[1], x[2], x[3]), qv, S0);
         else S1 = mfma(make_h8(x[0], x[1], x[2], x[3]), qv, S1);
       }
     }
-    const u4 sv = mb[r];
+    // dword (4r + i) of the pair-ordered token scales = (s[4r+i], s[16+4r+i])
+    const u4 sv = km[r];
     const uint32_t ss[4] = {sv.x, sv.y, sv.z, sv.w};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -187,24 +178,26 @@ __device__ __forceinline__ void block_step(const Ctx& c, KStage<BK>& s,
     const h2 off = {(_Float16)1024.0f, (_Float16)1024.0f};
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      const u4 s4 = mb[r * 8 + kb], z4 = mb[r * 8 + 4 + kb];
+      const u4 s4 = km[r * 8 + kb], z4 = km[r * 8 + 4 + kb];
       const uint32_t sp[4] = {s4.x, s4.y, s4.z, s4.w};
       const uint32_t zp[4] = {z4.x, z4.y, z4.z, z4.w};
+      const h8 qv = __builtin_bit_cast(h8, qb[kb * kWave]);
 #pragma unroll
       for (int tile = 0; tile < 2; ++tile) {
         uint32_t x[4];
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
-          const h2 u = magic_to_h2(pair_or<BK>(s.kw[tile], 4 * kb + kk, mg), off);
+          const h2 u = magic_to_h2(pair_or<BK>(kw[tile], 4 * kb + kk, mg), off);
           x[kk] = as_u32(__builtin_elementwise_fma(u, as_h2(sp[kk]), as_h2(zp[kk])));
         }
-        const h8 qv = __builtin_bit_cast(h8, qb[kb * kWave]);
         if (tile == 0) S0 = mfma(make_h8(x[0], x[1], x[2], x[3]), qv, S0);
         else S1 = mfma(make_h8(x[0], x[1], x[2], x[3]), qv, S1);
       }
     }
   }
-  if (more) fetch_k<BK>(c, nb, s);
+  // keep the phases apart: hoisting all LDS reads of the block to its top
+  // would need more registers than four waves per SIMD allow
+  __builtin_amdgcn_sched_barrier(0);
   // Online softmax in the log2 domain, column col = query row j, tokens
   // 4r+i and 16+4r+i.  The running max only moves when a block exceeds it
   // by more than 2^8 (or on the wave's first block): probabilities stay
@@ -235,7 +228,7 @@ __device__ __forceinline__ void block_step(const Ctx& c, KStage<BK>& s,
   }
   uint32_t pp[4];
   if (QUAROT) {
-    const u4 sv = mb[32 + r];
+    const u4 sv = vm[r];
     const uint32_t ss[4] = {sv.x, sv.y, sv.z, sv.w};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -251,13 +244,14 @@ __device__ __forceinline__ void block_step(const Ctx& c, KStage<BK>& s,
     }
   }
   const h8 P = make_h8(pp[0], pp[1], pp[2], pp[3]);
+  __builtin_amdgcn_sched_barrier(0);
   if (QUAROT) {
     const _Float16 o = (_Float16)(1024.0f + (float)(1 << (BV - 1)));
     const h2 off = {o, o};
 #pragma unroll
     for (int nt = 0; nt < 8; ++nt) {
       uint32_t pr[4];
-      vpairs<BV>(sv_.vw[nt], r, mg, pr);
+      vpairs<BV>(vwb + (16 * nt + c.col) * BV, r, mg, pr);
       ws.acc[nt] = mfma(P,
                         make_h8(as_u32(magic_to_h2(pr[0], off)),
                                 as_u32(magic_to_h2(pr[1], off)),
@@ -269,14 +263,14 @@ __device__ __forceinline__ void block_step(const Ctx& c, KStage<BK>& s,
     const h2 off = {(_Float16)1024.0f, (_Float16)1024.0f};
 #pragma unroll
     for (int cg = 0; cg < 4; ++cg) {
-      const u4 s4 = mb[32 + cg * 8 + r], z4 = mb[32 + cg * 8 + 4 + r];
+      const u4 s4 = vm[cg * 8 + r], z4 = vm[cg * 8 + 4 + r];
       const uint32_t sp[4] = {s4.x, s4.y, s4.z, s4.w};
       const uint32_t zp[4] = {z4.x, z4.y, z4.z, z4.w};
 #pragma unroll
       for (int half = 0; half < 2; ++half) {
         const int nt = 2 * cg + half;
         uint32_t pr[4], x[4];
-        vpairs<BV>(sv_.vw[nt], r, mg, pr);
+        vpairs<BV>(vwb + (16 * nt + c.col) * BV, r, mg, pr);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const h2 u = magic_to_h2(pr[i], off);
@@ -286,35 +280,40 @@ __device__ __forceinline__ void block_step(const Ctx& c, KStage<BK>& s,
       }
     }
   }
-  if (more) fetch_v<BV>(c, nb, sv_);
 }
 
+// The wave's blocks blk_lo, blk_lo + 4, ... < blk_hi.  Two blocks are in
+// flight in registers while the current one, copied into this wave's LDS
+// slot, is computed.
 template <int BK, int BV, bool QUAROT>
 __device__ __forceinline__ void stream_blocks(const Ctx& c, int blk_lo, int blk_hi,
-                                              u4* mb, const u4* qb, WaveState& ws) {
+                                              uint8_t* slot, const u4* qb,
+                                              WaveState& ws) {
+  using S = Slot<BK, BV, QUAROT>;
   if (blk_lo >= blk_hi) return;
-  // Single-buffered pipeline: the next block's K words (+ metadata) are
-  // requested as soon as QK^T has consumed this block's, and its V words
-  // as soon as PV has consumed this block's.
-  KStage<BK> ks;
-  VStage<BV> vs;
-  fetch_k<BK>(c, blk_lo, ks);
-  fetch_v<BV>(c, blk_lo, vs);
-  for (int blk = blk_lo; blk < blk_hi; blk += kWaves) {
-    mb[c.lane] = ks.meta;
-    const int nb = blk + kWaves;
-    block_step<BK, BV, QUAROT>(c, ks, vs, mb, qb, ws, nb < blk_hi, nb);
+  u4 ra[S::pieces], rb[S::pieces];
+  load_block<BK, BV, QUAROT>(c, blk_lo, ra);
+  if (blk_lo + kWaves < blk_hi) load_block<BK, BV, QUAROT>(c, blk_lo + kWaves, rb);
+  for (int blk = blk_lo; blk < blk_hi; blk += 2 * kWaves) {
+    store_block<BK, BV, QUAROT>(slot, c.lane, ra);
+    if (blk + 2 * kWaves < blk_hi) load_block<BK, BV, QUAROT>(c, blk + 2 * kWaves, ra);
+    block_step<BK, BV, QUAROT>(c, slot, qb, ws);
+    const int b1 = blk + kWaves;
+    if (b1 >= blk_hi) break;
+    store_block<BK, BV, QUAROT>(slot, c.lane, rb);
+    if (b1 + 2 * kWaves < blk_hi) load_block<BK, BV, QUAROT>(c, b1 + 2 * kWaves, rb);
+    block_step<BK, BV, QUAROT>(c, slot, qb, ws);
   }
 }
 
 template <bool QUAROT, int MAXB>
-__device__ __forceinline__ void dispatch(int bk, int bv, const Ctx& c, int lo, int hi, u4* mb,
-                         const u4* qb, WaveState& ws) {
+__device__ __forceinline__ void dispatch(int bk, int bv, const Ctx& c, int lo, int hi,
+                                         uint8_t* slot, const u4* qb, WaveState& ws) {
 #define RQ_CASE(K, V)                                                   \
   case (K - 1) * 8 + (V - 1):                                           \
     if (K <= MAXB && V <= MAXB)                                         \
       stream_blocks<(K <= MAXB ? K : 1), (V <= MAXB ? V : 1), QUAROT>(   \
-          c, lo, hi, mb, qb, ws);                                       \
+          c, lo, hi, slot, qb, ws);                                     \
     break;
 #define RQ_ROW(K) RQ_CASE(K, 1) RQ_CASE(K, 2) RQ_CASE(K, 3) RQ_CASE(K, 4) \
                   RQ_CASE(K, 5) RQ_CASE(K, 6) RQ_CASE(K, 7) RQ_CASE(K, 8)
@@ -417,14 +416,18 @@ __device__ __forceinline__ void residual_slot(const AttnLaunch& a, int b, int h,
 }
 
 // MAXB: largest bit-width the kernel handles (4: the common {1..4} range,
-// compiled for four resident waves per SIMD; 8: every width).
+// compiled for three resident waves per SIMD, each with two blocks in
+// flight; 8: every width).
 template <int MAXB>
-__global__ void __launch_bounds__(kThreads, MAXB <= 4 ? 4 : 2)
+__global__ void __launch_bounds__(kThreads, MAXB <= 4 ? 3 : 2)
 attn_kernel(AttnLaunch a) {
   __shared__ float qs[16][kD];
-  __shared__ u4 mbuf[kWaves][kWave];
   __shared__ u4 qbuf[4][kWave];      // QK B operand per (K-block, lane)
-  extern __shared__ float merge[];   // [kWaves][G][2 + 128]
+  // per-wave block slots while streaming, then the wave merge area
+  // [kWaves][G][2 + 128] floats
+  extern __shared__ u4 dyn[];
+  uint8_t* slots = reinterpret_cast<uint8_t*>(dyn);
+  float* merge = reinterpret_cast<float*>(dyn);
   const int slot = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid & (kWave - 1);
   const size_t unit = (size_t)b * a.H + h;
@@ -456,14 +459,12 @@ attn_kernel(AttnLaunch a) {
     const u4* qb = &qbuf[0][lane];
     const int bk = a.tab.bits[h][0], bv = a.tab.bits[h][1];
     const int nblk_cap = a.cap / kChunk;
+    const int per_blk = quarot ? kMetaBlockTok : kMetaBlockKivi;
     Ctx c;
-    c.per_blk = quarot ? kMetaBlockTok : kMetaBlockKivi;
-    c.kreg = reinterpret_cast<const uint32_t*>(a.codes + a.tab.code_off[h][0]) +
-             (size_t)b * a.cap * 4 * bk;
-    c.vreg = reinterpret_cast<const uint32_t*>(a.codes + a.tab.code_off[h][1]) +
-             (size_t)b * nblk_cap * kD * bv;
-    c.kmeta = a.meta + (((size_t)h * 2 + 0) * a.B + b) * nblk_cap * c.per_blk;
-    c.vmeta = a.meta + (((size_t)h * 2 + 1) * a.B + b) * nblk_cap * c.per_blk;
+    c.kreg = a.codes + a.tab.code_off[h][0] + (size_t)b * a.cap * 16 * bk;
+    c.vreg = a.codes + a.tab.code_off[h][1] + (size_t)b * a.cap * 16 * bv;
+    c.kmeta = a.meta + (((size_t)h * 2 + 0) * a.B + b) * nblk_cap * per_blk;
+    c.vmeta = a.meta + (((size_t)h * 2 + 1) * a.B + b) * nblk_cap * per_blk;
     c.r = r;
     c.col = col;
     c.lane = lane;
@@ -476,13 +477,15 @@ attn_kernel(AttnLaunch a) {
     const int lo = slot * a.blk_per_wg;
     int hi = lo + a.blk_per_wg;
     if (hi > nblk) hi = nblk;
+    uint8_t* my_slot = slots + (size_t)wave * a.slot_bytes;
     if (quarot)
-      dispatch<true, MAXB>(bk, bv, c, lo + wave, hi, mbuf[wave], qb, ws);
+      dispatch<true, MAXB>(bk, bv, c, lo + wave, hi, my_slot, qb, ws);
     else
-      dispatch<false, MAXB>(bk, bv, c, lo + wave, hi, mbuf[wave], qb, ws);
+      dispatch<false, MAXB>(bk, bv, c, lo + wave, hi, my_slot, qb, ws);
     ws.l_run += xor_shfl(ws.l_run, 16);
     ws.l_run += xor_shfl(ws.l_run, 32);
-    // merge the four waves in LDS
+    // merge the four waves in LDS (the merge area reuses the block slots)
+    __syncthreads();
     float* mw = merge + (size_t)wave * G * (2 + kD);
     if (r == 0 && col < G) {
       mw[col * (2 + kD)] = ws.m_run;
@@ -588,8 +591,10 @@ combine_kernel(AttnLaunch a) {
 
 }  // namespace
 
-size_t attention_lds_bytes(int G) {
-  return (size_t)kWaves * G * (2 + kD) * sizeof(float);
+size_t attention_lds_bytes(int G, int slot_bytes) {
+  const size_t merge = (size_t)kWaves * G * (2 + kD) * sizeof(float);
+  const size_t slots = (size_t)kWaves * slot_bytes;
+  return merge > slots ? merge : slots;
 }
 
 hipError_t launch_attention(const AttnLaunch& a, hipStream_t s) {
@@ -599,10 +604,10 @@ hipError_t launch_attention(const AttnLaunch& a, hipStream_t s) {
     for (int k = 0; k < 2; ++k) maxb = a.tab.bits[h][k] > maxb ? a.tab.bits[h][k] : maxb;
   if (maxb <= 4)
     hipLaunchKernelGGL(attn_kernel<4>, grid, dim3(kThreads),
-                       attention_lds_bytes(a.G), s, a);
+                       attention_lds_bytes(a.G, a.slot_bytes), s, a);
   else
     hipLaunchKernelGGL(attn_kernel<8>, grid, dim3(kThreads),
-                       attention_lds_bytes(a.G), s, a);
+                       attention_lds_bytes(a.G, a.slot_bytes), s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const size_t lds = ((size_t)2 * (a.n_wg + 1) * a.G + (size_t)a.G * kD) * sizeof(float);

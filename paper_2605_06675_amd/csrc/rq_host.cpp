@@ -118,10 +118,28 @@ struct SplitPlan {
   int nq, n_wg, blk_per_wg;
 };
 
-// Workgroups (four waves each) per (batch, kv-head) unit: enough to give
-// every CU several resident workgroups, each streaming a contiguous run of
-// 32-token blocks.
-SplitPlan plan_splits(const rq_cache* c, int n_tokens) {
+// Compute units of the current device (queried once; 256 when no device
+// can be queried, e.g. for host-only sizing calls).
+int cu_count() {
+  static int n = 0;
+  if (n == 0) {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) ==
+            hipSuccess &&
+        v > 0)
+      n = v;
+    else
+      n = 256;
+  }
+  return n;
+}
+
+// Workgroups (four waves each) per (batch, kv-head) unit.  The grid is sized
+// to one resident round: wg_per_cu workgroups per CU (the attention kernel
+// for widths <= 4 bits runs three waves per SIMD, i.e. three workgroups per
+// CU; the 8-bit one two), counting each unit's residual-window workgroup.
+SplitPlan plan_splits(const rq_cache* c, int n_tokens, int wg_per_cu = 3) {
   SplitPlan p;
   p.nq = n_quantized(n_tokens, c->residual);
   const long nblk = p.nq / rq::kChunk;
@@ -131,10 +149,10 @@ SplitPlan plan_splits(const rq_cache* c, int n_tokens) {
   if (env && std::atoi(env) > 0) {
     per = std::atoi(env);
   } else {
-    const long target_wg = 1024;
-    const long total = units * nblk;
-    per = (total + target_wg - 1) / target_wg;
-    if (per < 32) per = 32;
+    long slots = (long)cu_count() * wg_per_cu / units - 1;
+    if (slots < 1) slots = 1;
+    per = (nblk + slots - 1) / slots;
+    if (per < 8) per = 8;
     per = (per + 3) / 4 * 4;
   }
   p.blk_per_wg = (int)per;
@@ -255,7 +273,15 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
   if (!q || !out || !ws || !c->codes || !c->meta || !c->resid)
     return fail(RQ_EINVAL, "NULL device pointer");
   if (!std::isfinite(scale)) return fail(RQ_EINVAL, "scale is not finite");
-  const SplitPlan p = plan_splits(c, n_tokens);
+  const rq::LayerTable tab = layer_table(c, layer);
+  int maxb = 1, maxkv = 0;
+  for (int h = 0; h < c->n_kv_heads; ++h) {
+    const int kb = tab.bits[h][0], vb = tab.bits[h][1];
+    maxb = kb > maxb ? kb : maxb;
+    maxb = vb > maxb ? vb : maxb;
+    maxkv = kb + vb > maxkv ? kb + vb : maxkv;
+  }
+  const SplitPlan p = plan_splits(c, n_tokens, maxb <= 4 ? 3 : 2);
   const uint64_t need = attn_ws_bytes(c, p);
   if (ws_bytes < need)
     return fail(RQ_ESMALLWS, "workspace %llu bytes < %llu needed",
@@ -280,7 +306,8 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
   a.is_bf16 = c->dtype == RQ_BF16;
   a.family = c->family;
   a.qscale = scale * 1.4426950408889634f;
-  a.tab = layer_table(c, layer);
+  a.tab = tab;
+  a.slot_bytes = 512 * maxkv + 2 * meta_per_block(c);
   hipError_t e = rq::launch_attention(a, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "attention launch");
   return ok();

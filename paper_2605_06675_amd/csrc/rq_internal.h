@@ -52,6 +52,7 @@ struct AttnLaunch {
   int B, H, G, cap, R;
   int nq, n_tokens;
   int n_wg, blk_per_wg;   // workgroups per unit streaming blocks
+  int slot_bytes;         // LDS bytes per wave for one block of this layer
   int is_bf16, family;
   float qscale;           // scale * log2(e)
   LayerTable tab;
