@@ -13,8 +13,8 @@ CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "librq.so")
 BUILD = os.path.join(HERE, "_build")
 
-SOURCES = ["rq_host.cpp", "rq_alloc.cpp", "rq_quant.hip", "rq_attn.hip",
-           "rq_calib.hip"]
+SOURCES = ["rq_host.cpp", "rq_alloc.cpp"] + sorted(
+    f for f in os.listdir(CSRC) if f.endswith(".hip"))
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
@@ -28,40 +28,37 @@ COMMON = [
 
 
 def _compile(src):
-    obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
+    """Compile one source; for HIP sources keep the device assembly
+    (-save-temps) and reject any call instruction in it: device functions
+    are force-inlined (a called function that needs long-branch relaxation
+    may reuse its return-address registers)."""
+    stem = os.path.splitext(src)[0]
+    obj = os.path.join(BUILD, stem + ".o")
     cmd = [HIPCC, *COMMON, "-c", os.path.join(CSRC, src), "-o", obj]
-    r = subprocess.run(cmd, capture_output=True, text=True)
+    if src.endswith(".hip"):
+        cmd.insert(-4, "-save-temps=obj")
+    r = subprocess.run(cmd, capture_output=True, text=True, cwd=BUILD)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stderr}")
+    if src.endswith(".hip"):
+        asm = [f for f in os.listdir(BUILD)
+               if f.startswith(stem + "-hip-amdgcn") and f.endswith(".s")]
+        if not asm:
+            raise RuntimeError(f"{src}: device assembly not found")
+        with open(os.path.join(BUILD, asm[0])) as f:
+            if "s_swappc" in f.read():
+                raise RuntimeError(f"{src}: device code contains a function call")
     return obj
-
-
-def _check_no_calls(src):
-    """Kernels must be call-free: device functions are force-inlined (a
-    called function that needs long-branch relaxation may reuse its
-    return-address registers).  Compile to device assembly and reject any
-    call instruction."""
-    asm = os.path.join(BUILD, os.path.splitext(src)[0] + ".s")
-    cmd = [HIPCC, *COMMON, "--cuda-device-only", "-S", os.path.join(CSRC, src),
-           "-o", asm]
-    r = subprocess.run(cmd, capture_output=True, text=True)
-    if r.returncode != 0:
-        raise RuntimeError(f"hipcc -S failed for {src}:\n{r.stderr}")
-    with open(asm) as f:
-        if "s_swappc" in f.read():
-            raise RuntimeError(f"{src}: device code contains a function call")
-    return asm
 
 
 def build(verbose=False):
     """Compile every source and link librq.so (always rebuilds)."""
     os.makedirs(BUILD, exist_ok=True)
-    hip = [s for s in SOURCES if s.endswith(".hip")]
-    with concurrent.futures.ThreadPoolExecutor(len(SOURCES) + len(hip)) as ex:
-        checks = [ex.submit(_check_no_calls, s) for s in hip]
-        objs = list(ex.map(_compile, SOURCES))
-        for c in checks:
-            c.result()
+    # the attention variants for widths up to 8 instantiate the most
+    # kernels: start them first, they bound the wall time
+    order = sorted(SOURCES, key=lambda f: (0 if "_b8" in f else 1, f))
+    with concurrent.futures.ThreadPoolExecutor(os.cpu_count() or 8) as ex:
+        objs = list(ex.map(_compile, order))
     tmp = OUT + ".tmp"
     cmd = [HIPCC, "-shared", "-fPIC", "--offload-arch=gfx950", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)

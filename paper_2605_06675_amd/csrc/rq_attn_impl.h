@@ -1,0 +1,923 @@
+// Decode attention over the packed mixed-bit cache (KIVI-style and
+// QuaRot-style quantizers).
+//
+// Grid (workgroup slot, kv-head, batch), four waves per workgroup.  Slots
+// 0 .. n_wg-1 stream the quantized 32-token blocks of their (batch, kv-head)
+// unit (about three workgroups per CU in all).  The 16-bit residual window
+// is attended to by the kernel that merges the partials.  A wave streams every
+// fourth block of its slot's range: the block's bytes (codes and metadata)
+// are fetched two blocks ahead with 1 KB-per-instruction loads and copied
+// into the wave's LDS slot, from where each lane reads its MFMA operands.
+//
+// Per block (32 tokens) a wave runs QK^T and PV on v_mfma_f32_16x16x32_f16.
+// The VALU only turns packed fields into fp16 operands, and it does so in
+// one v_and_or_b32 per pair of codes: a field sitting at mantissa bit P of
+// the fp16 pattern 1024 (0x6400) reads as 1024 + u * 2^P.  The weight 2^P is
+// divided out of the other operand (the query for keys, the probability for
+// values) and the 1024 offset, the zero points and the symmetric offsets are
+// removed by a few more MFMAs against constant operands, so no per-element
+// subtraction or FMA is needed:
+//   KIVI keys    S = sum_c (q_c s_c 2^-P)(1024 + u 2^P)
+//                    + sum_c z_c q_c - 1024 sum_c (q_c s_c 2^-P)
+//   KIVI values  O = sum_t (p_t s_t 2^-P)(1024 + u 2^P)
+//                    + sum_t p_t z_t - 1024 sum_t (p_t s_t 2^-P)
+//   QuaRot       the same with per-token scales and codes u - 2^(b-1).
+// With G query heads per kv-head the sixteen MFMA columns carry the G
+// queries 16/G times over; the KIVI value side uses the spare rows for the
+// four 32-channel groups of a token, so one A operand serves all of them.
+// Softmax runs in the log2 domain with a lazily moved maximum (it moves
+// only when a block exceeds it by 2^4), so probabilities stay <= 16.
+//
+// A workgroup merges its waves in LDS and writes one partial (max, sum,
+// acc); a second kernel merges each unit's partials and writes the output
+// (QuaRot: rotated back).
+#pragma once
+
+#include "rq_device.h"
+#include "rq_internal.h"
+
+namespace rq {
+
+namespace {
+
+constexpr int kWave = 64;
+constexpr int kWaves = 4;
+constexpr int kThreads = kWave * kWaves;
+constexpr float kInvSqrtD = 0.08838834764831845f;
+constexpr uint32_t kMagic = 0x64006400u;   // fp16 pair (1024, 1024)
+constexpr uint32_t kNeg1024 = 0xE400E400u; // fp16 pair (-1024, -1024)
+constexpr uint32_t kOnes = 0x3C003C00u;    // fp16 pair (1, 1)
+constexpr float kLazy = 4.0f;              // log2 headroom of the running max
+
+// LDS slots per wave (blocks in flight).  Two keep three workgroups per CU
+// inside the LDS for widths up to 4 bits.
+constexpr int attn_depth(int maxb) { return maxb <= 4 ? 2 : 2; }
+// waves per SIMD the attention kernel is compiled for
+constexpr int kAttnOcc = 3;
+
+// ---------------------------------------------------------- field positions
+// Plane widths of a b-bit code are the binary digits of b, widest first.
+__host__ __device__ __forceinline__ constexpr int plane_w(int b, int p) {
+  int n = 0;
+  for (int w = 8; w >= 1; w >>= 1)
+    if (b & w) {
+      if (n == p) return w;
+      ++n;
+    }
+  return 0;
+}
+__host__ __device__ __forceinline__ constexpr int plane_n(int b) {
+  int n = 0;
+  for (int w = 8; w >= 1; w >>= 1) n += (b & w) ? 1 : 0;
+  return n;
+}
+// first word of plane p inside a chunk == first code bit of plane p
+__host__ __device__ __forceinline__ constexpr int plane_off(int b, int p) {
+  int o = 0;
+  for (int q = 0; q < p; ++q) o += plane_w(b, q);
+  return o;
+}
+constexpr uint32_t pair_mask(int w) { return ((1u << w) - 1u) * 0x00010001u; }
+
+// Key pair i (0..15) of a chunk: plane-0 slot k = i mod (16 / w0) at bit
+// k * w0 of its word.  The word is shifted right by kshift before masking so
+// that the whole b-bit code lies inside the 10 fp16 mantissa bits; the code
+// then carries the weight 2^kpos.  One shift serves all later slots.
+__host__ __device__ __forceinline__ constexpr int kshift(int b, int i) {
+  const int w = plane_w(b, 0), k = i % (16 / w);
+  int cur = 0;
+  for (int s = 0; s <= k; ++s)
+    if (s * w - cur + b > 10) cur = s * w;
+  return cur;
+}
+__host__ __device__ __forceinline__ constexpr int kpos(int b, int i) {
+  const int w = plane_w(b, 0);
+  return (i % (16 / w)) * w - kshift(b, i);
+}
+// Value pair slot i (0..3) of lane quarter r (codes 4r+i and 16+4r+i of a
+// channel's chunk): after a per-lane pre-shift the plane-0 field sits at bit
+// i * w0 (w0 <= 4), or at 8 * (i & 1) of word 2r + i/2 (w0 = 8).
+__host__ __device__ __forceinline__ constexpr int vshift(int b, int i) {
+  const int w = plane_w(b, 0);
+  if (w == 8) return 8 * (i & 1);
+  int cur = 0;
+  for (int s = 0; s <= i; ++s)
+    if (s * w - cur + b > 10) cur = s * w;
+  return cur;
+}
+__host__ __device__ __forceinline__ constexpr int vpos(int b, int i) {
+  const int w = plane_w(b, 0);
+  return (w == 8 ? 8 * (i & 1) : i * w) - vshift(b, i);
+}
+// fp16 bits of 2^-e (0 <= e <= 14), exact
+constexpr uint32_t h_pow2_neg(int e) { return (uint32_t)(15 - e) << 10; }
+constexpr uint32_t h_pair(uint32_t h) { return h | (h << 16); }
+
+__device__ __forceinline__ h8 make_h8(uint32_t a, uint32_t b, uint32_t c,
+                                      uint32_t d) {
+  u4 v = {a, b, c, d};
+  return __builtin_bit_cast(h8, v);
+}
+__device__ __forceinline__ h8 u4_h8(u4 v) { return __builtin_bit_cast(h8, v); }
+
+__device__ __forceinline__ f4 mfma(h8 a, h8 b, f4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float xor_shfl(float v, int mask) {
+  return __shfl_xor(v, mask, kWave);
+}
+
+// max of three floats (v_maximum3_f32; the operands are never NaN, and
+// fmaxf would add canonicalising moves)
+__device__ __forceinline__ float max3(float a, float b, float c) {
+  return __builtin_elementwise_maximum(__builtin_elementwise_maximum(a, b), c);
+}
+
+// Wait states around the in-place rescale below: the compiler does not
+// insert them for inline assembly, and its operands are MFMA results (XDL
+// write -> VALU read needs up to 19) that the next MFMA reads back.
+__device__ __forceinline__ void xdl_wait() {
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7");
+}
+
+// x *= s in place: tying the operands keeps a rarely taken rescale from
+// making the register allocator copy every accumulator on the other path
+__device__ __forceinline__ void scale_inplace(f4& v, int i, float s) {
+  float x = v[i];
+  asm volatile("v_mul_f32 %0, %0, %1" : "+v"(x) : "v"(s));
+  v[i] = x;
+}
+
+// (x & mask) | c: with c opaque (the magic pattern) this is one
+// v_and_or_b32, the mask in an SGPR
+__device__ __forceinline__ uint32_t and_or(uint32_t x, uint32_t mask, uint32_t c) {
+  return (x & mask) | c;
+}
+// insert the bits of x under mask into c (one v_bfi_b32; used for the
+// lower planes of a code, whose bits are still zero in c)
+__device__ __forceinline__ uint32_t insert(uint32_t x, uint32_t mask, uint32_t c) {
+  return (x & mask) | (c & ~mask);
+}
+
+__device__ __forceinline__ uint32_t pk_mul(uint32_t a, uint32_t b) {
+  return as_u32(as_h2(a) * as_h2(b));
+}
+
+// fp16 pair (1024 + u_i 2^P, 1024 + u_{i+16} 2^P) of key pair i of a chunk
+// (its B words), P = kpos(B, i).
+template <int B>
+__device__ __forceinline__ uint32_t kpair(const uint32_t* wds, int i, uint32_t magic) {
+  constexpr int w0 = plane_w(B, 0);
+  const int P = kpos(B, i);
+  uint32_t acc = and_or(wds[i / (16 / w0)] >> kshift(B, i), pair_mask(w0) << P, magic);
+#pragma unroll
+  for (int p = 1; p < plane_n(B); ++p) {
+    const int w = plane_w(B, p), per = 16 / w, off = plane_off(B, p);
+    const int pos = (i % per) * w, tgt = P + off;
+    acc = insert(shr_signed(wds[off + i / per], pos - tgt), pair_mask(w) << tgt, acc);
+  }
+  return acc;
+}
+
+// fp16 pairs (1024 + u 2^P) of value slots i = 0..3 (codes 4r+i, 16+4r+i)
+// of one channel's chunk (its B words in LDS), P = vpos(B, i).
+template <int B>
+__device__ __forceinline__ void vpairs(const uint32_t* ch, int r, uint32_t magic,
+                                       uint32_t out[4]) {
+  constexpr int w0 = plane_w(B, 0);
+  if constexpr (w0 == 8) {
+    const uint32_t x = ch[2 * r], y = ch[2 * r + 1];
+    out[0] = and_or(x, pair_mask(8), magic);
+    out[1] = and_or(x >> 8, pair_mask(8), magic);
+    out[2] = and_or(y, pair_mask(8), magic);
+    out[3] = and_or(y >> 8, pair_mask(8), magic);
+  } else {
+    constexpr int per = 16 / w0;
+    const uint32_t x = ch[(4 * r) / per] >> (((4 * r) % per) * w0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      out[i] = and_or(x >> vshift(B, i), pair_mask(w0) << vpos(B, i), magic);
+#pragma unroll
+    for (int p = 1; p < plane_n(B); ++p) {
+      const int w = plane_w(B, p), pp = 16 / w, off = plane_off(B, p);
+      const uint32_t y = ch[off + (4 * r) / pp] >> (((4 * r) % pp) * w);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int tgt = vpos(B, i) + off;
+        out[i] = insert(shr_signed(y, i * w - tgt), pair_mask(w) << tgt, out[i]);
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------ wave state
+template <int NA>
+struct WaveState {
+  f4 acc[8];        // PV accumulators, channel tiles 16nt..16nt+15
+  f4 corrA[NA];     // -1024 (and symmetric-offset) corrections per A operand
+  f4 corrZ;         // KIVI: sum_t p z_{t,g} in column g, sum_t p in column 4;
+                    // QuaRot: sum_t p in every column
+  float m_run;      // running max of this lane's query (log2 domain)
+};
+
+// Static per-lane operands built once per workgroup.
+struct LaneOps {
+  uint32_t qh[16];  // QK B operand: fp16 (q * 2^-kpos) per k-slot pair
+  uint32_t qz[16];  // KIVI: fp16 q per k-slot pair (zero-point term)
+  uint32_t wv[4];   // fp16 pair 2^-vpos of value slot i
+  uint32_t vq[4];   // QuaRot: fp16 pair -(1024 + 2^(b-1) 2^vpos) of slot i
+  f4 corrK;         // QuaRot: -sum_c qh (1024 + off 2^kpos) (same in all rows)
+  uint32_t magic;   // kMagic, kept in a VGPR so that "(x & m) | magic" is one
+                    // v_and_or_b32 with the mask in an SGPR (VOP3 takes no
+                    // literal operand on this target)
+  int r, col, lane;
+  int gsub;         // col / GP
+  int GP;           // queries per replica (power of two >= G)
+};
+
+struct SlotPtrs {
+  const uint32_t* kc;  // K codes of the block (LDS)
+  const uint32_t* vc;  // V codes
+  const u4* km;        // K metadata
+  const u4* vm;        // V metadata
+};
+
+// K side of one block: S0 (tokens 4r+i), S1 (tokens 16+4r+i) relative to
+// m_ref, for this lane's query.  A operands: tile t (tokens 16t..16t+15,
+// row = col), k-slot pairs (kb, k') of chunk r, unpacked per K-step.
+template <int FAM, int BK>
+__device__ __forceinline__ void kpart(const SlotPtrs& sp, const LaneOps& lo, float m_ref,
+                                      f4& S0, f4& S1) {
+  const int r = lo.r;
+  uint32_t kw[2][BK];
+#pragma unroll
+  for (int tile = 0; tile < 2; ++tile)
+#pragma unroll
+    for (int i = 0; i < BK; ++i) kw[tile][i] = sp.kc[((16 * tile + lo.col) * 4 + r) * BK + i];
+  uint32_t Bq[16];
+  f4 X;
+  if constexpr (FAM == RQ_KIVI) {
+    // per-channel scales folded into the query; zero points and the 1024
+    // offset enter through the X chain
+    const h8 neg = make_h8(kNeg1024, kNeg1024, kNeg1024, kNeg1024);
+    X = (f4){-m_ref, -m_ref, -m_ref, -m_ref};
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      const u4 s4 = sp.km[r * 8 + kb], z4 = sp.km[r * 8 + 4 + kb];
+      Bq[4 * kb + 0] = pk_mul(lo.qh[4 * kb + 0], s4.x);
+      Bq[4 * kb + 1] = pk_mul(lo.qh[4 * kb + 1], s4.y);
+      Bq[4 * kb + 2] = pk_mul(lo.qh[4 * kb + 2], s4.z);
+      Bq[4 * kb + 3] = pk_mul(lo.qh[4 * kb + 3], s4.w);
+      X = mfma(u4_h8(z4), make_h8(lo.qz[4 * kb], lo.qz[4 * kb + 1], lo.qz[4 * kb + 2],
+                                  lo.qz[4 * kb + 3]), X);
+    }
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+      X = mfma(neg, make_h8(Bq[4 * kb], Bq[4 * kb + 1], Bq[4 * kb + 2], Bq[4 * kb + 3]), X);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) Bq[i] = lo.qh[i];
+    X = lo.corrK;
+  }
+  S0 = X;
+  S1 = X;
+#pragma unroll
+  for (int kb = 0; kb < 4; ++kb) {
+    const h8 Bk = make_h8(Bq[4 * kb], Bq[4 * kb + 1], Bq[4 * kb + 2], Bq[4 * kb + 3]);
+    S0 = mfma(make_h8(kpair<BK>(kw[0], 4 * kb, lo.magic), kpair<BK>(kw[0], 4 * kb + 1, lo.magic),
+                      kpair<BK>(kw[0], 4 * kb + 2, lo.magic), kpair<BK>(kw[0], 4 * kb + 3, lo.magic)),
+              Bk, S0);
+    S1 = mfma(make_h8(kpair<BK>(kw[1], 4 * kb, lo.magic), kpair<BK>(kw[1], 4 * kb + 1, lo.magic),
+                      kpair<BK>(kw[1], 4 * kb + 2, lo.magic), kpair<BK>(kw[1], 4 * kb + 3, lo.magic)),
+              Bk, S1);
+  }
+  if constexpr (FAM != RQ_KIVI) {
+    // per-token scales: dword 4r+i of the pair-ordered scales holds tokens
+    // (4r+i, 16+4r+i)
+    const u4 sv = sp.km[r];
+    const uint32_t ss[4] = {sv.x, sv.y, sv.z, sv.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const h2 sc = as_h2(ss[i]);
+      S0[i] = __builtin_fmaf(S0[i], (float)sc.x, -m_ref);
+      S1[i] = __builtin_fmaf(S1[i], (float)sc.y, -m_ref);
+    }
+  }
+}
+
+// V side of one block: probabilities P (fp16 pairs of tokens 4r+i and
+// 16+4r+i of this lane's query) times the dequantized values; B operands:
+// tile nt (channels 16nt..16nt+15, column = col), token slots of quarter r.
+template <int FAM, int NA, int BV>
+__device__ __forceinline__ void vpart(const SlotPtrs& sp, const LaneOps& lo,
+                                      const uint32_t (&P)[4], const uint32_t* cst,
+                                      WaveState<NA>& ws) {
+  constexpr int GPA = 4 / NA;   // value groups per A operand (KIVI)
+  const int r = lo.r, col = lo.col;
+  uint32_t P2[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) P2[i] = pk_mul(P[i], h_pair(h_pow2_neg(vpos(BV, i))));
+  uint32_t A[NA][4];
+  if constexpr (FAM == RQ_KIVI) {
+#pragma unroll
+    for (int a = 0; a < NA; ++a) {
+      const int g = a * GPA + lo.gsub % GPA;
+      const u4 s4 = sp.vm[g * 8 + r];
+      A[a][0] = pk_mul(P2[0], s4.x);
+      A[a][1] = pk_mul(P2[1], s4.y);
+      A[a][2] = pk_mul(P2[2], s4.z);
+      A[a][3] = pk_mul(P2[3], s4.w);
+    }
+  } else {
+    const u4 s4 = sp.vm[r];
+    A[0][0] = pk_mul(P2[0], s4.x);
+    A[0][1] = pk_mul(P2[1], s4.y);
+    A[0][2] = pk_mul(P2[2], s4.z);
+    A[0][3] = pk_mul(P2[3], s4.w);
+  }
+#pragma unroll
+  for (int nt = 0; nt < 8; ++nt) {
+    const int a = (FAM == RQ_KIVI) ? (nt / 2) / GPA : 0;
+    uint32_t pr[4];
+    vpairs<BV>(sp.vc + (16 * nt + col) * BV, r, lo.magic, pr);
+    ws.acc[nt] = mfma(make_h8(A[a][0], A[a][1], A[a][2], A[a][3]),
+                      make_h8(pr[0], pr[1], pr[2], pr[3]), ws.acc[nt]);
+  }
+  const h8 Ph = make_h8(P[0], P[1], P[2], P[3]);
+  if constexpr (FAM == RQ_KIVI) {
+    const h8 neg = make_h8(kNeg1024, kNeg1024, kNeg1024, kNeg1024);
+#pragma unroll
+    for (int a = 0; a < NA; ++a)
+      ws.corrA[a] = mfma(make_h8(A[a][0], A[a][1], A[a][2], A[a][3]), neg, ws.corrA[a]);
+    // column g < 4: zero points of group g; column 4: ones; others: zeros
+    const u4 bz = (col < 4) ? sp.vm[col * 8 + 4 + r]
+                            : reinterpret_cast<const u4*>(cst)[col == 4 ? 0 : 1];
+    ws.corrZ = mfma(Ph, u4_h8(bz), ws.corrZ);
+  } else {
+    uint32_t c[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      // -(1024 + 2^(b-1) 2^vpos) of slot i, exact in fp16
+      const _Float16 v = (_Float16)(-(1024.0f + (float)(1 << (BV - 1)) *
+                                                    (float)(1 << vpos(BV, i))));
+      const h2 vv = {v, v};
+      c[i] = as_u32(vv);
+    }
+    ws.corrA[0] = mfma(make_h8(A[0][0], A[0][1], A[0][2], A[0][3]),
+                       make_h8(c[0], c[1], c[2], c[3]), ws.corrA[0]);
+    ws.corrZ = mfma(Ph, make_h8(kOnes, kOnes, kOnes, kOnes), ws.corrZ);
+  }
+}
+
+// One block from the LDS slot: QK^T, online softmax, PV.
+template <int FAM, int NA, int BK, int BV>
+__device__ __forceinline__ void block_step(const uint8_t* slot, const LaneOps& lo,
+                                           const uint32_t* cst, WaveState<NA>& ws) {
+  constexpr int MB = FAM == RQ_KIVI ? kMetaBlockKivi : kMetaBlockTok;
+  SlotPtrs sp;
+  sp.kc = reinterpret_cast<const uint32_t*>(slot);
+  sp.vc = reinterpret_cast<const uint32_t*>(slot + 512 * BK);
+  sp.km = reinterpret_cast<const u4*>(slot + 512 * (BK + BV));
+  sp.vm = reinterpret_cast<const u4*>(slot + 512 * (BK + BV) + MB);
+  const float m_ref = ws.m_run == -INFINITY ? 0.0f : ws.m_run;
+  f4 S0, S1;
+  kpart<FAM, BK>(sp, lo, m_ref, S0, S1);
+  // keep the phases apart: hoisting all LDS reads of the block to its top
+  // needs more registers than two waves per SIMD allow
+  __builtin_amdgcn_sched_barrier(0);
+  float mx = max3(S0[0], S1[0], S0[1]);
+  mx = max3(mx, S1[1], S0[2]);
+  mx = max3(mx, S1[2], S0[3]);
+  mx = max3(mx, S1[3], S1[3]);
+  if (__builtin_amdgcn_ballot_w64(!(mx <= kLazy) || ws.m_run == -INFINITY)) {
+    mx = __builtin_fmaxf(mx, xor_shfl(mx, 16));
+    mx = __builtin_fmaxf(mx, xor_shfl(mx, 32));
+    const float mnew = __builtin_fmaxf(ws.m_run, m_ref + mx);
+    const float alpha = __builtin_amdgcn_exp2f(ws.m_run - mnew);
+    const float delta = m_ref - mnew;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      S0[i] += delta;
+      S1[i] += delta;
+    }
+    ws.m_run = mnew;
+    xdl_wait();
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      // accumulator row 4r+i belongs to query (4r+i) mod GP
+      const float ar = __shfl(alpha, (4 * lo.r + i) & (lo.GP - 1), kWave);
+#pragma unroll
+      for (int nt = 0; nt < 8; ++nt) scale_inplace(ws.acc[nt], i, ar);
+#pragma unroll
+      for (int a = 0; a < NA; ++a) scale_inplace(ws.corrA[a], i, ar);
+      scale_inplace(ws.corrZ, i, ar);
+    }
+    xdl_wait();
+  }
+  uint32_t P[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const h2 pv = {(_Float16)__builtin_amdgcn_exp2f(S0[i]),
+                   (_Float16)__builtin_amdgcn_exp2f(S1[i])};
+    P[i] = as_u32(pv);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  vpart<FAM, NA, BV>(sp, lo, P, cst, ws);
+}
+
+// A block's data is four contiguous byte ranges: K codes (512*BK), V codes
+// (512*BV), K metadata and V metadata (MB bytes each).  A wave copies it
+// straight from global memory into one of its LDS slots with
+// global_load_lds_dwordx4: piece k of lane l covers bytes [16 l + 1024 k,
+// +16) of the concatenation, so every instruction moves 1 KB of contiguous
+// memory and no VGPR holds the data in flight.
+template <int FAM, int BK, int BV> struct Slot {
+  static constexpr int kb = 512 * BK;
+  static constexpr int vb = 512 * BV;
+  static constexpr int mb = FAM == RQ_KIVI ? kMetaBlockKivi : kMetaBlockTok;
+  static constexpr int bytes = kb + vb + 2 * mb;
+  static constexpr int pieces = (bytes + 1023) / 1024;
+};
+
+struct Geo {
+  const uint8_t* kreg;   // K codes of this unit
+  const uint8_t* vreg;   // V codes
+  const uint8_t* kmeta;  // K metadata
+  const uint8_t* vmeta;  // V metadata
+};
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+template <int FAM, int BK, int BV>
+__device__ __forceinline__ void issue_block(const Geo& g, int blk, int lane, uint8_t* slot) {
+  using S = Slot<FAM, BK, BV>;
+#pragma unroll
+  for (int k = 0; k < S::pieces; ++k) {
+    const int o = 16 * lane + 1024 * k;
+    if (o < S::bytes) {
+      const uint8_t* src;
+      if (o < S::kb) src = g.kreg + (size_t)blk * S::kb + o;
+      else if (o < S::kb + S::vb) src = g.vreg + (size_t)blk * S::vb + (o - S::kb);
+      else if (o < S::kb + S::vb + S::mb) src = g.kmeta + (size_t)blk * S::mb + (o - S::kb - S::vb);
+      else src = g.vmeta + (size_t)blk * S::mb + (o - S::kb - S::vb - S::mb);
+      __builtin_amdgcn_global_load_lds(src, (lds_void*)(slot + 1024 * k), 16, 0, 0);
+    }
+  }
+}
+
+// Wait until at most N vector-memory operations of this wave are in flight
+// (gfx9 s_waitcnt encoding: vmcnt in bits 3:0 and 15:14, expcnt and lgkmcnt
+// at their maxima).  The compiler does not track LDS written by
+// global_load_lds, so the reads of a slot are fenced by hand.
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N < 64, "vmcnt is 6 bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+  asm volatile("" ::: "memory");
+}
+
+// The first DEPTH blocks of a wave, issued before the workgroup prologue so
+// that their latency overlaps it (bytes and pieces as in Slot<>, at run time).
+__device__ __forceinline__ int issue_first(const Geo& g, int bk, int bv, int mb, int depth,
+                                           int blk_lo, int blk_hi, int lane, uint8_t* slots,
+                                           int slot_bytes) {
+  const int kb = 512 * bk, vb = 512 * bv, bytes = kb + vb + 2 * mb;
+  const int pieces = (bytes + 1023) / 1024;
+  int issued = 0;
+  for (int j = 0; j < depth; ++j) {
+    const int blk = blk_lo + kWaves * j;
+    if (blk >= blk_hi) break;
+    issued += pieces;
+    uint8_t* slot = slots + j * slot_bytes;
+    for (int k = 0; k < pieces; ++k) {
+      const int o = 16 * lane + 1024 * k;
+      if (o < bytes) {
+        const uint8_t* src;
+        if (o < kb) src = g.kreg + (size_t)blk * kb + o;
+        else if (o < kb + vb) src = g.vreg + (size_t)blk * vb + (o - kb);
+        else if (o < kb + vb + mb) src = g.kmeta + (size_t)blk * mb + (o - kb - vb);
+        else src = g.vmeta + (size_t)blk * mb + (o - kb - vb - mb);
+        __builtin_amdgcn_global_load_lds(src, (lds_void*)(slot + 1024 * k), 16, 0, 0);
+      }
+    }
+  }
+  return issued;
+}
+
+// wait_vm<n> for a run-time n (0 .. 31; larger counts wait for everything)
+__device__ __forceinline__ void wait_vm_rt(int n) {
+  switch (n) {
+#define RQ_W(N) case N: wait_vm<N>(); break;
+    RQ_W(1) RQ_W(2) RQ_W(3) RQ_W(4) RQ_W(5) RQ_W(6) RQ_W(7) RQ_W(8) RQ_W(9) RQ_W(10)
+    RQ_W(11) RQ_W(12) RQ_W(13) RQ_W(14) RQ_W(15) RQ_W(16) RQ_W(17) RQ_W(18) RQ_W(19)
+    RQ_W(20) RQ_W(21) RQ_W(22) RQ_W(23) RQ_W(24) RQ_W(25) RQ_W(26) RQ_W(27) RQ_W(28)
+    RQ_W(29) RQ_W(30) RQ_W(31)
+#undef RQ_W
+    default: wait_vm<0>(); break;
+  }
+}
+
+// The wave's blocks blk_lo, blk_lo + 4, ... < blk_hi, DEPTH of them in
+// flight: block i lives in slot i mod DEPTH, and the slot is refilled with
+// block i + DEPTH once block i has been computed.
+template <int FAM, int NA, int BK, int BV, int DEPTH>
+__device__ __forceinline__ void stream_blocks(const Geo& g, int blk_lo, int blk_hi,
+                                              uint8_t* slots, int slot_bytes, const LaneOps& lo,
+                                              const uint32_t* cst, WaveState<NA>& ws) {
+  using S = Slot<FAM, BK, BV>;
+  static_assert(DEPTH >= 1 && DEPTH <= 3, "wait counts below cover up to three slots");
+  // the first DEPTH blocks were issued by issue_first
+  const int n = blk_lo < blk_hi ? (blk_hi - blk_lo + kWaves - 1) / kWaves : 0;
+  int cur = 0;
+  for (int i = 0; i < n; ++i) {
+    // blocks i+1 .. i+ahead were issued after block i
+    const int ahead = (n - 1 - i) < (DEPTH - 1) ? (n - 1 - i) : (DEPTH - 1);
+    if (ahead >= 2) wait_vm<2 * S::pieces>();
+    else if (ahead == 1) wait_vm<S::pieces>();
+    else wait_vm<0>();
+    uint8_t* slot = slots + cur * slot_bytes;
+    block_step<FAM, NA, BK, BV>(slot, lo, cst, ws);
+    if (i + DEPTH < n) {
+      // every LDS read of this slot has returned before it is refilled
+      __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+      asm volatile("" ::: "memory");
+      issue_block<FAM, BK, BV>(g, blk_lo + kWaves * (i + DEPTH), lo.lane, slot);
+    }
+    cur = cur + 1 == DEPTH ? 0 : cur + 1;
+  }
+}
+
+// Dispatch on the unit's (K bits, V bits), uniform per workgroup; widths
+// above MAXB are not instantiated.
+template <int FAM, int NA, int MAXB, int DEPTH>
+__device__ __forceinline__ void dispatch(int bk, int bv, const Geo& g, int lo_blk, int hi_blk,
+                                         uint8_t* slots, int slot_bytes, const LaneOps& lo,
+                                         const uint32_t* cst, WaveState<NA>& ws) {
+#define RQ_CASE(K, V)                                                              \
+  case (K - 1) * 8 + (V - 1):                                                      \
+    if (K <= MAXB && V <= MAXB)                                                    \
+      stream_blocks<FAM, NA, (K <= MAXB ? K : 1), (V <= MAXB ? V : 1), DEPTH>(     \
+          g, lo_blk, hi_blk, slots, slot_bytes, lo, cst, ws);                      \
+    break;
+#define RQ_ROW(K) RQ_CASE(K, 1) RQ_CASE(K, 2) RQ_CASE(K, 3) RQ_CASE(K, 4) \
+                  RQ_CASE(K, 5) RQ_CASE(K, 6) RQ_CASE(K, 7) RQ_CASE(K, 8)
+  switch ((bk - 1) * 8 + (bv - 1)) {
+    RQ_ROW(1) RQ_ROW(2) RQ_ROW(3) RQ_ROW(4) RQ_ROW(5) RQ_ROW(6) RQ_ROW(7) RQ_ROW(8)
+    default: break;
+  }
+#undef RQ_ROW
+#undef RQ_CASE
+}
+
+// The 16-bit query rows of this kv-head as 16-byte pieces (thread tid holds
+// piece tid: row tid / 16, channels 8 (tid % 16) ..), zero beyond G rows.
+__device__ __forceinline__ u4 query_piece(const AttnLaunch& a, int b, int h) {
+  const int tid = threadIdx.x;
+  u4 v = {0u, 0u, 0u, 0u};
+  if (tid < a.G * 16)
+    v = reinterpret_cast<const u4*>(a.q + ((size_t)b * a.H * a.G + (size_t)h * a.G) * kD)[tid];
+  return v;
+}
+
+// Copy the 16-bit query rows of this kv-head (G x 256 bytes) into qraw with
+// global_load_lds: wave w moves bytes [1024 w, 1024 w + 1024).  Returns the
+// number of copy instructions this wave issued (0 or 1).
+__device__ __forceinline__ int issue_query(const AttnLaunch& a, int b, int h, int wave,
+                                           int lane, uint16_t* qraw) {
+  const int bytes = a.G * kD * 2;
+  if (1024 * wave >= bytes) return 0;
+  const uint8_t* src = reinterpret_cast<const uint8_t*>(
+      a.q + ((size_t)b * a.H * a.G + (size_t)h * a.G) * kD);
+  if (1024 * wave + 16 * lane < bytes)
+    __builtin_amdgcn_global_load_lds(src + 1024 * wave + 16 * lane,
+                                     (lds_void*)(reinterpret_cast<uint8_t*>(qraw) + 1024 * wave),
+                                     16, 0, 0);
+  return 1;
+}
+
+// Scaled query rows into qs (rows >= G zero), rotated for QuaRot.  Whole
+// workgroup; piece from query_piece.
+__device__ __forceinline__ void store_queries(const AttnLaunch& a, u4 piece, bool rotate,
+                                              float (*qs)[kD]) {
+  const int tid = threadIdx.x;
+  float f = a.qscale;
+  if (rotate) f *= kInvSqrtD;
+  const float fs = rotate ? 1.0f : f;
+  {
+    const int j = tid >> 4, c = 8 * (tid & 15);
+    const uint32_t w[4] = {piece.x, piece.y, piece.z, piece.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      qs[j][c + 2 * e] = widen(w[e] & 0xffffu, a.is_bf16) * fs;
+      qs[j][c + 2 * e + 1] = widen(w[e] >> 16, a.is_bf16) * fs;
+    }
+  }
+  __syncthreads();
+  if (rotate) {
+    for (int hh = 1; hh < kD; hh *= 2) {
+      for (int e = tid; e < a.G * (kD / 2); e += kThreads) {
+        const int j = e / (kD / 2), i = e % (kD / 2);
+        const int base = (i / hh) * 2 * hh + (i % hh);
+        const float x = qs[j][base], y = qs[j][base + hh];
+        qs[j][base] = x + y;
+        qs[j][base + hh] = x - y;
+      }
+      __syncthreads();
+    }
+    for (int e = tid; e < a.G * kD; e += kThreads) qs[e / kD][e % kD] *= f;
+    __syncthreads();
+  }
+}
+
+// Partial of (unit, slot): float [G][2 + 128] = (max, sum, acc[128]).
+__device__ __forceinline__ float* part_ptr(const AttnLaunch& a, size_t unit, int slot) {
+  return a.part + (unit * (a.n_wg + 1) + slot) * (size_t)a.G * (2 + kD);
+}
+
+// Residual-window staging: 64 tokens of K and of V per chunk, rows padded
+// to 272 bytes so that lanes reading different rows spread over the banks.
+constexpr int kResTok = 64;
+constexpr int kResRow = 136;   // uint16 per padded row
+constexpr size_t kResLds = (size_t)2 * kResTok * kResRow * sizeof(uint16_t);
+
+// 16-bit residual window of one unit, original domain.  The window is read
+// in chunks of 64 tokens staged in LDS with coalesced 16-byte loads; wave w
+// takes query rows w, w+4, ...; lane = token for the scores, lane = channel
+// pair for PV.  stage: LDS for the chunk (kResLds bytes), qs: query rows.
+__device__ __forceinline__ void residual_slot(const AttnLaunch& a, int b, int h,
+                                              const float (*qs)[kD], uint16_t* stage,
+                                              float* dst) {
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid & (kWave - 1);
+  const int cap = a.R + kChunk;
+  const uint16_t* kb = a.resid + (((size_t)b * a.H + h) * 2 + 0) * cap * kD;
+  const uint16_t* vb = a.resid + (((size_t)b * a.H + h) * 2 + 1) * cap * kD;
+  uint16_t* ks = stage;
+  uint16_t* vs = stage + kResTok * kResRow;
+  float m_run[4], l_run[4], ac0[4], ac1[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    m_run[q] = -INFINITY;
+    l_run[q] = 0.0f;
+    ac0[q] = 0.0f;
+    ac1[q] = 0.0f;
+  }
+  for (int t0 = a.nq; t0 < a.n_tokens; t0 += kResTok) {
+    const int n = (a.n_tokens - t0) < kResTok ? (a.n_tokens - t0) : kResTok;
+    for (int e = tid; e < n * 16; e += kThreads) {
+      const int t = e >> 4, piece = e & 15;
+      const size_t row = (size_t)((t0 + t) % cap) * kD + piece * 8;
+      *reinterpret_cast<u4*>(ks + t * kResRow + piece * 8) = *reinterpret_cast<const u4*>(kb + row);
+      *reinterpret_cast<u4*>(vs + t * kResRow + piece * 8) = *reinterpret_cast<const u4*>(vb + row);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int j = wave + kWaves * q;
+      if (j >= a.G) break;
+      float s = -INFINITY;
+      if (lane < n) {
+        s = 0.0f;
+        const u4* kr = reinterpret_cast<const u4*>(ks + lane * kResRow);
+#pragma unroll 4
+        for (int c8 = 0; c8 < kD / 8; ++c8) {
+          const u4 w = kr[c8];
+          const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            s = __builtin_fmaf(qs[j][8 * c8 + 2 * e], widen(ww[e] & 0xffffu, a.is_bf16), s);
+            s = __builtin_fmaf(qs[j][8 * c8 + 2 * e + 1], widen(ww[e] >> 16, a.is_bf16), s);
+          }
+        }
+      }
+      float mx = s;
+      for (int d = 32; d >= 1; d >>= 1) mx = __builtin_fmaxf(mx, xor_shfl(mx, d));
+      const float mn = __builtin_fmaxf(m_run[q], mx);
+      const float al = __builtin_amdgcn_exp2f(m_run[q] - mn);
+      const float p = lane < n ? __builtin_amdgcn_exp2f(s - mn) : 0.0f;
+      float sum = p;
+      for (int d = 32; d >= 1; d >>= 1) sum += xor_shfl(sum, d);
+      l_run[q] = l_run[q] * al + sum;
+      m_run[q] = mn;
+      float c0 = ac0[q] * al, c1 = ac1[q] * al;
+#pragma unroll 8
+      for (int i = 0; i < n; ++i) {
+        const uint32_t w = *reinterpret_cast<const uint32_t*>(vs + i * kResRow + 2 * lane);
+        const float pi = __builtin_bit_cast(
+            float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, p), i));
+        c0 = __builtin_fmaf(pi, widen(w & 0xffffu, a.is_bf16), c0);
+        c1 = __builtin_fmaf(pi, widen(w >> 16, a.is_bf16), c1);
+      }
+      ac0[q] = c0;
+      ac1[q] = c1;
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int j = wave + kWaves * q;
+    if (j >= a.G) break;
+    float* d = dst + (size_t)j * (2 + kD);
+    if (lane == 0) {
+      d[0] = m_run[q];
+      d[1] = l_run[q];
+    }
+    d[2 + 2 * lane] = ac0[q];
+    d[2 + 2 * lane + 1] = ac1[q];
+  }
+}
+
+// Quantized blocks of workgroup slot `slot` of unit (b, h): stream, merge the
+// four waves and write the slot's partial.
+template <int FAM, int NA, int MAXB>
+__device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h, int b,
+                                            float (*qs)[kD], uint16_t* qraw, uint32_t* cst,
+                                            uint8_t* slots, float* merge) {
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid & (kWave - 1);
+  const size_t unit = (size_t)b * a.H + h;
+  const int G = a.G;
+  const int bk = a.tab.bits[h][0], bv = a.tab.bits[h][1];
+  const int nblk_cap = a.cap / kChunk;
+  const int per_blk = FAM == RQ_QUAROT ? kMetaBlockTok : kMetaBlockKivi;
+  Geo g;
+  g.kreg = a.codes + a.tab.code_off[h][0] + (size_t)b * a.cap * 16 * bk;
+  g.vreg = a.codes + a.tab.code_off[h][1] + (size_t)b * a.cap * 16 * bv;
+  g.kmeta = a.meta + (((size_t)h * 2 + 0) * a.B + b) * nblk_cap * per_blk;
+  g.vmeta = a.meta + (((size_t)h * 2 + 1) * a.B + b) * nblk_cap * per_blk;
+  const int nblk = a.nq / kChunk;
+  const int blo = slot * a.blk_per_wg;
+  int bhi = blo + a.blk_per_wg;
+  if (bhi > nblk) bhi = nblk;
+  constexpr int DEPTH = attn_depth(MAXB);
+  uint8_t* my_slots = slots + (size_t)wave * DEPTH * a.slot_bytes;
+  // query copy first, then the first blocks: waiting for the queries then
+  // leaves the block copies in flight
+  const int nq_ops = issue_query(a, b, h, wave, lane, qraw);
+  const int nb_ops = issue_first(g, bk, bv, per_blk, DEPTH, blo + wave, bhi, lane, my_slots,
+                                 a.slot_bytes);
+  if (nq_ops) wait_vm_rt(nb_ops);
+  __syncthreads();
+  const uint16_t* qr = qraw + (threadIdx.x >> 4) * kD + 8 * (threadIdx.x & 15);
+  const u4 qpiece = (int)(threadIdx.x >> 4) < G ? *reinterpret_cast<const u4*>(qr)
+                                                 : (u4){0u, 0u, 0u, 0u};
+  store_queries(a, qpiece, FAM == RQ_QUAROT, qs);
+  if (tid < 8) cst[tid] = tid < 4 ? kOnes : 0u;
+  __syncthreads();
+  LaneOps lo;
+  lo.lane = lane;
+  lo.magic = opaque_magic();
+  lo.r = lane >> 4;
+  lo.col = lane & 15;
+  lo.GP = a.GP;
+  lo.gsub = lo.col / a.GP;
+  {
+    // static QK operands: k-slot pair (kb, k') = channels 32r + 4kb + k'
+    // and 32r + 16 + 4kb + k' of query col mod GP
+    const int j = lo.col & (a.GP - 1);
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        const int c0 = 32 * lo.r + 4 * kb + kk;
+        const float q0 = j < G ? qs[j][c0] : 0.0f, q1 = j < G ? qs[j][c0 + 16] : 0.0f;
+        const float wgt = __builtin_ldexpf(1.0f, -kpos(bk, 4 * kb + kk));
+        const h2 vh = {(_Float16)(q0 * wgt), (_Float16)(q1 * wgt)};
+        const h2 vz = {(_Float16)q0, (_Float16)q1};
+        lo.qh[4 * kb + kk] = as_u32(vh);
+        lo.qz[4 * kb + kk] = as_u32(vz);
+      }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int e = vpos(bv, i);
+      lo.wv[i] = h_pair((uint32_t)(15 - e) << 10);
+      const _Float16 v = (_Float16)(-(1024.0f + (float)(1 << (bv - 1)) * __builtin_ldexpf(1.0f, e)));
+      const h2 vv = {v, v};
+      lo.vq[i] = as_u32(vv);
+    }
+    lo.corrK = (f4){0.f, 0.f, 0.f, 0.f};
+    if (FAM == RQ_QUAROT) {
+      const float off = (float)(1 << (bk - 1));
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        uint32_t c[4];
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+          const _Float16 v = (_Float16)(-(1024.0f + off * __builtin_ldexpf(1.0f, kpos(bk, 4 * kb + kk))));
+          const h2 vv = {v, v};
+          c[kk] = as_u32(vv);
+        }
+        lo.corrK = mfma(make_h8(c[0], c[1], c[2], c[3]),
+                        make_h8(lo.qh[4 * kb], lo.qh[4 * kb + 1], lo.qh[4 * kb + 2],
+                                lo.qh[4 * kb + 3]),
+                        lo.corrK);
+      }
+    }
+  }
+  WaveState<NA> ws;
+#pragma unroll
+  for (int nt = 0; nt < 8; ++nt) ws.acc[nt] = (f4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int i = 0; i < NA; ++i) ws.corrA[i] = (f4){0.f, 0.f, 0.f, 0.f};
+  ws.corrZ = (f4){0.f, 0.f, 0.f, 0.f};
+  ws.m_run = -INFINITY;
+
+  dispatch<FAM, NA, MAXB, DEPTH>(bk, bv, g, blo + wave, bhi, my_slots, a.slot_bytes, lo, cst, ws);
+
+  // ---- this wave's result per query row: (m, l, out[128]) in canonical form
+  const int r = lo.r, col = lo.col, GP = a.GP;
+  constexpr int GPA = 4 / NA;
+  float zt[4][4], lrow[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+#pragma unroll
+    for (int gg = 0; gg < 4; ++gg) zt[gg][i] = __shfl(ws.corrZ[i], r * 16 + gg, kWave);
+    lrow[i] = __shfl(ws.corrZ[i], r * 16 + (FAM == RQ_KIVI ? 4 : 0), kWave);
+  }
+  float mrow[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) mrow[i] = __shfl(ws.m_run, (4 * r + i) & (GP - 1), kWave);
+  __syncthreads();   // every wave is done with its slot
+  float* mw = merge + (size_t)wave * G * (2 + kD);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = 4 * r + i, jj = row & (GP - 1), gs = row / GP;
+    if (jj < G) {
+      if (FAM == RQ_KIVI) {
+#pragma unroll
+        for (int nt = 0; nt < 8; ++nt) {
+          const int gt = nt / 2, at = gt / GPA;
+          if (gs == gt % GPA)
+            mw[jj * (2 + kD) + 2 + 16 * nt + col] =
+                ws.acc[nt][i] + ws.corrA[at][i] + zt[gt][i];
+        }
+        if (gs == 0 && col == 0) {
+          mw[jj * (2 + kD)] = mrow[i];
+          mw[jj * (2 + kD) + 1] = lrow[i];
+        }
+      } else if (gs == 0) {
+#pragma unroll
+        for (int nt = 0; nt < 8; ++nt)
+          mw[jj * (2 + kD) + 2 + 16 * nt + col] = ws.acc[nt][i] + ws.corrA[0][i];
+        if (col == 0) {
+          mw[jj * (2 + kD)] = mrow[i];
+          mw[jj * (2 + kD) + 1] = lrow[i];
+        }
+      }
+    }
+  }
+  __syncthreads();
+  float* dst = part_ptr(a, unit, slot);
+  for (int e = tid; e < G * kD; e += kThreads) {
+    const int j = e / kD, cc = e % kD;
+    float M = -INFINITY;
+    for (int w = 0; w < kWaves; ++w) M = __builtin_fmaxf(M, merge[(w * G + j) * (2 + kD)]);
+    float acc = 0.0f, l = 0.0f;
+    for (int w = 0; w < kWaves; ++w) {
+      const float* src = merge + (size_t)(w * G + j) * (2 + kD);
+      const float f = (src[0] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(src[0] - M);
+      acc = __builtin_fmaf(f, src[2 + cc], acc);
+      l = __builtin_fmaf(f, src[1], l);
+    }
+    dst[j * (2 + kD) + 2 + cc] = acc;
+    if (cc == 0) {
+      dst[j * (2 + kD)] = M;
+      dst[j * (2 + kD) + 1] = l;
+    }
+  }
+}
+
+// FAM: quantizer family; NA: A operands of the KIVI value side (G <= 4: 1,
+// G <= 8: 2, else 4); MAXB: largest bit-width handled (4 or 8).
+template <int FAM, int NA, int MAXB>
+__global__ void __launch_bounds__(kThreads, kAttnOcc)
+attn_kernel(AttnLaunch a) {
+  __shared__ u4 cst4[2];             // fp16 ones (4 dwords), zeros (4 dwords)
+  uint32_t* cst = reinterpret_cast<uint32_t*>(cst4);
+  // one area used in turn for the per-wave block slots while streaming and
+  // the wave merge area [kWaves][G][2 + 128] floats; behind it the query
+  // rows (float [16][128]) and their 16-bit copy (uint16 [16][128])
+  extern __shared__ u4 dyn[];
+  uint8_t* slots = reinterpret_cast<uint8_t*>(dyn);
+  float* merge = reinterpret_cast<float*>(dyn);
+  float (*qs)[kD] = reinterpret_cast<float (*)[kD]>(slots + a.area_bytes);
+  uint16_t* qraw = reinterpret_cast<uint16_t*>(slots + a.area_bytes + 16 * kD * sizeof(float));
+  const int slot = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+
+  if (slot < a.n_wg) stream_slot<FAM, NA, MAXB>(a, slot, h, b, qs, qraw, cst, slots, merge);
+}
+
+}  // namespace
+
+}  // namespace rq
+
+// Defines hipError_t NAME(const AttnLaunch&, size_t lds, hipStream_t):
+// launches attn_kernel<FAM, NA, MAXB> over the unit grid.
+#define RQ_DEFINE_ATTN_LAUNCHER(FAM, NA, MAXB, NAME)                            \
+  namespace rq {                                                                \
+  hipError_t NAME(const AttnLaunch& a, size_t lds, hipStream_t s) {             \
+    dim3 grid(a.n_wg > 0 ? a.n_wg : 1, a.H, a.B);                               \
+    hipLaunchKernelGGL((attn_kernel<FAM, NA, MAXB>), grid, dim3(kThreads), lds, \
+                       s, a);                                                   \
+    return hipGetLastError();                                                   \
+  }                                                                             \
+  }

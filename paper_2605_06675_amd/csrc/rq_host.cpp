@@ -114,6 +114,23 @@ rq::LayerTable layer_table(const rq_cache* c, int layer) {
   return t;
 }
 
+// LDS bytes a workgroup may allocate on the current device (queried once;
+// 64 KiB when no device can be queried).
+size_t lds_limit() {
+  static size_t n = 0;
+  if (n == 0) {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) ==
+            hipSuccess &&
+        v > 0)
+      n = (size_t)v;
+    else
+      n = 65536;
+  }
+  return n;
+}
+
 struct SplitPlan {
   int nq, n_wg, blk_per_wg;
 };
@@ -136,9 +153,9 @@ int cu_count() {
 }
 
 // Workgroups (four waves each) per (batch, kv-head) unit.  The grid is sized
-// to one resident round: wg_per_cu workgroups per CU (the attention kernel
-// for widths <= 4 bits runs three waves per SIMD, i.e. three workgroups per
-// CU; the 8-bit one two), counting each unit's residual-window workgroup.
+// to one resident round with every CU busy: three workgroups per CU (the
+// attention kernel runs three waves per SIMD), split evenly over the units;
+// the last workgroup of a unit also takes its residual window.
 SplitPlan plan_splits(const rq_cache* c, int n_tokens, int wg_per_cu = 3) {
   SplitPlan p;
   p.nq = n_quantized(n_tokens, c->residual);
@@ -149,10 +166,10 @@ SplitPlan plan_splits(const rq_cache* c, int n_tokens, int wg_per_cu = 3) {
   if (env && std::atoi(env) > 0) {
     per = std::atoi(env);
   } else {
-    long slots = (long)cu_count() * wg_per_cu / units - 1;
-    if (slots < 1) slots = 1;
-    per = (nblk + slots - 1) / slots;
-    if (per < 8) per = 8;
+    long target = (long)cu_count() * wg_per_cu / units;
+    if (target < 1) target = 1;
+    per = (nblk + target - 1) / target;
+    if (per < 4) per = 4;
     per = (per + 3) / 4 * 4;
   }
   p.blk_per_wg = (int)per;
@@ -281,7 +298,7 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
     maxb = vb > maxb ? vb : maxb;
     maxkv = kb + vb > maxkv ? kb + vb : maxkv;
   }
-  const SplitPlan p = plan_splits(c, n_tokens, maxb <= 4 ? 3 : 2);
+  const SplitPlan p = plan_splits(c, n_tokens);
   const uint64_t need = attn_ws_bytes(c, p);
   if (ws_bytes < need)
     return fail(RQ_ESMALLWS, "workspace %llu bytes < %llu needed",
@@ -297,6 +314,8 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
   a.B = c->batch;
   a.H = c->n_kv_heads;
   a.G = G;
+  a.GP = 1;
+  while (a.GP < G) a.GP *= 2;
   a.cap = c->capacity;
   a.R = c->residual;
   a.nq = p.nq;
@@ -308,6 +327,14 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
   a.qscale = scale * 1.4426950408889634f;
   a.tab = tab;
   a.slot_bytes = 512 * maxkv + 2 * meta_per_block(c);
+  a.area_bytes = (int)rq::attention_area_bytes(G, a.slot_bytes, maxb);
+  size_t lds = rq::attention_lds_bytes(G, a.slot_bytes, maxb);
+  const size_t clds = rq::combine_lds_bytes(G, p.n_wg);
+  lds = lds > clds ? lds : clds;
+  if (lds > lds_limit())
+    return fail(RQ_EUNSUPPORTED,
+                "layer %d needs %zu bytes of LDS per workgroup (device limit %zu): "
+                "K+V bit-widths of one kv-head are too wide", layer, lds, lds_limit());
   hipError_t e = rq::launch_attention(a, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "attention launch");
   return ok();

@@ -48,11 +48,14 @@ struct AttnLaunch {
   const uint8_t* meta;    // this layer
   const uint16_t* resid;  // this layer
   float* out;             // [B][Hq][128]
-  float* part;            // [B][H][n_wg + 1][G][2 + 128] (max, sum, acc)
+  float* part;            // [B][H][n_wg + 1][G][2 + 128] (max, sum, acc);
+                          // slot n_wg is unused (the window stays in LDS)
   int B, H, G, cap, R;
+  int GP;                 // smallest power of two >= G
   int nq, n_tokens;
   int n_wg, blk_per_wg;   // workgroups per unit streaming blocks
   int slot_bytes;         // LDS bytes per wave for one block of this layer
+  int area_bytes;         // LDS bytes of the slot/merge/staging area
   int is_bf16, family;
   float qscale;           // scale * log2(e)
   LayerTable tab;
@@ -69,6 +72,12 @@ struct CalibLaunch {
 hipError_t launch_quantize(const QuantLaunch& a, hipStream_t s);
 hipError_t launch_ring(const RingLaunch& a, hipStream_t s);
 hipError_t launch_attention(const AttnLaunch& a, hipStream_t s);
+// LDS bytes of the attention kernel for a layer (query rows, block slots
+// and merge area share one allocation)
+size_t attention_area_bytes(int G, int slot_bytes, int maxb);
+size_t attention_lds_bytes(int G, int slot_bytes, int maxb);
+// LDS bytes of the merge kernel
+size_t combine_lds_bytes(int G, int n_wg);
 hipError_t launch_calibrate(const CalibLaunch& a, hipStream_t s);
 
 }  // namespace rq
