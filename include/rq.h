@@ -148,9 +148,11 @@ rq_status rq_decode_workspace(const rq_cache* c, int32_t n_tokens,
  * K_hat/V_hat the dequantized prefix plus the 16-bit window, query head j
  * reading kv-head j / (n_q_heads / n_kv_heads).  q: device
  * [batch][n_q_heads][128] in dtype; out: device fp32, same shape; ws:
- * device scratch of at least rq_decode_workspace bytes for per-call
- * partial results (contents on entry do not matter; calls that share a
- * workspace must not overlap).  Asynchronous. */
+ * device scratch of at least rq_decode_workspace bytes.  Its first
+ * 4 * batch * n_kv_heads bytes are arrival counters that must be zero
+ * before the first call on a workspace (zero the whole buffer once); every
+ * call leaves them zero again.  The rest holds per-call partial results.
+ * Calls that share a workspace must not overlap.  Asynchronous. */
 rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
                               int32_t n_tokens, const void* q, float* out,
                               float scale, void* ws, uint64_t ws_bytes,

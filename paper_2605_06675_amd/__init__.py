@@ -254,7 +254,9 @@ class KVCache:
         import torch
         need = rq_decode_workspace(self.desc, n_tokens)
         if self._ws is None or self._ws.numel() < need:
-            self._ws = torch.empty(need, dtype=torch.uint8,
+            # zeroed once: the arrival counters at its start must be zero
+            # before the first call (every call leaves them zero)
+            self._ws = torch.zeros(need, dtype=torch.uint8,
                                    device=self.codes.device)
         return self._ws
 

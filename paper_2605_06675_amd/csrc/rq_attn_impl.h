@@ -3,8 +3,11 @@
 //
 // Grid (workgroup slot, kv-head, batch), four waves per workgroup.  Slots
 // 0 .. n_wg-1 stream the quantized 32-token blocks of their (batch, kv-head)
-// unit (about three workgroups per CU in all).  The 16-bit residual window
-// is attended to by the kernel that merges the partials.  A wave streams every
+// unit (about three workgroups per CU in all); the last slot, given fewer
+// blocks, also attends to the 16-bit residual window.  Each workgroup
+// writes a partial (max, sum, acc) with cache-coherent stores and takes a
+// ticket from a per-unit counter; the last to arrive merges the unit's
+// partials and writes the output (QuaRot: rotated back).  A wave streams every
 // fourth block of its slot's range: the block's bytes (codes and metadata)
 // are fetched two blocks ahead with 1 KB-per-instruction loads and copied
 // into the wave's LDS slot, from where each lane reads its MFMA operands.
@@ -28,9 +31,7 @@
 // Softmax runs in the log2 domain with a lazily moved maximum (it moves
 // only when a block exceeds it by 2^4), so probabilities stay <= 16.
 //
-// A workgroup merges its waves in LDS and writes one partial (max, sum,
-// acc); a second kernel merges each unit's partials and writes the output
-// (QuaRot: rotated back).
+
 #pragma once
 
 #include "rq_device.h"
@@ -158,6 +159,16 @@ __device__ __forceinline__ uint32_t and_or(uint32_t x, uint32_t mask, uint32_t c
 // lower planes of a code, whose bits are still zero in c)
 __device__ __forceinline__ uint32_t insert(uint32_t x, uint32_t mask, uint32_t c) {
   return (x & mask) | (c & ~mask);
+}
+
+// Stores and loads of the partial results, coherent across the GPU's L2
+// caches (agent scope), so that the workgroup that merges a unit's partials
+// sees the other workgroups' results without a cache flush.
+__device__ __forceinline__ void st_agent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_agent(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 __device__ __forceinline__ uint32_t pk_mul(uint32_t a, uint32_t b) {
@@ -719,11 +730,11 @@ __device__ __forceinline__ void residual_slot(const AttnLaunch& a, int b, int h,
     if (j >= a.G) break;
     float* d = dst + (size_t)j * (2 + kD);
     if (lane == 0) {
-      d[0] = m_run[q];
-      d[1] = l_run[q];
+      st_agent(d, m_run[q]);
+      st_agent(d + 1, l_run[q]);
     }
-    d[2 + 2 * lane] = ac0[q];
-    d[2 + 2 * lane + 1] = ac1[q];
+    st_agent(d + 2 + 2 * lane, ac0[q]);
+    st_agent(d + 2 + 2 * lane + 1, ac1[q]);
   }
 }
 
@@ -878,11 +889,102 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
       acc = __builtin_fmaf(f, src[2 + cc], acc);
       l = __builtin_fmaf(f, src[1], l);
     }
-    dst[j * (2 + kD) + 2 + cc] = acc;
+    st_agent(dst + j * (2 + kD) + 2 + cc, acc);
     if (cc == 0) {
-      dst[j * (2 + kD)] = M;
-      dst[j * (2 + kD) + 1] = l;
+      st_agent(dst + j * (2 + kD), M);
+      st_agent(dst + j * (2 + kD) + 1, l);
     }
+  }
+}
+
+// Merge the partials of one (batch, kv-head) unit and write its output:
+// slots 0 .. n_wg-1 hold the quantized blocks (QuaRot: rotated domain), slot
+// n_wg the 16-bit window (original domain).  Thread t owns output elements
+// t, t + 256, ... of the G x 128 rows, two at a time; it loads the (max,
+// sum, value) of both for eight slots at once, all loads in flight
+// together.  Whole workgroup; lds: scratch of 128 G floats (QuaRot).
+__device__ __forceinline__ void merge_unit(const AttnLaunch& a, size_t unit, float* lds) {
+  constexpr int kE = 2;   // elements per pass
+  constexpr int kS = 8;   // slots per batch of loads
+  const int tid = threadIdx.x;
+  const int G = a.G;
+  const int ns = a.n_wg + 1;
+  const bool quarot = a.family == RQ_QUAROT;
+  const size_t stride = (size_t)G * (2 + kD);
+  const float* base = part_ptr(a, unit, 0);
+  float* rot = lds;
+  float* out = a.out + unit * G * kD;   // (b, h) -> query rows h*G..
+  for (int e0 = tid; e0 < G * kD; e0 += kE * kThreads) {
+    float M[kE], den[kE], num[kE], tail[kE];
+#pragma unroll
+    for (int k = 0; k < kE; ++k) {
+      M[k] = -INFINITY;
+      den[k] = 0.0f;
+      num[k] = 0.0f;
+      tail[k] = 0.0f;
+    }
+    for (int s0 = 0; s0 < ns; s0 += kS) {
+      float m[kS][kE], l[kS][kE], v[kS][kE];
+#pragma unroll
+      for (int i = 0; i < kS; ++i)
+#pragma unroll
+        for (int k = 0; k < kE; ++k) {
+          const int e = e0 + k * kThreads;
+          m[i][k] = -INFINITY;
+          l[i][k] = 0.0f;
+          v[i][k] = 0.0f;
+          if (s0 + i < ns && e < G * kD) {
+            const float* src = base + (s0 + i) * stride + (e / kD) * (2 + kD);
+            m[i][k] = ld_agent(src);
+            l[i][k] = ld_agent(src + 1);
+            v[i][k] = ld_agent(src + 2 + e % kD);
+          }
+        }
+#pragma unroll
+      for (int i = 0; i < kS; ++i)
+#pragma unroll
+        for (int k = 0; k < kE; ++k) {
+          if (!(l[i][k] > 0.0f)) continue;
+          const float mn = __builtin_fmaxf(M[k], m[i][k]);
+          const float fo = __builtin_amdgcn_exp2f(M[k] - mn);
+          const float fi = __builtin_amdgcn_exp2f(m[i][k] - mn);
+          M[k] = mn;
+          den[k] = __builtin_fmaf(den[k], fo, fi * l[i][k]);
+          // the window slot (ns - 1) is in the original domain: kept apart
+          const bool win = s0 + i == ns - 1;
+          num[k] = num[k] * fo + (win ? 0.0f : fi * v[i][k]);
+          tail[k] = tail[k] * fo + (win ? fi * v[i][k] : 0.0f);
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < kE; ++k) {
+      const int e = e0 + k * kThreads;
+      if (e < G * kD) {
+        if (quarot) {
+          rot[e] = num[k];
+          rot[G * kD + e] = tail[k] / den[k];
+          rot[2 * G * kD + e] = 1.0f / den[k];
+        } else {
+          out[e] = (num[k] + tail[k]) / den[k];
+        }
+      }
+    }
+  }
+  if (quarot) {
+    // rotate the quantized-domain sums back: x = H y / sqrt(128)
+    __syncthreads();
+    for (int hh = 1; hh < kD; hh *= 2) {
+      for (int e = tid; e < G * (kD / 2); e += kThreads) {
+        const int j = e / (kD / 2), i = e % (kD / 2);
+        const int bse = (i / hh) * 2 * hh + (i % hh);
+        const float x = rot[j * kD + bse], y = rot[j * kD + bse + hh];
+        rot[j * kD + bse] = x + y;
+        rot[j * kD + bse + hh] = x - y;
+      }
+      __syncthreads();
+    }
+    for (int e = tid; e < G * kD; e += kThreads)
+      out[e] = rot[e] * kInvSqrtD * rot[2 * G * kD + e] + rot[G * kD + e];
   }
 }
 
@@ -902,8 +1004,33 @@ attn_kernel(AttnLaunch a) {
   float (*qs)[kD] = reinterpret_cast<float (*)[kD]>(slots + a.area_bytes);
   uint16_t* qraw = reinterpret_cast<uint16_t*>(slots + a.area_bytes + 16 * kD * sizeof(float));
   const int slot = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const size_t unit = (size_t)b * a.H + h;
+  const int nwg = a.n_wg > 0 ? a.n_wg : 1;
 
   if (slot < a.n_wg) stream_slot<FAM, NA, MAXB>(a, slot, h, b, qs, qraw, cst, slots, merge);
+  // the unit's last workgroup (given fewer blocks) also attends to the
+  // 16-bit residual window
+  if (slot == nwg - 1) {
+    const u4 qpiece = query_piece(a, b, h);
+    __syncthreads();   // the merge area and the query rows are read until here
+    store_queries(a, qpiece, false, qs);
+    residual_slot(a, b, h, qs, reinterpret_cast<uint16_t*>(slots), part_ptr(a, unit, a.n_wg));
+  }
+  // publish this workgroup's partials, then take a ticket; the last
+  // workgroup of the unit merges and leaves the counter at zero for the
+  // next call
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  __shared__ uint32_t ticket;
+  if (threadIdx.x == 0)
+    ticket = __hip_atomic_fetch_add(a.counters + unit, 1u, __ATOMIC_RELAXED,
+                                    __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();
+  if (ticket == (uint32_t)(nwg - 1)) {
+    merge_unit(a, unit, merge);
+    if (threadIdx.x == 0)
+      __hip_atomic_store(a.counters + unit, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
 }
 
 }  // namespace

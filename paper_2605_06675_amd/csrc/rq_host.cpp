@@ -131,6 +131,8 @@ size_t lds_limit() {
   return n;
 }
 
+constexpr long kResidualBlocks = 12;
+
 struct SplitPlan {
   int nq, n_wg, blk_per_wg;
 };
@@ -166,21 +168,29 @@ SplitPlan plan_splits(const rq_cache* c, int n_tokens, int wg_per_cu = 3) {
   if (env && std::atoi(env) > 0) {
     per = std::atoi(env);
   } else {
+    // the last workgroup of a unit also attends to the residual window,
+    // which costs about as much as kResidualBlocks quantized blocks
     long target = (long)cu_count() * wg_per_cu / units;
     if (target < 1) target = 1;
-    per = (nblk + target - 1) / target;
+    const long work = nblk + (nblk > 0 ? kResidualBlocks : 0);
+    per = (work + target - 1) / target;
     if (per < 4) per = 4;
-    per = (per + 3) / 4 * 4;
   }
   p.blk_per_wg = (int)per;
   p.n_wg = nblk == 0 ? 0 : (int)((nblk + per - 1) / per);
   return p;
 }
 
+// Workspace: per-unit arrival counters (zero between calls), padded to 256
+// bytes, then the partials [B][H][n_wg + 1][G][2 + 128] floats.
+uint64_t attn_counter_bytes(const rq_cache* c) {
+  return ((uint64_t)c->batch * c->n_kv_heads * sizeof(uint32_t) + 255) / 256 * 256;
+}
+
 uint64_t attn_ws_bytes(const rq_cache* c, const SplitPlan& p) {
   const uint64_t G = c->n_q_heads / c->n_kv_heads;
   const uint64_t parts = (uint64_t)c->batch * c->n_kv_heads * (p.n_wg + 1);
-  return parts * G * (2 + rq::kD) * sizeof(float);
+  return attn_counter_bytes(c) + parts * G * (2 + rq::kD) * sizeof(float);
 }
 
 }  // namespace
@@ -310,7 +320,8 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
   a.meta = static_cast<const uint8_t*>(c->meta) + meta_layer_bytes(c) * layer;
   a.resid = static_cast<const uint16_t*>(c->resid) + resid_layer_elems(c) * layer;
   a.out = out;
-  a.part = static_cast<float*>(ws);
+  a.counters = static_cast<uint32_t*>(ws);
+  a.part = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + attn_counter_bytes(c));
   a.B = c->batch;
   a.H = c->n_kv_heads;
   a.G = G;
@@ -327,10 +338,8 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
   a.qscale = scale * 1.4426950408889634f;
   a.tab = tab;
   a.slot_bytes = 512 * maxkv + 2 * meta_per_block(c);
-  a.area_bytes = (int)rq::attention_area_bytes(G, a.slot_bytes, maxb);
-  size_t lds = rq::attention_lds_bytes(G, a.slot_bytes, maxb);
-  const size_t clds = rq::combine_lds_bytes(G, p.n_wg);
-  lds = lds > clds ? lds : clds;
+  a.area_bytes = (int)rq::attention_area_bytes(G, a.slot_bytes, maxb, p.n_wg);
+  const size_t lds = rq::attention_lds_bytes(G, a.slot_bytes, maxb, p.n_wg);
   if (lds > lds_limit())
     return fail(RQ_EUNSUPPORTED,
                 "layer %d needs %zu bytes of LDS per workgroup (device limit %zu): "

@@ -49,7 +49,8 @@ struct AttnLaunch {
   const uint16_t* resid;  // this layer
   float* out;             // [B][Hq][128]
   float* part;            // [B][H][n_wg + 1][G][2 + 128] (max, sum, acc);
-                          // slot n_wg is unused (the window stays in LDS)
+                          // slot n_wg: the residual window
+  uint32_t* counters;     // [B][H] arrival counters, zero between calls
   int B, H, G, cap, R;
   int GP;                 // smallest power of two >= G
   int nq, n_tokens;
@@ -74,10 +75,8 @@ hipError_t launch_ring(const RingLaunch& a, hipStream_t s);
 hipError_t launch_attention(const AttnLaunch& a, hipStream_t s);
 // LDS bytes of the attention kernel for a layer (query rows, block slots
 // and merge area share one allocation)
-size_t attention_area_bytes(int G, int slot_bytes, int maxb);
-size_t attention_lds_bytes(int G, int slot_bytes, int maxb);
-// LDS bytes of the merge kernel
-size_t combine_lds_bytes(int G, int n_wg);
+size_t attention_area_bytes(int G, int slot_bytes, int maxb, int n_wg);
+size_t attention_lds_bytes(int G, int slot_bytes, int maxb, int n_wg);
 hipError_t launch_calibrate(const CalibLaunch& a, hipStream_t s);
 
 }  // namespace rq
