@@ -653,11 +653,13 @@ constexpr int kResRow = 136;   // uint16 per padded row
 constexpr size_t kResLds = (size_t)2 * kResTok * kResRow * sizeof(uint16_t);
 
 // 16-bit residual window of one unit, original domain.  The window is read
-// in chunks of 64 tokens staged in LDS with coalesced 16-byte loads; wave w
-// takes query rows w, w+4, ...; lane = token for the scores, lane = channel
-// pair for PV.  stage: LDS for the chunk (kResLds bytes), qs: query rows.
+// in chunks of 64 tokens staged in LDS; the loads of the next chunk (and of
+// the queries, before the first) are in flight while a chunk is computed.
+// Wave w takes query rows w, w+4, ...; lane = token for the scores, lane =
+// channel pair for PV.  stage: LDS for one chunk (kResLds bytes), qs: LDS
+// for the query rows.
 __device__ __forceinline__ void residual_slot(const AttnLaunch& a, int b, int h,
-                                              const float (*qs)[kD], uint16_t* stage,
+                                              float (*qs)[kD], uint16_t* stage,
                                               float* dst) {
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid & (kWave - 1);
   const int cap = a.R + kChunk;
@@ -665,6 +667,23 @@ __device__ __forceinline__ void residual_slot(const AttnLaunch& a, int b, int h,
   const uint16_t* vb = a.resid + (((size_t)b * a.H + h) * 2 + 1) * cap * kD;
   uint16_t* ks = stage;
   uint16_t* vs = stage + kResTok * kResRow;
+  // a chunk is 64 tokens x 16 pieces of 16 bytes: four pieces per thread
+  u4 kr[4], vr[4];
+  auto load_chunk = [&](int t0) {
+    const int n = (a.n_tokens - t0) < kResTok ? (a.n_tokens - t0) : kResTok;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int e = tid + i * kThreads, t = e >> 4, piece = e & 15;
+      if (t < n) {
+        const size_t row = (size_t)((t0 + t) % cap) * kD + piece * 8;
+        kr[i] = *reinterpret_cast<const u4*>(kb + row);
+        vr[i] = *reinterpret_cast<const u4*>(vb + row);
+      }
+    }
+  };
+  const u4 qpiece = query_piece(a, b, h);
+  if (a.nq < a.n_tokens) load_chunk(a.nq);
+  store_queries(a, qpiece, false, qs);
   float m_run[4], l_run[4], ac0[4], ac1[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
@@ -675,13 +694,16 @@ __device__ __forceinline__ void residual_slot(const AttnLaunch& a, int b, int h,
   }
   for (int t0 = a.nq; t0 < a.n_tokens; t0 += kResTok) {
     const int n = (a.n_tokens - t0) < kResTok ? (a.n_tokens - t0) : kResTok;
-    for (int e = tid; e < n * 16; e += kThreads) {
-      const int t = e >> 4, piece = e & 15;
-      const size_t row = (size_t)((t0 + t) % cap) * kD + piece * 8;
-      *reinterpret_cast<u4*>(ks + t * kResRow + piece * 8) = *reinterpret_cast<const u4*>(kb + row);
-      *reinterpret_cast<u4*>(vs + t * kResRow + piece * 8) = *reinterpret_cast<const u4*>(vb + row);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int e = tid + i * kThreads, t = e >> 4, piece = e & 15;
+      if (t < n) {
+        *reinterpret_cast<u4*>(ks + t * kResRow + piece * 8) = kr[i];
+        *reinterpret_cast<u4*>(vs + t * kResRow + piece * 8) = vr[i];
+      }
     }
     __syncthreads();
+    if (t0 + kResTok < a.n_tokens) load_chunk(t0 + kResTok);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int j = wave + kWaves * q;
@@ -689,10 +711,10 @@ __device__ __forceinline__ void residual_slot(const AttnLaunch& a, int b, int h,
       float s = -INFINITY;
       if (lane < n) {
         s = 0.0f;
-        const u4* kr = reinterpret_cast<const u4*>(ks + lane * kResRow);
+        const u4* krow = reinterpret_cast<const u4*>(ks + lane * kResRow);
 #pragma unroll 4
         for (int c8 = 0; c8 < kD / 8; ++c8) {
-          const u4 w = kr[c8];
+          const u4 w = krow[c8];
           const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
@@ -1011,9 +1033,7 @@ attn_kernel(AttnLaunch a) {
   // the unit's last workgroup (given fewer blocks) also attends to the
   // 16-bit residual window
   if (slot == nwg - 1) {
-    const u4 qpiece = query_piece(a, b, h);
     __syncthreads();   // the merge area and the query rows are read until here
-    store_queries(a, qpiece, false, qs);
     residual_slot(a, b, h, qs, reinterpret_cast<uint16_t*>(slots), part_ptr(a, unit, a.n_wg));
   }
   // publish this workgroup's partials, then take a ticket; the last
