@@ -9,7 +9,7 @@ two share no code (only the seeded input generators in ``workloads``).
 Modules
   fit        distortion model D(b) = alpha * beta^-b, log-linear OLS
   alloc      reverse waterfilling, greedy integer allocation, brute force
-  lloydmax   Lloyd-Max scalar quantizer of N(0,1)
+  lloydmax   Lloyd-Max scalar quantizer of N(0,1) (the TurboQuant codebook)
   fmt        fp16/bf16 rounding helpers and the packed code format
   quant      KIVI-, QuaRot- and TurboQuant-style quantize / dequantize
   cache      residual-window rule and packed-cache assembly for one unit

@@ -18,6 +18,7 @@ see ``fmt`` for chunks and pair order):
            K: [chunk q][s(32, pair order), z(32, pair order)]  fp16
            V: [channel group cg][s(32 tokens, pair order), z(...)]  fp16
   QuaRot meta, per block: [32 tokens, pair order] fp16 scale
+  TurboQuant meta, per block: [32 tokens, pair order] fp16 norm
 """
 import numpy as np
 
@@ -83,7 +84,9 @@ class Unit:
     """Oracle cache of one unit, built from the first T tokens of k, v
     (float32 [T][128], exact values of the 16-bit inputs)."""
 
-    def __init__(self, family, k, v, bk, bv, R):
+    def __init__(self, family, k, v, bk, bv, R, rotation=None):
+        """rotation: the (layer, kv-head) rotation for TurboQuant (float64
+        [128][128], the exact bf16 values), else None."""
         self.family, self.bk, self.bv, self.R = family, bk, bv, R
         T = k.shape[0]
         self.T = T
@@ -103,6 +106,13 @@ class Unit:
             self.v_hat = quant.quarot_dequant(uv, sv, bv)
             self.k_meta = token_meta(sk)
             self.v_meta = token_meta(sv)
+        elif family == TURBO:
+            uk, nk, self.k_t = quant.turbo_quant(kq, rotation, bk)
+            uv, nv, self.v_t = quant.turbo_quant(vq, rotation, bv)
+            self.k_hat = quant.turbo_dequant(uk, nk, rotation, bk)
+            self.v_hat = quant.turbo_dequant(uv, nv, rotation, bv)
+            self.k_meta = token_meta(nk)
+            self.v_meta = token_meta(nv)
         else:
             raise NotImplementedError(family)
         self.k_codes, self.v_codes = uk, uv

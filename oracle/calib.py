@@ -15,7 +15,7 @@ from . import quant
 KIVI, QUAROT, TURBO = 0, 1, 2
 
 
-def roundtrip(family, x, b, is_value):
+def roundtrip(family, x, b, is_value, rotation=None):
     if family == KIVI:
         if is_value:
             u, s, z = quant.kivi_quant_values(x, b)
@@ -25,16 +25,21 @@ def roundtrip(family, x, b, is_value):
     if family == QUAROT:
         u, s = quant.quarot_quant(x, b)
         return quant.quarot_dequant(u, s, b)
+    if family == TURBO:
+        u, n, _ = quant.turbo_quant(x, rotation, b)
+        return quant.turbo_dequant(u, n, rotation, b)
     raise NotImplementedError(family)
 
 
-def sweep(family, x, bits, is_value):
-    """x: float32[n_comp][T][128] -> D float64[n_comp][len(bits)]."""
+def sweep(family, x, bits, is_value, rotations=None):
+    """x: float32[n_comp][T][128] -> D float64[n_comp][len(bits)].
+    rotations: TurboQuant's per-component rotation [n_comp][128][128]."""
     x = np.asarray(x, dtype=np.float32)
     out = np.zeros((x.shape[0], len(bits)))
     for i in range(x.shape[0]):
         xi = x[i].astype(np.float64)
+        rot = None if rotations is None else rotations[i]
         for j, b in enumerate(bits):
-            xh = roundtrip(family, x[i], b, is_value)
+            xh = roundtrip(family, x[i], b, is_value, rot)
             out[i, j] = np.mean((xi - xh) ** 2)
     return out

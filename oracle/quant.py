@@ -4,8 +4,8 @@ The paper treats the base quantizer as a black box with a calibrated
 distortion curve (Sec. 3.4) and names three: KIVI (keys grouped per channel
 across tokens, values per token), QuaRot (a Hadamard rotation, then
 symmetric per-token quantization) and TurboQuant (a random rotation, then a
-per-coordinate codebook) -- Sec. 2, Appendix "Implementation Details" and
-"Quantizer Implementation".  It gives no rounding rules; the ones below are
+per-coordinate codebook) -- Sec. 2, Sec. 3.1, Appendix "Implementation
+Details" and "Quantizer Implementation".  It gives no rounding rules; the ones below are
 this library's readings (each is listed in the design notes) and both the
 oracle and the GPU kernels follow them bit for bit wherever a floating-point
 decision yields an integer code:
@@ -19,11 +19,12 @@ decision yields an integer code:
 Dequantization (used for attention and for the distortion sweep) is exact
 real arithmetic on the stored codes and metadata, evaluated in fp64.
 """
+import functools
 import math
 
 import numpy as np
 
-from . import fmt
+from . import fmt, lloydmax
 
 F32 = np.float32
 D = 128
@@ -150,3 +151,64 @@ def quarot_dequant(u, s, b):
     yhat = (np.asarray(u, np.float64) - (1 << (b - 1))) * np.asarray(
         s, np.float64)[..., None]
     return yhat @ hadamard() / math.sqrt(D)
+
+
+# --------------------------------------------------------------- TurboQuant
+# A random rotation spreads each vector's energy evenly over the coordinates,
+# which then follow (nearly) a Gaussian of variance |x|^2 / d; each rotated
+# coordinate, normalised by |x| / sqrt(d), is quantized with the Lloyd-Max
+# quantizer of N(0,1) at b bits (Sec. 2; Sec. 3.1, whose Table 6 lists that
+# quantizer's MSE).  Readings:
+#  * the rotation R is an input: one orthogonal matrix per (layer, kv-head),
+#    given as bf16 values (the workloads draw it from the Haar measure);
+#    y = R x with the exact products and sums (fp64 here);
+#  * the norm is stored per token as fp16: n = fp16(fp32(sqrt(sum x^2))),
+#    the sum and root taken in fp64;
+#  * t = y * sqrt(128) / n (t = 0 when n == 0) and the code is the number of
+#    thresholds below t, code = #{k : t > theta_k}, theta_k the fp32 midpoint
+#    of Lloyd-Max centroids k and k+1 (ties to the lower code);
+#  * dequantization: y_hat = c_code * n / sqrt(128), x_hat = R^T y_hat.
+SQRT_D = math.sqrt(128.0)
+
+
+@functools.lru_cache(maxsize=None)
+def turbo_codebook(b):
+    """(centroids fp64 [2^b], thresholds fp32 [2^b - 1]) of N(0,1)."""
+    c = lloydmax.centroids(b)
+    return c, lloydmax.thresholds_f32(c)
+
+
+def turbo_norm(x):
+    """fp16 norm of each row of x (float32 [T][128])."""
+    n = np.sqrt(np.sum(np.asarray(x, np.float64) ** 2, axis=-1))
+    return fmt.f16_sat(n.astype(np.float32))
+
+
+def turbo_quant(x, R, b):
+    """x float32 [T][128] (exact 16-bit values), R float64 [128][128].
+    Returns (codes int64 [T][128], n fp16 [T], t float64 [T][128])."""
+    x = np.asarray(x, dtype=np.float64)
+    R = np.asarray(R, dtype=np.float64)
+    y = x @ R.T                                   # y_t = R x_t
+    n = turbo_norm(x)
+    nf = n.astype(np.float64)
+    safe = np.where(nf > 0, nf, 1.0)
+    t = np.where(nf[:, None] > 0, y * SQRT_D / safe[:, None], 0.0)
+    _, th = turbo_codebook(b)
+    codes = np.sum(t[..., None] > th.astype(np.float64), axis=-1)
+    return codes.astype(np.int64), n, t
+
+
+def turbo_dequant(u, n, R, b):
+    """x_hat [T][128] (fp64) from codes, fp16 norms and the rotation."""
+    c, _ = turbo_codebook(b)
+    yhat = c[np.asarray(u)] * (np.asarray(n, np.float64)[:, None] / SQRT_D)
+    return yhat @ np.asarray(R, dtype=np.float64)   # x_hat_t = R^T y_hat_t
+
+
+def turbo_near_threshold(t, b, eps):
+    """Boolean mask of coordinates whose t lies within eps of a threshold
+    (where a computation in another precision may pick the adjacent code)."""
+    _, th = turbo_codebook(b)
+    d = np.min(np.abs(np.asarray(t)[..., None] - th.astype(np.float64)), axis=-1)
+    return d <= eps

@@ -160,6 +160,24 @@ def calib_cpu(n_comp, n_tokens, dtype, seed=42, key_outliers=True):
     return bits16_from_f32(x, dtype)
 
 
+def turbo_rotation(seed, layer, head, d=HEAD_DIM):
+    """Seeded random rotation of one (layer, kv-head) for the TurboQuant
+    quantizer: a Haar-distributed orthogonal matrix (QR of a Gaussian matrix,
+    the signs of R's diagonal folded into Q), rounded to bf16.  Returns the
+    uint16 bf16 bit patterns [d][d], row-major, used as y = R x."""
+    g = _rng(seed, 7, layer, head).standard_normal((d, d))
+    q, r = np.linalg.qr(g)
+    q = q * np.sign(np.diag(r))[None, :]
+    return bits16_from_f32(q.astype(np.float32), BF16)
+
+
+def turbo_rotations(wl: Workload, seed=42):
+    """Rotations of every (layer, kv-head): uint16 [L][H][128][128]."""
+    return np.stack([np.stack([turbo_rotation(seed, l, h)
+                               for h in range(wl.n_kv_heads)])
+                     for l in range(wl.n_layers)])
+
+
 def u16_to_f32(bits, dtype):
     """Exact widening of 16-bit patterns to float32."""
     bits = np.asarray(bits, dtype=np.uint16)
