@@ -34,6 +34,12 @@
  *             stages h = 1, 2, ..., 64 in that order; s = fp16(max|y| /
  *             (2^(b-1) - 1)); code = rint(clamp(y * fp32(1/s), -q, q)) +
  *             2^(b-1), q = 2^(b-1) - 1 (all codes 2^(b-1) when s == 0).
+ *      Turbo  n = fp16(fp32(|x|)) (sum of squares and root in fp64);
+ *             y = R x, t = y * (sqrt(128) / n) (0 when n == 0); code =
+ *             number of thresholds of the b-bit codebook below t.  y is
+ *             summed in fp32 on the matrix cores, so a coordinate whose t
+ *             lies within the rounding of that sum of a threshold may take
+ *             the neighbouring code; everything else is exact.
  *  - Packed chunk: 32 codes of one stream in exactly b uint32 words.  The
  *    code bits are split into planes of widths equal to the binary digits
  *    of b, widest first (3 -> 2+1, 5 -> 4+1, 6 -> 4+2, 7 -> 4+2+1); plane
@@ -54,6 +60,7 @@
  *                 order; K: group index = chunk q, entries = channels;
  *                 V: group index = channel group cg, entries = tokens.
  *         QuaRot: [l][h][kind][batch][block][s(32 tokens)] fp16, pair order.
+ *         Turbo:  [l][h][kind][batch][block][n(32 tokens)] fp16, pair order.
  *  resid  [l][batch][h][kind][R + 32][128] in the input dtype; token t of
  *         the 16-bit window lives in slot t mod (R + 32).
  *  Residual rule: with T tokens cached the quantized prefix is
@@ -86,6 +93,9 @@ typedef int32_t rq_status;
 
 #define RQ_MAX_KV_HEADS 32
 
+/* Floats of the TurboQuant codebook table filled by rq_turbo_codebook. */
+#define RQ_TURBO_TABLE_FLOATS (8 * 2 * 256)
+
 /* HIP stream handle, passed through as an opaque pointer. */
 typedef void* rq_stream;
 
@@ -94,7 +104,7 @@ typedef void* rq_stream;
  * "static lookup table", Appendix "Runtime Analysis"): host int8
  * [n_layers][n_kv_heads][2], K then V. */
 typedef struct rq_cache {
-  int32_t family;        /* RQ_KIVI or RQ_QUAROT                          */
+  int32_t family;        /* RQ_KIVI, RQ_QUAROT or RQ_TURBO                */
   int32_t dtype;         /* RQ_F16 or RQ_BF16: K/V/q input type           */
   int32_t n_layers;
   int32_t batch;
@@ -107,7 +117,23 @@ typedef struct rq_cache {
   void* codes;           /* device, >= codes_bytes                        */
   void* meta;            /* device, >= meta_bytes                         */
   void* resid;           /* device, >= resid_bytes                        */
+  /* RQ_TURBO only (NULL otherwise): device bf16 [n_layers][n_kv_heads]
+   * [128][128], the orthogonal rotation R of each (layer, kv-head),
+   * row-major, applied as y = R x; and the device copy of the table filled
+   * by rq_turbo_codebook. */
+  const void* rotation;
+  const float* codebook;
 } rq_cache;
+
+/* The per-coordinate codebook of the TurboQuant-style quantizer: the
+ * Lloyd-Max quantizer of N(0,1) with 2^b levels, b = 1..8 (Sec. 2;
+ * Sec. 3.1, Table 6).  Fills host float [8][2][256]: entry [b-1][0][k] is
+ * the decision threshold between levels k and k+1 (the fp32 rounding of the
+ * midpoint of the two centroids, k < 2^b - 1; +inf beyond), entry
+ * [b-1][1][k] centroid k (ascending, k < 2^b).  The caller copies the table
+ * to the device and passes it in rq_cache.codebook and to the sweep.  The
+ * first call computes it (about a second); later calls copy.  Host only. */
+rq_status rq_turbo_codebook(float* table);
 
 /* Library version (major*10000 + minor*100 + patch). */
 int32_t rq_version(void);
@@ -169,7 +195,9 @@ rq_status rq_calibrate_workspace(int32_t n_comp, int32_t n_tokens,
  *   mse[i][j] = mean over tokens and channels of (x - dequant(quant(x)))^2
  * with the key grouping (is_value = 0) or value grouping (is_value = 1) of
  * the family, measured in the unrotated domain; then alpha, beta, r2 as in
- * rq_fit_distortion.  mse, alpha, beta, r2: host arrays ([n_comp][n_bits]
+ * rq_fit_distortion.  rotation, codebook: RQ_TURBO only (NULL otherwise):
+ * device bf16 [n_comp][128][128], one rotation per component, and the
+ * device codebook table.  mse, alpha, beta, r2: host arrays ([n_comp][n_bits]
  * and [n_comp]); alpha/beta/r2 may be NULL to skip the fit.  ws: device
  * scratch of rq_calibrate_workspace bytes.  Synchronous: waits for the
  * stream and copies the results to the host. */
@@ -177,6 +205,7 @@ rq_status rq_calibrate_distortion(int32_t family, int32_t dtype,
                                   const void* x, int32_t n_comp,
                                   int32_t n_tokens, int32_t is_value,
                                   const int32_t* bits, int32_t n_bits,
+                                  const void* rotation, const float* codebook,
                                   double* mse, double* alpha, double* beta,
                                   double* r2, void* ws, uint64_t ws_bytes,
                                   rq_stream stream);

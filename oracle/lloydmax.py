@@ -5,7 +5,7 @@ The TurboQuant-style base quantizer maps each rotated coordinate to one of
 paper's Table 6 (Appendix "Distortion Model Validation") lists the exact MSE
 of that quantizer for unit-variance Gaussian data, b = 1..6.
 
-Lloyd's two conditions, iterated to a fixed point in fp64:
+Lloyd's two conditions, solved for their fixed point in fp64:
   thresholds are midpoints of adjacent centroids;
   each centroid is the conditional mean of N(0,1) on its cell,
       c_k = (phi(t_{k-1}) - phi(t_k)) / (Phi(t_k) - Phi(t_{k-1})).
@@ -25,26 +25,57 @@ def _cells(c):
     return np.concatenate(([-np.inf], t, [np.inf]))
 
 
-def centroids(b, iters=100000, tol=1e-15):
-    """2^b Lloyd-Max centroids of N(0,1), ascending (float64)."""
+def _upper_cells(u):
+    """Cells [a_k, b_k) of the upper-half centroids u (ascending, > 0): the
+    first starts at the symmetric midpoint 0, the last runs to infinity."""
+    mid = 0.5 * (u[1:] + u[:-1])
+    return np.concatenate(([0.0], mid)), np.concatenate((mid, [np.inf]))
+
+
+def _cell_means(a, b):
+    """Mean of N(0,1) on [a, b), 0 <= a < b, with its partial derivatives in
+    a and b.  Upper-tail probabilities avoid cancellation far out."""
+    pa, pb = _phi(a), np.where(np.isinf(b), 0.0, _phi(b))
+    mass = ndtr(-a) - ndtr(-b)
+    m = (pa - pb) / mass
+    dm_da = pa * (m - a) / mass
+    dm_db = np.where(np.isinf(b), 0.0, pb * (np.where(np.isinf(b), 0.0, b) - m) / mass)
+    return m, dm_da, dm_db
+
+
+def centroids(b, lloyd_iters=2000):
+    """2^b Lloyd-Max centroids of N(0,1), ascending (float64).
+
+    N(0,1) is symmetric, so the levels are +-u with u the upper half and the
+    middle threshold at 0.  Plain Lloyd iterations bring u near the fixed
+    point; they contract slowly at many levels, so Newton steps on the
+    fixed-point equations u_k = E[X | X in cell k] (a tridiagonal system,
+    since cell k's ends are the midpoints with u_{k-1} and u_{k+1}) finish
+    the solve to rounding level."""
     L = 1 << b
-    # start from equal-probability cell means
-    c = np.sort(np.array([0.0]) if L == 1 else
-                np.linspace(-1.0, 1.0, L) * (1.0 + 0.5 * b))
-    for _ in range(iters):
-        e = _cells(c)
-        pa, pb = _phi(e[:-1]), _phi(e[1:])
-        pa[0] = 0.0
-        pb[-1] = 0.0
-        mass = ndtr(e[1:]) - ndtr(e[:-1])
-        cn = (pa - pb) / mass
-        # exact symmetry of the standard normal: c_k = -c_{L-1-k}
-        cn = 0.5 * (cn - cn[::-1])
-        if np.max(np.abs(cn - c)) <= tol:
-            c = cn
+    h = L // 2
+    u = (np.arange(h) + 0.5) * (3.0 + 0.5 * b) / h
+    for _ in range(lloyd_iters):
+        u = _cell_means(*_upper_cells(u))[0]
+    for _ in range(100):
+        a, e = _upper_cells(u)
+        m, dm_da, dm_db = _cell_means(a, e)
+        F = u - m
+        # d m_k / d u_j: the lower end a_k = (u_{k-1} + u_k) / 2 for k >= 1,
+        # the upper end b_k = (u_k + u_{k+1}) / 2 for k < h - 1
+        J = np.eye(h)
+        for k in range(h):
+            if k >= 1:
+                J[k, k - 1] -= 0.5 * dm_da[k]
+                J[k, k] -= 0.5 * dm_da[k]
+            if k < h - 1:
+                J[k, k] -= 0.5 * dm_db[k]
+                J[k, k + 1] -= 0.5 * dm_db[k]
+        step = np.linalg.solve(J, F)
+        u = u - step
+        if np.max(np.abs(step)) <= 1e-16:
             break
-        c = cn
-    return c
+    return np.concatenate((-u[::-1], u))
 
 
 def mse(c):

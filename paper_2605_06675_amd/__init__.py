@@ -24,7 +24,8 @@ RQ_MAX_KV_HEADS = 32
 EXPORTS = ("rq_version", "rq_last_error", "rq_cache_sizes", "rq_region_offset",
            "rq_quantize_kv", "rq_decode_workspace", "rq_decode_attention",
            "rq_calibrate_workspace", "rq_calibrate_distortion",
-           "rq_fit_distortion", "rq_allocate_bits")
+           "rq_fit_distortion", "rq_allocate_bits", "rq_turbo_codebook")
+RQ_TURBO_TABLE_FLOATS = 8 * 2 * 256
 
 
 class RQError(RuntimeError):
@@ -40,7 +41,8 @@ class RqCache(C.Structure):
                 ("head_dim", C.c_int32), ("capacity", C.c_int32),
                 ("residual", C.c_int32), ("bits", C.POINTER(C.c_int8)),
                 ("codes", C.c_void_p), ("meta", C.c_void_p),
-                ("resid", C.c_void_p)]
+                ("resid", C.c_void_p), ("rotation", C.c_void_p),
+                ("codebook", C.c_void_p)]
 
 
 _lib = None
@@ -71,11 +73,12 @@ def lib():
                                           u64, vp]),
             "rq_calibrate_workspace": (i32, [i32, i32, i32, pu64]),
             "rq_calibrate_distortion": (i32, [i32, i32, vp, i32, i32, i32, pi,
-                                              i32, pd, pd, pd, pd, vp, u64,
-                                              vp]),
+                                              i32, vp, vp, pd, pd, pd, pd, vp,
+                                              u64, vp]),
             "rq_fit_distortion": (i32, [pd, i32, pi, i32, pd, pd, pd]),
             "rq_allocate_bits": (i32, [i32, pd, pd, pd, C.c_double, i32, i32,
                                        pi, pd, pd]),
+            "rq_turbo_codebook": (i32, [C.POINTER(C.c_float)]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)
@@ -146,6 +149,14 @@ def rq_allocate_bits(w, alpha, beta, avg_bits, bmin, bmax, want_cont=True):
     return bits, cont, J.value
 
 
+def rq_turbo_codebook():
+    """The TurboQuant codebook table, float32 [8][2][256]: [b-1][0] the
+    thresholds, [b-1][1] the centroids of the b-bit Lloyd-Max quantizer."""
+    t = np.empty(RQ_TURBO_TABLE_FLOATS, dtype=np.float32)
+    _check(lib().rq_turbo_codebook(t.ctypes.data_as(C.POINTER(C.c_float))))
+    return t.reshape(8, 2, 256)
+
+
 def rq_calibrate_workspace(n_comp, n_tokens, n_bits):
     v = C.c_uint64()
     _check(lib().rq_calibrate_workspace(n_comp, n_tokens, n_bits, C.byref(v)))
@@ -153,15 +164,19 @@ def rq_calibrate_workspace(n_comp, n_tokens, n_bits):
 
 
 def make_cache(family, dtype, n_layers, batch, n_kv_heads, n_q_heads,
-               capacity, residual, bits, codes=None, meta=None, resid=None):
-    """Fill an RqCache descriptor.  bits: int8 [n_layers][n_kv_heads][2].
-    The numpy bit table is kept alive on the returned object."""
+               capacity, residual, bits, codes=None, meta=None, resid=None,
+               rotation=None, codebook=None):
+    """Fill an RqCache descriptor.  bits: int8 [n_layers][n_kv_heads][2];
+    rotation, codebook: device tensors (TurboQuant only).  The numpy bit
+    table is kept alive on the returned object."""
     bt = np.ascontiguousarray(bits, dtype=np.int8).reshape(-1)
     c = RqCache(family, dtype, n_layers, batch, n_kv_heads, n_q_heads, 128,
                 capacity, residual, bt.ctypes.data_as(C.POINTER(C.c_int8)),
                 _tptr(codes) if codes is not None else None,
                 _tptr(meta) if meta is not None else None,
-                _tptr(resid) if resid is not None else None)
+                _tptr(resid) if resid is not None else None,
+                _tptr(rotation) if rotation is not None else None,
+                _tptr(codebook) if codebook is not None else None)
     c._bits = bt
     return c
 
@@ -206,10 +221,12 @@ def rq_decode_attention(cache, layer, n_tokens, q, out, ws, scale=None,
 
 
 def rq_calibrate_distortion(family, dtype, x, is_value, bits, ws=None,
-                            fit=True, stream=None):
-    """x: torch [n_comp][n_tokens][128] (device).  Returns
-    (mse[n_comp][n_bits], alpha, beta, r2) as numpy arrays (None when
-    fit is False)."""
+                            fit=True, rotation=None, codebook=None,
+                            stream=None):
+    """x: torch [n_comp][n_tokens][128] (device); rotation (bf16
+    [n_comp][128][128]) and codebook (float32 table) on the device for
+    TurboQuant.  Returns (mse[n_comp][n_bits], alpha, beta, r2) as numpy
+    arrays (None when fit is False)."""
     import torch
     n_comp, T = x.shape[0], x.shape[1]
     b, bp = _dptr(bits, np.int32)
@@ -222,7 +239,8 @@ def rq_calibrate_distortion(family, dtype, x, is_value, bits, ws=None,
     ptrs = [o.ctypes.data_as(dp) if o is not None else None for o in outs]
     _check(lib().rq_calibrate_distortion(
         family, dtype, _tptr(x), n_comp, T, int(bool(is_value)), bp, b.size,
-        mse.ctypes.data_as(dp), *ptrs, _tptr(ws),
+        _tptr(rotation), _tptr(codebook), mse.ctypes.data_as(dp), *ptrs,
+        _tptr(ws),
         ws.numel() * ws.element_size(), _stream(stream)))
     return (mse, *outs)
 

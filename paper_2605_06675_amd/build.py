@@ -13,7 +13,7 @@ CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "librq.so")
 BUILD = os.path.join(HERE, "_build")
 
-SOURCES = ["rq_host.cpp", "rq_alloc.cpp"] + sorted(
+SOURCES = ["rq_host.cpp", "rq_alloc.cpp", "rq_codebook.cpp"] + sorted(
     f for f in os.listdir(CSRC) if f.endswith(".hip"))
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -363,7 +363,8 @@ rq_status rq_calibrate_workspace(int32_t n_comp, int32_t n_tokens,
 rq_status rq_calibrate_distortion(int32_t family, int32_t dtype, const void* x,
                                   int32_t n_comp, int32_t n_tokens,
                                   int32_t is_value, const int32_t* bits,
-                                  int32_t n_bits, double* mse, double* alpha,
+                                  int32_t n_bits, const void* rotation,
+                                  const float* codebook, double* mse, double* alpha,
                                   double* beta, double* r2, void* ws,
                                   uint64_t ws_bytes, rq_stream stream) {
   if (family == RQ_TURBO)
@@ -419,6 +420,13 @@ rq_status rq_calibrate_distortion(int32_t family, int32_t dtype, const void* x,
       if (r2) r2[i] = rr[i];
     }
   }
+  return ok();
+}
+
+rq_status rq_turbo_codebook(float* table) {
+  if (!table) return fail(RQ_EINVAL, "table is NULL");
+  const float* t = rq::turbo_table();
+  for (int i = 0; i < RQ_TURBO_TABLE_FLOATS; ++i) table[i] = t[i];
   return ok();
 }
 

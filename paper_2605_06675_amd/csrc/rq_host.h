@@ -14,5 +14,7 @@ void waterfill(int n, const double* w, const double* alpha, const double* beta,
                int64_t B, int bmin, int bmax, double* out);
 void greedy(int n, const double* w, const double* alpha, const double* beta,
             int64_t B, int bmin, int bmax, int32_t* out);
+// TurboQuant codebook table, host float [8][2][256] (computed once)
+const float* turbo_table();
 
 }  // namespace rq

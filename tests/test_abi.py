@@ -188,19 +188,34 @@ def test_device_calls_validate_before_launch():
     # calibration
     b = (C.c_int32 * 2)(1, 2)
     m = (C.c_double * 4)()
-    assert L.rq_calibrate_distortion(rq.RQ_TURBO, 0, fake, 2, 64, 0, b, 2, m,
-                                     None, None, None, fake, 1 << 20,
+    assert L.rq_calibrate_distortion(rq.RQ_TURBO, 0, fake, 2, 64, 0, b, 2, None,
+                                     None, m, None, None, None, fake, 1 << 20,
                                      None) == rq.RQ_EUNSUPPORTED
-    assert L.rq_calibrate_distortion(rq.RQ_KIVI, 0, fake, 2, 60, 0, b, 2, m,
-                                     None, None, None, fake, 1 << 20,
+    assert L.rq_calibrate_distortion(rq.RQ_KIVI, 0, fake, 2, 60, 0, b, 2, None,
+                                     None, m, None, None, None, fake, 1 << 20,
                                      None) == rq.RQ_EINVAL
     b1 = (C.c_int32 * 2)(1, 1)
-    assert L.rq_calibrate_distortion(rq.RQ_KIVI, 0, fake, 2, 64, 0, b1, 2, m,
-                                     None, None, None, fake, 1 << 20,
+    assert L.rq_calibrate_distortion(rq.RQ_KIVI, 0, fake, 2, 64, 0, b1, 2, None,
+                                     None, m, None, None, None, fake, 1 << 20,
                                      None) == rq.RQ_EINVAL
-    assert L.rq_calibrate_distortion(rq.RQ_QUAROT, 0, fake, 2, 64, 0, b, 2, m,
-                                     None, None, None, fake, 1 << 20,
+    assert L.rq_calibrate_distortion(rq.RQ_QUAROT, 0, fake, 2, 64, 0, b, 2, None,
+                                     None, m, None, None, None, fake, 1 << 20,
                                      None) == rq.RQ_EINVAL
-    assert L.rq_calibrate_distortion(rq.RQ_KIVI, 0, fake, 2, 64, 0, b, 2, m,
-                                     None, None, None, fake, 8,
+    assert L.rq_calibrate_distortion(rq.RQ_KIVI, 0, fake, 2, 64, 0, b, 2, None,
+                                     None, m, None, None, None, fake, 8,
                                      None) == rq.RQ_ESMALLWS
+
+
+def test_turbo_codebook_matches_oracle():
+    # The library solves Lloyd-Max in its own C++; its fp32 thresholds are
+    # the ones the quantizer compares against, so they must equal the
+    # oracle's exactly, and the centroids agree to fp32 rounding.
+    from oracle import quant
+    tab = rq.rq_turbo_codebook()
+    for b in range(1, 9):
+        c, th = quant.turbo_codebook(b)
+        L = 1 << b
+        assert np.array_equal(tab[b - 1, 0, :L - 1], th), b
+        assert np.all(np.isinf(tab[b - 1, 0, L - 1:]))
+        np.testing.assert_allclose(tab[b - 1, 1, :L], c, rtol=2.0 ** -23)
+        assert np.all(tab[b - 1, 1, L:] == 0)

@@ -94,3 +94,22 @@ def test_lloydmax_monte_carlo(b):
     idx = np.searchsorted(0.5 * (c[1:] + c[:-1]), x)
     emp = np.mean((x - c[idx]) ** 2)
     assert abs(emp / lloydmax.mse(c) - 1) < 0.01
+
+
+@pytest.mark.parametrize("b", range(1, 9))
+def test_lloydmax_is_a_fixed_point_of_both_conditions(b):
+    # Lloyd's conditions define the quantizer: each centroid is the mean of
+    # N(0,1) over its cell, measured here by numerical integration on a fine
+    # grid (independent of the solver's closed-form cell means), and the
+    # centroids are symmetric.
+    from scipy import integrate
+    c = lloydmax.centroids(b)
+    assert np.array_equal(c, -c[::-1])
+    t = np.concatenate(([-np.inf], 0.5 * (c[1:] + c[:-1]), [np.inf]))
+    for k in range(len(c)):
+        lo, hi = max(t[k], -12.0), min(t[k + 1], 12.0)
+        pdf = lambda x: np.exp(-0.5 * x * x)
+        mass = integrate.quad(pdf, lo, hi, epsabs=0, epsrel=1e-13)[0]
+        first = integrate.quad(lambda x: x * pdf(x), lo, hi, epsabs=0,
+                               epsrel=1e-13)[0]
+        assert abs(first / mass - c[k]) < 1e-9 * max(1.0, abs(c[k]))
