@@ -81,11 +81,13 @@ def quantize_bytes(wl, bits_table, T):
 
 
 def cpu_baseline(wl, bits_table, seconds):
-    """The oracle (numpy), as it stands, on a bounded sample: decode
-    attention of whole (batch entry, kv-head) units of layer 0 read from the
-    oracle's own packed cache (unpack + dequantize + fp64 attention), units
-    added until the time budget is spent.  Returns the oracle-equivalent
-    effective GB/s over the same algorithmic bytes per unit."""
+    """The oracle (numpy), as it stands, on a bounded sample of the same
+    workload: whole (layer, batch entry, kv-head) units, each quantized
+    and packed by the oracle (its cache builder), then decode attention read
+    back from the packed codes (unpack + dequantize + fp64 attention).  Units
+    are added until the time budget is spent.  Reports the attention rate in
+    the metric's unit (algorithmic bytes / oracle attention time) and the
+    quantize rate in whole-model tokens per second."""
     from threadpoolctl import threadpool_limits
 
     import workloads
@@ -97,37 +99,79 @@ def cpu_baseline(wl, bits_table, seconds):
     R = wl.residual
     nq = max(0, ((T - R) // 32) * 32)
     G = wl.group
-    q16 = workloads.q_cpu(wl, 0)
-    done_bytes, spent, units = 0, 0.0, 0
+    att_bytes, t_att, t_q, units = 0, 0.0, 0.0, 0
     with threadpool_limits(limits=1):
-        h = 0
-        while spent < seconds and units < wl.batch * wl.n_kv_heads:
-            b = units % wl.batch
-            h = units // wl.batch % wl.n_kv_heads
-            k16, v16 = workloads.kv_cpu(wl, 0, b, T)
-            k = workloads.u16_to_f32(k16[h], wl.dtype)
-            v = workloads.u16_to_f32(v16[h], wl.dtype)
-            bk, bv = int(bits_table[0, h, 0]), int(bits_table[0, h, 1])
-            u = ocache.Unit(wl.family, k, v, bk, bv, R)   # builds the cache
-            q = workloads.u16_to_f32(q16[b, h * G:(h + 1) * G], wl.dtype)
-            t0 = time.perf_counter()
-            # decode attention from the packed representation
-            kc = ocache.unpack_keys(u.k_words, bk)
-            vc = ocache.unpack_values(u.v_words, bv)
-            ks = np.concatenate([oq.kivi_dequant_keys(
-                kc, *_kivi_meta_keys(u.k_meta)), u.k_res])
-            vs = np.concatenate([oq.kivi_dequant_values(
-                vc, *_kivi_meta_values(u.v_meta)), u.v_res])
-            oatt.decode_attention(q, ks, vs)
-            spent += time.perf_counter() - t0
-            units += 1
-            done_bytes += (nq * 128 * (bk + bv) // 8 + 2 * (nq // 32) * 512
-                           + 2 * (T - nq) * 256 + G * 128 * 6)
-    return {"value": round(done_bytes / spent / 1e9, 4), "unit": "GB/s",
+        for l, b in ((l, b) for l in range(wl.n_layers)
+                     for b in range(wl.batch)):
+            if t_att + t_q >= seconds:
+                break
+            q16 = workloads.q_cpu(wl, l)
+            k16, v16 = workloads.kv_cpu(wl, l, b, T)
+            for h in range(wl.n_kv_heads):
+                k = workloads.u16_to_f32(k16[h], wl.dtype)
+                v = workloads.u16_to_f32(v16[h], wl.dtype)
+                bk, bv = int(bits_table[l, h, 0]), int(bits_table[l, h, 1])
+                q = workloads.u16_to_f32(q16[b, h * G:(h + 1) * G], wl.dtype)
+                t0 = time.perf_counter()
+                u = ocache.Unit(wl.family, k, v, bk, bv, R)   # quantize + pack
+                t1 = time.perf_counter()
+                kc = ocache.unpack_keys(u.k_words, bk)
+                vc = ocache.unpack_values(u.v_words, bv)
+                ks = np.concatenate([oq.kivi_dequant_keys(
+                    kc, *_kivi_meta_keys(u.k_meta)), u.k_res])
+                vs = np.concatenate([oq.kivi_dequant_values(
+                    vc, *_kivi_meta_values(u.v_meta)), u.v_res])
+                oatt.decode_attention(q, ks, vs)
+                t2 = time.perf_counter()
+                t_q += t1 - t0
+                t_att += t2 - t1
+                units += 1
+                att_bytes += (nq * 128 * (bk + bv) // 8 + 2 * (nq // 32) * 512
+                              + 2 * (T - nq) * 256 + G * 128 * 6)
+    # a whole-model token is one token of every (layer, kv-head)
+    q_tok_s = units * T / (wl.n_layers * wl.n_kv_heads) / t_q
+    return {"value": round(att_bytes / t_att / 1e9, 4), "unit": "GB/s",
             "cores": 1, "kind": "oracle",
-            "sample": f"{units} (batch, kv-head) units of layer 0 "
-                      f"({T} tokens each): unpack + dequantize + fp64 decode "
-                      f"attention, {spent:.1f} s, single thread"}
+            "quantize_tok_s": round(q_tok_s, 1),
+            "sample": f"{units} (layer, batch, kv-head) units, {T} tokens "
+                      f"each: oracle quantize + pack ({t_q:.1f} s), then "
+                      f"unpack + dequantize + fp64 decode attention "
+                      f"({t_att:.1f} s); single thread"}
+
+
+TRAFFIC = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+
+
+def kernel_sources_digest(name):
+    """sha256 over the sources a kernel is built from: counters taken on
+    an older build no longer describe it."""
+    import glob
+    import hashlib
+    csrc = os.path.join(ROOT, "paper_2605_06675_amd", "csrc")
+    pats = {"quantize_kernel": ["rq_quant.hip"],
+            "attn_kernel": ["rq_attn*.hip", "rq_attn_impl.h"]}[name]
+    files = sorted(f for p in pats + ["rq_device.h", "rq_internal.h"]
+                   for f in glob.glob(os.path.join(csrc, p)))
+    h = hashlib.sha256()
+    for f in files:
+        with open(f, "rb") as fh:
+            h.update(os.path.basename(f).encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(name):
+    """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE and
+    WRITE_SIZE passes (scaled by the copy-kernel calibration), or None when
+    none were taken or the kernel's sources changed since."""
+    try:
+        with open(TRAFFIC) as f:
+            rec = json.load(f).get(name)
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("sources_sha256") != kernel_sources_digest(name):
+        return None
+    return int(rec["fetch_bytes"] * rec["fetch_factor"]
+               + rec["write_bytes"] * rec["write_factor"])
 
 
 def _kivi_meta_keys(m):
@@ -244,22 +288,32 @@ def main():
     att_bytes = attention_bytes(wl, table, T)
     q_bytes = quantize_bytes(wl, table, T - 1)
     att_gbs = att_bytes / (ms["attention"] * 1e-3) / 1e9
-    q_tok_s = B * (T - 1) * L / (ms["quantize"] * 1e-3)
+    # KV quantize tok/s: B * T tokens through all L layers' K and V
+    q_tok_s = B * (T - 1) / (ms["quantize"] * 1e-3)
     q_gbs = q_bytes / (ms["quantize"] * 1e-3) / 1e9
-    # dominant kernel of the step by time: its roofline
-    per_call_att = ms["attention"] / L
-    per_call_q = ms["quantize"] / L
-    if ms["quantize"] >= ms["attention"]:
-        dom = {"kernel": "quantize_kernel (rq_quantize_kv prefill, one layer)",
-               "achieved": q_bytes / L / (per_call_q * 1e-3) / 1e9}
-    else:
-        dom = {"kernel": "attn_kernel + combine_kernel (rq_decode_attention, "
-                         "one layer)",
-               "achieved": att_bytes / L / (per_call_att * 1e-3) / 1e9}
-    roofline = {"bound": "hbm", "achieved": round(dom["achieved"], 1),
-                "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": round(dom["achieved"] / PEAK_HBM_GBS, 4),
-                "traffic": None, "kernel": dom["kernel"]}
+    # per-launch figures: the phases are L back-to-back launches on the
+    # stream the events were recorded on
+    kernels = {
+        "quantize_kernel": {
+            "call": "rq_quantize_kv prefill of one layer (quantize_kernel; "
+                    "ring_kernel writes the window)",
+            "bytes": q_bytes / L, "us": ms["quantize"] * 1e3 / L},
+        "attn_kernel": {
+            "call": "rq_decode_attention of one layer (attn_kernel)",
+            "bytes": att_bytes / L, "us": ms["attention"] * 1e3 / L},
+    }
+    rooflines = {}
+    for name, k in kernels.items():
+        ach = k["bytes"] / (k["us"] * 1e-6) / 1e9
+        rooflines[name] = {
+            "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
+            "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4),
+            "traffic": measured_traffic(name), "kernel": name,
+            "call": k["call"], "bytes_per_launch": int(k["bytes"]),
+            "avg_launch_us": round(k["us"], 2)}
+    # the kernel that takes the most time in a step
+    dom = max(kernels, key=lambda n: kernels[n]["us"])
+    roofline = rooflines[dom]
     r1, r2 = rec[-1][2]
     beta_fit = np.concatenate([r1[2], r2[2]])
     line = {
@@ -275,7 +329,9 @@ def main():
         "phase_ms": {**{p: round(v, 3) for p, v in ms.items()},
                      "alloc_host": round(alloc_ms, 3)},
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "bf16" if wl.dtype == workloads.BF16 else "f16",
+        # inputs are 16-bit; quantization runs in fp32, attention on fp16
+        # matrix-core operands with fp32 accumulation and softmax
+        "dtype": "f16/f32",
         "data": "synthetic",
         "config": {"workload": wl.name, "layers": L, "batch": B,
                    "kv_heads": H, "q_heads": Hq, "head_dim": 128,
@@ -285,6 +341,7 @@ def main():
                    "quantize_bytes_per_step": q_bytes,
                    "fitted_beta_median": round(float(np.median(beta_fit)), 3)},
         "roofline": roofline,
+        "roofline_by_kernel": rooflines,
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl, table, args.cpu_seconds)

@@ -125,10 +125,13 @@ def bits16_from_f32(x, dtype):
     x = np.asarray(x, dtype=np.float32)
     if dtype == F16:
         return x.astype(np.float16).view(np.uint16)
-    u = x.view(np.uint32).astype(np.uint64)
-    lsb = (u >> 16) & 1
-    u = (u + 0x7FFF + lsb) >> 16
-    return u.astype(np.uint16)
+    # finite inputs only: u + 0x8000 stays below 2^32 for every finite x
+    u = np.ascontiguousarray(x).view(np.uint32)
+    r = (u >> 16) & 1
+    r += 0x7FFF
+    r += u
+    r >>= 16
+    return r.astype(np.uint16)
 
 
 def kv_cpu(wl: Workload, layer, batch_idx, n_tokens, seed=42, token0=0):
