@@ -14,6 +14,16 @@ typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 
+// Pointers into global memory.  Pointers held in a launch struct are
+// generic to the compiler; accessing through a global-address-space pointer
+// gives global (not flat) loads and stores, which do not tie the LDS wait
+// counter to memory latency.
+#define RQ_GLOBAL __attribute__((address_space(1)))
+template <class T>
+__device__ __forceinline__ RQ_GLOBAL T* gptr(T* p) {
+  return (RQ_GLOBAL T*)p;
+}
+
 __device__ __forceinline__ float widen(uint32_t bits16, int is_bf16) {
   if (is_bf16) return __uint_as_float(bits16 << 16);
   _Float16 h = __builtin_bit_cast(_Float16, (uint16_t)bits16);

@@ -256,6 +256,7 @@ rq_status rq_quantize_kv(const rq_cache* c, int32_t layer, int32_t n_past,
   q.nblk = (nq_new - nq_old) / rq::kChunk;
   q.is_bf16 = c->dtype == RQ_BF16;
   q.family = c->family;
+  q.n_cu = cu_count();
   q.tab = layer_table(c, layer);
   hipError_t e = rq::launch_quantize(q, s);
   if (e != hipSuccess) return hip_fail(e, "quantize launch");

@@ -31,6 +31,7 @@ struct QuantLaunch {
   int blk0, nblk;         // blocks [blk0, blk0 + nblk) get quantized
   int is_bf16;
   int family;
+  int n_cu;               // compute units of the device (grid sizing)
   LayerTable tab;
 };
 

@@ -2,6 +2,12 @@
 // window append.  One wave quantizes one 32-token block of one
 // (batch entry, kv-head, K|V) unit; the unit's bit-width and code region come
 // from the per-layer table in the kernel arguments.
+//
+// The KIVI block is staged once in LDS.  Group statistics run along one
+// axis of the block and packing along the other (keys: statistics per
+// channel over the 32 tokens, chunks of 32 channels per token; values: the
+// reverse), so each phase reads the rows or columns it needs from LDS and
+// every code goes straight into its packed word.
 #include "rq_device.h"
 #include "rq_internal.h"
 
@@ -79,105 +85,347 @@ __device__ __forceinline__ void pack_values_from_smem(const Smem& sm, int bits,
   }
 }
 
-// ------------------------------------------------------------------ KIVI K
-__device__ __forceinline__ void kivi_keys(const QuantLaunch& a, Smem& sm, int b, int h,
-                          int blk, int lane) {
-  const int bits = a.tab.bits[h][0];
-  const float qmax = (float)((1 << bits) - 1);
-  const int t0 = blk * kChunk;
-  float x0[kChunk], x1[kChunk];
-  float mn0 = INFINITY, mx0 = -INFINITY, mn1 = INFINITY, mx1 = -INFINITY;
+// ------------------------------------------------------------- KIVI (LDS)
+// Persistent kernel: every wave loops over blocks (block, kv-head, batch,
+// K|V in that order), with the next block's 8 KB already loading into
+// registers while the current one is quantized from the wave's own LDS
+// area.  The waves of a workgroup share nothing, so no workgroup barrier is
+// needed: a wave's LDS operations complete in issue order.
+constexpr int kQWaves = 4;                // waves per workgroup
+constexpr int kQOcc = 2;                  // workgroups per CU
+constexpr int kRowW = 68;                 // dwords per staged row (272 B)
+constexpr int kTabE = 34;                 // float2 entries per table row
+
+struct KiviSmem {
+  uint32_t x[kChunk * kRowW];             // [token][channel pair]
+  float2 tab[4 * kTabE];                  // (zero, 1/scale): K [chunk][channel],
+                                          // V [group][token]
+  uint16_t meta[256];                     // the block's metadata (512 B)
+};
+
+template <int BF16>
+__device__ __forceinline__ float lo16(uint32_t w) {
+  if (BF16) return __uint_as_float(w << 16);
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)(w & 0xffffu));
+}
+template <int BF16>
+__device__ __forceinline__ float hi16(uint32_t w) {
+  if (BF16) return __uint_as_float(w & 0xffff0000u);
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)(w >> 16));
+}
+
+// Group bounds of finite inputs (minimum/maximum map to the three-input
+// instructions without canonicalising every operand).
+__device__ __forceinline__ float vmin(float a, float b) {
+  return __builtin_elementwise_minimum(a, b);
+}
+__device__ __forceinline__ float vmax(float a, float b) {
+  return __builtin_elementwise_maximum(a, b);
+}
+
+constexpr uint32_t kMagicBits = 0x4B000000u;   // the float 2^23
+
+// Code of x in the low bits of a float: the clamped quotient plus 2^23 is
+// rounded by the fp32 add to the nearest integer, ties to even (the
+// quotient lies in [0, 2^b - 1]), leaving rint(quotient) in the low
+// mantissa bits under the constant field kMagicBits.
+template <int B>
+__device__ __forceinline__ uint32_t kivi_code_bits(float x, float zf, float inv) {
+  float r = (x - zf) * inv;               // two roundings: fp-contract is off
+  r = __builtin_amdgcn_fmed3f(r, 0.0f, (float)((1 << B) - 1));
+  return __float_as_uint(r + 8388608.0f);
+}
+
+// Packed words of one chunk, built by adding each code's fields at their
+// bit positions.  A code arrives as kMagicBits + code; the fields of a plane
+// that reaches the top bit are added as (bits >> shift), which carries the
+// constant kMagicBits >> shift along, and lower planes are extracted
+// exactly.  Fields never overlap, so the sum equals the OR of the fields
+// plus a compile-time constant per word, removed by finish().
+template <int B> struct ChunkAcc {
+  uint32_t w[B];
+  uint32_t bias[B];
+
+  __device__ __forceinline__ void init() {
 #pragma unroll
-  for (int t = 0; t < kChunk; ++t) {
-    const uint32_t w =
-        *reinterpret_cast<const uint32_t*>(token_src(a, b, h, 0, t0 + t) + 2 * lane);
-    x0[t] = widen(w & 0xffffu, a.is_bf16);
-    x1[t] = widen(w >> 16, a.is_bf16);
-    mn0 = __builtin_fminf(mn0, x0[t]);
-    mx0 = __builtin_fmaxf(mx0, x0[t]);
-    mn1 = __builtin_fminf(mn1, x1[t]);
-    mx1 = __builtin_fmaxf(mx1, x1[t]);
+    for (int i = 0; i < B; ++i) w[i] = 0, bias[i] = 0;
   }
-  const AsymParams p0 = asym_params(mn0, mx0, qmax);
-  const AsymParams p1 = asym_params(mn1, mx1, qmax);
-  uint16_t* cs = reinterpret_cast<uint16_t*>(sm.codes);
+  // code i of the chunk (0..31, constant after unrolling)
+  __device__ __forceinline__ void add(int i, uint32_t cb) {
+    int word = 0, shift = 0;
 #pragma unroll
-  for (int t = 0; t < kChunk; ++t) {
-    const uint32_t u0 = asym_code(x0[t], p0, qmax);
-    const uint32_t u1 = asym_code(x1[t], p1, qmax);
-    cs[(t * kD + 2 * lane) >> 1] = (uint16_t)(u0 | (u1 << 8));
+    for (int p = 0; p < Planes<B>::n; ++p) {
+      const int wd = Planes<B>::w[p];
+      const int per = 16 / wd;
+      const int j = i & 15, d = j / per, k = j % per;
+      const int pos = k * wd + (i >= 16 ? 16 : 0);
+      if (shift + wd == B) {
+        w[word + d] += (cb >> shift) << pos;
+        bias[word + d] += (kMagicBits >> shift) << pos;
+      } else {
+        w[word + d] += __builtin_amdgcn_ubfe(cb, shift, wd) << pos;
+      }
+      word += wd;
+      shift += wd;
+    }
   }
-  // metadata: chunk q = lane / 16, channels j, j+1 of the chunk
-  const int q = lane >> 4, j = 2 * (lane & 15);
-  sm.meta[q * 64 + pair_pos(j)] = p0.s16;
-  sm.meta[q * 64 + pair_pos(j + 1)] = p1.s16;
-  sm.meta[q * 64 + 32 + pair_pos(j)] = p0.z16;
-  sm.meta[q * 64 + 32 + pair_pos(j + 1)] = p1.z16;
-  __syncthreads();
-  // pack: unit (token, chunk) = lane and lane + 64
-  uint32_t* region = reinterpret_cast<uint32_t*>(a.codes + a.tab.code_off[h][0]);
+  __device__ __forceinline__ void finish() {
 #pragma unroll
-  for (int rep = 0; rep < 2; ++rep) {
-    const int u = lane + rep * kWave;
-    const int t = u >> 2, qq = u & 3;
-    uint32_t c[8];
+    for (int i = 0; i < B; ++i) w[i] -= bias[i];
+  }
+};
+
+template <int B>
+__device__ __forceinline__ void store_chunk(uint32_t* dst, const uint32_t* w) {
+  RQ_GLOBAL uint32_t* g = gptr(dst);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) c[i] = sm.codes[(t * kD + qq * 32) / 4 + i];
-    const size_t tok = (size_t)b * a.cap + t0 + t;
-    pack_store_dyn(bits, c, region + (tok * 4 + qq) * bits);
+  for (int i = 0; i < B; ++i) g[i] = w[i];
+}
+
+struct BlockId {
+  int blk, h, b, kind;
+};
+
+__device__ __forceinline__ BlockId block_id(const QuantLaunch& a, int it) {
+  BlockId id;
+  id.blk = a.blk0 + it % a.nblk;
+  const int r = it / a.nblk;
+  id.h = r % a.H;
+  const int z = r / a.H;
+  id.b = z >> 1;
+  id.kind = z & 1;
+  return id;
+}
+
+// Global -> registers: the block's 32 token rows, 16 bytes per lane and
+// step (step j, lane l: token 4 j + l / 16, bytes 16 (l % 16) of the row).
+__device__ __forceinline__ void load_block(const QuantLaunch& a, const BlockId& id,
+                                           u4 v[8], int lane) {
+  const int t0 = id.blk * kChunk;
+  if (t0 >= a.n_past) {
+    // the whole block is new input: 8 KB contiguous
+    const RQ_GLOBAL u4* src = gptr(reinterpret_cast<const u4*>(
+        (id.kind ? a.v : a.k) +
+        ((size_t)(id.b * a.H + id.h) * a.n_new + (t0 - a.n_past)) * kD));
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = src[j * kWave + lane];
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int c = j * kWave + lane, t = c >> 4, p = c & 15;
+      v[j] = gptr(reinterpret_cast<const u4*>(
+          token_src(a, id.b, id.h, id.kind, t0 + t)))[p];
+    }
   }
 }
 
-// ------------------------------------------------------------------ KIVI V
-__device__ __forceinline__ void kivi_values(const QuantLaunch& a, Smem& sm, int b, int h,
-                            int blk, int lane) {
-  const int bits = a.tab.bits[h][1];
-  const float qmax = (float)((1 << bits) - 1);
-  const int t0 = blk * kChunk;
-  const int t = lane >> 1, half = lane & 1;
-  const uint16_t* src = token_src(a, b, h, 1, t0 + t) + half * 64;
-  uint8_t* cb = reinterpret_cast<uint8_t*>(sm.codes);
+__device__ __forceinline__ void stage_block(KiviSmem& sm, const u4 v[8], int lane) {
 #pragma unroll
-  for (int g = 0; g < 2; ++g) {
-    float x[32];
-    const uint4* s4 = reinterpret_cast<const uint4*>(src + g * 32);
+  for (int j = 0; j < 8; ++j) {
+    const int c = j * kWave + lane, t = c >> 4, p = c & 15;
+    *reinterpret_cast<u4*>(&sm.x[t * kRowW + 4 * p]) = v[j];
+  }
+  __builtin_amdgcn_wave_barrier();
+}
+
+// Metadata of the block, staged in LDS, to its 512-byte slot.
+__device__ __forceinline__ void store_meta(const QuantLaunch& a, const KiviSmem& sm,
+                                           const BlockId& id, int lane) {
+  typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+  const int nblk_cap = a.cap / kChunk;
+  RQ_GLOBAL u2* m = gptr(reinterpret_cast<u2*>(
+      a.meta + ((((size_t)id.h * 2 + id.kind) * a.B + id.b) * nblk_cap + id.blk) *
+                   kMetaBlockKivi));
+  m[lane] = reinterpret_cast<const u2*>(sm.meta)[lane];
+}
+
+// Keys: scale and zero per channel over the block's 32 tokens; chunk q of
+// token t holds channels 32q .. 32q + 31.
+template <int BF16, int B>
+__device__ __forceinline__ void kivi_keys_lds(const QuantLaunch& a, KiviSmem& sm,
+                                              const BlockId& id, int lane) {
+  // statistics: lane -> channels 2 lane, 2 lane + 1
+  float mn0 = INFINITY, mx0 = -INFINITY, mn1 = INFINITY, mx1 = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const uint4 w = s4[i];
-      const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+  for (int t = 0; t < kChunk; ++t) {
+    const uint32_t w = sm.x[t * kRowW + lane];
+    const float x0 = lo16<BF16>(w), x1 = hi16<BF16>(w);
+    mn0 = vmin(mn0, x0);
+    mx0 = vmax(mx0, x0);
+    mn1 = vmin(mn1, x1);
+    mx1 = vmax(mx1, x1);
+  }
+  const float qmax = (float)((1 << B) - 1);
+  const AsymParams p0 = asym_params(mn0, mx0, qmax);
+  const AsymParams p1 = asym_params(mn1, mx1, qmax);
+  {
+    const int q = lane >> 4, j = 2 * (lane & 15);
+    *reinterpret_cast<float4*>(&sm.tab[q * kTabE + j]) =
+        make_float4(p0.zf, p0.inv, p1.zf, p1.inv);
+    sm.meta[q * 64 + pair_pos(j)] = p0.s16;
+    sm.meta[q * 64 + pair_pos(j + 1)] = p1.s16;
+    sm.meta[q * 64 + 32 + pair_pos(j)] = p0.z16;
+    sm.meta[q * 64 + 32 + pair_pos(j + 1)] = p1.z16;
+  }
+  __builtin_amdgcn_wave_barrier();
+  store_meta(a, sm, id, lane);
+  // packing: lane -> chunk q of tokens ta and ta + 16
+  const int q = lane & 3, ta = lane >> 2;
+  ChunkAcc<B> acc[2];
+  acc[0].init();
+  acc[1].init();
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        x[8 * i + 2 * e] = widen(ww[e] & 0xffffu, a.is_bf16);
-        x[8 * i + 2 * e + 1] = widen(ww[e] >> 16, a.is_bf16);
-      }
-    }
-    float mn = x[0], mx = x[0];
-#pragma unroll
-    for (int i = 1; i < 32; ++i) {
-      mn = __builtin_fminf(mn, x[i]);
-      mx = __builtin_fmaxf(mx, x[i]);
-    }
-    const AsymParams p = asym_params(mn, mx, qmax);
-    uint32_t cw[8];
+  for (int half = 0; half < 2; ++half) {
+    // keep the two halves apart: their table and row reads would otherwise
+    // all be hoisted, beyond the register budget
+    __builtin_amdgcn_sched_barrier(0);
+    float zf[16], inv[16];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      cw[i] = (uint32_t)asym_code(x[4 * i], p, qmax) |
-              ((uint32_t)asym_code(x[4 * i + 1], p, qmax) << 8) |
-              ((uint32_t)asym_code(x[4 * i + 2], p, qmax) << 16) |
-              ((uint32_t)asym_code(x[4 * i + 3], p, qmax) << 24);
+      const float4 e = *reinterpret_cast<const float4*>(
+          &sm.tab[q * kTabE + 16 * half + 2 * i]);
+      zf[2 * i] = e.x;
+      inv[2 * i] = e.y;
+      zf[2 * i + 1] = e.z;
+      inv[2 * i + 1] = e.w;
     }
-    const int cg = 2 * half + g;
-    uint32_t* dst = reinterpret_cast<uint32_t*>(cb + t * kD + cg * 32);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) dst[i] = cw[i];
-    sm.meta[cg * 64 + pair_pos(t)] = p.s16;
-    sm.meta[cg * 64 + 32 + pair_pos(t)] = p.z16;
+    for (int u = 0; u < 2; ++u) {
+      const int t = ta + 16 * u;
+      const u4* row = reinterpret_cast<const u4*>(&sm.x[t * kRowW + 16 * q + 8 * half]);
+      const u4 d0 = row[0], d1 = row[1];
+      const uint32_t w[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int i = 16 * half + 2 * k;
+        acc[u].add(i, kivi_code_bits<B>(lo16<BF16>(w[k]), zf[2 * k], inv[2 * k]));
+        acc[u].add(i + 1, kivi_code_bits<B>(hi16<BF16>(w[k]), zf[2 * k + 1], inv[2 * k + 1]));
+      }
+    }
   }
-  __syncthreads();
+  uint32_t* region = reinterpret_cast<uint32_t*>(a.codes + a.tab.code_off[id.h][0]);
+  const int t0 = id.blk * kChunk;
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    acc[u].finish();
+    const size_t tok = (size_t)id.b * a.cap + t0 + ta + 16 * u;
+    store_chunk<B>(region + (tok * 4 + q) * B, acc[u].w);
+  }
+}
+
+// Values: scale and zero per token over each group of 32 channels; chunk c
+// of the block holds channel c over its 32 tokens.
+template <int BF16, int B>
+__device__ __forceinline__ void kivi_values_lds(const QuantLaunch& a, KiviSmem& sm,
+                                                const BlockId& id, int lane) {
+  const float qmax = (float)((1 << B) - 1);
+  {
+    // statistics: lane -> token t, groups 2 hb and 2 hb + 1
+    const int t = lane >> 1, hb = lane & 1;
+#pragma unroll
+    for (int g2 = 0; g2 < 2; ++g2) {
+      const int g = 2 * hb + g2;
+      const u4* row = reinterpret_cast<const u4*>(&sm.x[t * kRowW + 16 * g]);
+      float mn = INFINITY, mx = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const u4 d = row[i];
+        const uint32_t w[4] = {d.x, d.y, d.z, d.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float x0 = lo16<BF16>(w[e]), x1 = hi16<BF16>(w[e]);
+          mn = vmin(mn, vmin(x0, x1));
+          mx = vmax(mx, vmax(x0, x1));
+        }
+      }
+      const AsymParams p = asym_params(mn, mx, qmax);
+      sm.tab[g * kTabE + t] = make_float2(p.zf, p.inv);
+      sm.meta[g * 64 + pair_pos(t)] = p.s16;
+      sm.meta[g * 64 + 32 + pair_pos(t)] = p.z16;
+    }
+  }
+  __builtin_amdgcn_wave_barrier();
+  store_meta(a, sm, id, lane);
+  // packing: lane -> channels 2 lane, 2 lane + 1 (group lane / 16)
+  const int g = lane >> 4;
+  ChunkAcc<B> acc0, acc1;
+  acc0.init();
+  acc1.init();
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+    __builtin_amdgcn_sched_barrier(0);
+    float zf[16], inv[16];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float4 e = *reinterpret_cast<const float4*>(
+          &sm.tab[g * kTabE + 16 * half + 2 * i]);
+      zf[2 * i] = e.x;
+      inv[2 * i] = e.y;
+      zf[2 * i + 1] = e.z;
+      inv[2 * i + 1] = e.w;
+    }
+#pragma unroll
+    for (int tt = 0; tt < 16; ++tt) {
+      const int t = 16 * half + tt;
+      const uint32_t w = sm.x[t * kRowW + lane];
+      acc0.add(t, kivi_code_bits<B>(lo16<BF16>(w), zf[tt], inv[tt]));
+      acc1.add(t, kivi_code_bits<B>(hi16<BF16>(w), zf[tt], inv[tt]));
+    }
+  }
+  acc0.finish();
+  acc1.finish();
   const int nblk_cap = a.cap / kChunk;
-  uint32_t* region = reinterpret_cast<uint32_t*>(a.codes + a.tab.code_off[h][1]);
-  pack_values_from_smem(sm, bits,
-                        region + ((size_t)b * nblk_cap + blk) * kD * bits, lane);
+  uint32_t* dst = reinterpret_cast<uint32_t*>(a.codes + a.tab.code_off[id.h][1]) +
+                  (((size_t)id.b * nblk_cap + id.blk) * kD + 2 * lane) * B;
+  store_chunk<B>(dst, acc0.w);
+  store_chunk<B>(dst + B, acc1.w);
+}
+
+template <int BF16>
+__device__ __forceinline__ void kivi_block(const QuantLaunch& a, KiviSmem& sm,
+                                           const BlockId& id, int lane) {
+  const int bits = a.tab.bits[id.h][id.kind];
+#define RQ_KIVI_CASE(NB)                                          \
+  case NB:                                                        \
+    if (id.kind == 0)                                             \
+      kivi_keys_lds<BF16, NB>(a, sm, id, lane);                   \
+    else                                                          \
+      kivi_values_lds<BF16, NB>(a, sm, id, lane);                 \
+    break;
+  switch (bits) {
+    RQ_KIVI_CASE(1)
+    RQ_KIVI_CASE(2)
+    RQ_KIVI_CASE(3)
+    RQ_KIVI_CASE(4)
+    RQ_KIVI_CASE(5)
+    RQ_KIVI_CASE(6)
+    RQ_KIVI_CASE(7)
+    RQ_KIVI_CASE(8)
+    default: break;
+  }
+#undef RQ_KIVI_CASE
+}
+
+template <int BF16>
+__global__ void __launch_bounds__(kQWaves * kWave, kQOcc)
+kivi_quant_kernel(QuantLaunch a) {
+  __shared__ KiviSmem smem[kQWaves];
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & (kWave - 1);
+  KiviSmem& sm = smem[wave];
+  const int total = a.nblk * a.H * a.B * 2;
+  const int stride = gridDim.x * kQWaves;
+  int it = blockIdx.x * kQWaves + wave;
+  if (it >= total) return;
+  u4 v[8];
+  load_block(a, block_id(a, it), v, lane);
+  for (; it < total; it += stride) {
+    const BlockId id = block_id(a, it);
+    stage_block(sm, v, lane);
+    if (it + stride < total) load_block(a, block_id(a, it + stride), v, lane);
+    kivi_block<BF16>(a, sm, id, lane);
+    __builtin_amdgcn_wave_barrier();
+  }
 }
 
 // ---------------------------------------------------------------- QuaRot
@@ -288,30 +536,20 @@ __device__ __forceinline__ void quarot_block(const QuantLaunch& a, Smem& sm, int
 }
 
 __global__ void __launch_bounds__(kWave)
-quantize_kernel(QuantLaunch a) {
+quarot_quant_kernel(QuantLaunch a) {
   __shared__ Smem sm;
   const int blk = a.blk0 + blockIdx.x;
   const int h = blockIdx.y;
   const int b = blockIdx.z >> 1, kind = blockIdx.z & 1;
   const int lane = threadIdx.x;
-  if (a.family == RQ_KIVI) {
-    if (kind == 0)
-      kivi_keys(a, sm, b, h, blk, lane);
-    else
-      kivi_values(a, sm, b, h, blk, lane);
-  } else {
-    quarot_block(a, sm, b, h, kind, blk, lane);
-  }
+  quarot_block(a, sm, b, h, kind, blk, lane);
   __syncthreads();
   // metadata of this block
   const int nblk_cap = a.cap / kChunk;
-  const int per_blk = (a.family == RQ_KIVI) ? kMetaBlockKivi : kMetaBlockTok;
   uint8_t* m = a.meta +
-               ((((size_t)h * 2 + kind) * a.B + b) * nblk_cap + blk) * per_blk;
-  const int words = per_blk / 4;
+               ((((size_t)h * 2 + kind) * a.B + b) * nblk_cap + blk) * kMetaBlockTok;
   const uint32_t* src = reinterpret_cast<const uint32_t*>(sm.meta);
-  for (int i = lane; i < words; i += kWave)
-    reinterpret_cast<uint32_t*>(m)[i] = src[i];
+  if (lane < kMetaBlockTok / 4) reinterpret_cast<uint32_t*>(m)[lane] = src[lane];
 }
 
 __global__ void __launch_bounds__(kWave)
@@ -332,8 +570,21 @@ ring_kernel(RingLaunch a) {
 
 hipError_t launch_quantize(const QuantLaunch& a, hipStream_t s) {
   if (a.nblk <= 0) return hipSuccess;
-  dim3 grid(a.nblk, a.H, a.B * 2);
-  hipLaunchKernelGGL(quantize_kernel, grid, dim3(kWave), 0, s, a);
+  if (a.family == RQ_KIVI) {
+    // persistent: at most kQOcc workgroups of kQWaves waves per CU
+    const long waves = (long)a.nblk * a.H * a.B * 2;
+    long wg = (waves + kQWaves - 1) / kQWaves;
+    const long cap = (long)(a.n_cu > 0 ? a.n_cu : 256) * kQOcc;
+    if (wg > cap) wg = cap;
+    dim3 grid((unsigned)wg), block(kQWaves * kWave);
+    if (a.is_bf16)
+      hipLaunchKernelGGL(kivi_quant_kernel<1>, grid, block, 0, s, a);
+    else
+      hipLaunchKernelGGL(kivi_quant_kernel<0>, grid, block, 0, s, a);
+  } else {
+    dim3 grid(a.nblk, a.H, a.B * 2);
+    hipLaunchKernelGGL(quarot_quant_kernel, grid, dim3(kWave), 0, s, a);
+  }
   return hipGetLastError();
 }
 
