@@ -92,7 +92,9 @@ __device__ __forceinline__ void pack_values_from_smem(const Smem& sm, int bits,
 // area.  The waves of a workgroup share nothing, so no workgroup barrier is
 // needed: a wave's LDS operations complete in issue order.
 constexpr int kQWaves = 4;                // waves per workgroup
-constexpr int kQOcc = 2;                  // workgroups per CU
+// workgroups per CU: three when every width of the layer is at most 4 bits
+// (the code paths then fit 168 registers), else two
+__host__ __device__ constexpr int quant_occupancy(int maxb) { return maxb <= 4 ? 3 : 2; }
 constexpr int kRowW = 68;                 // dwords per staged row (272 B)
 constexpr int kTabE = 34;                 // float2 entries per table row
 
@@ -269,47 +271,42 @@ __device__ __forceinline__ void kivi_keys_lds(const QuantLaunch& a, KiviSmem& sm
   }
   __builtin_amdgcn_wave_barrier();
   store_meta(a, sm, id, lane);
-  // packing: lane -> chunk q of tokens ta and ta + 16
+  // packing: lane -> chunk q of tokens ta and ta + 16, one token at a time
+  // (the table is read twice; holding both tokens' rows costs registers)
   const int q = lane & 3, ta = lane >> 2;
-  ChunkAcc<B> acc[2];
-  acc[0].init();
-  acc[1].init();
+  uint32_t* region = reinterpret_cast<uint32_t*>(a.codes + a.tab.code_off[id.h][0]);
+  const int t0 = id.blk * kChunk;
 #pragma unroll
-  for (int half = 0; half < 2; ++half) {
-    // keep the two halves apart: their table and row reads would otherwise
-    // all be hoisted, beyond the register budget
-    __builtin_amdgcn_sched_barrier(0);
-    float zf[16], inv[16];
+  for (int u = 0; u < 2; ++u) {
+    ChunkAcc<B> acc;
+    acc.init();
+    const int t = ta + 16 * u;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const float4 e = *reinterpret_cast<const float4*>(
-          &sm.tab[q * kTabE + 16 * half + 2 * i]);
-      zf[2 * i] = e.x;
-      inv[2 * i] = e.y;
-      zf[2 * i + 1] = e.z;
-      inv[2 * i + 1] = e.w;
-    }
+    for (int half = 0; half < 2; ++half) {
+      __builtin_amdgcn_sched_barrier(0);
+      float zf[16], inv[16];
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int t = ta + 16 * u;
+      for (int i = 0; i < 8; ++i) {
+        const float4 e = *reinterpret_cast<const float4*>(
+            &sm.tab[q * kTabE + 16 * half + 2 * i]);
+        zf[2 * i] = e.x;
+        inv[2 * i] = e.y;
+        zf[2 * i + 1] = e.z;
+        inv[2 * i + 1] = e.w;
+      }
       const u4* row = reinterpret_cast<const u4*>(&sm.x[t * kRowW + 16 * q + 8 * half]);
       const u4 d0 = row[0], d1 = row[1];
       const uint32_t w[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
         const int i = 16 * half + 2 * k;
-        acc[u].add(i, kivi_code_bits<B>(lo16<BF16>(w[k]), zf[2 * k], inv[2 * k]));
-        acc[u].add(i + 1, kivi_code_bits<B>(hi16<BF16>(w[k]), zf[2 * k + 1], inv[2 * k + 1]));
+        acc.add(i, kivi_code_bits<B>(lo16<BF16>(w[k]), zf[2 * k], inv[2 * k]));
+        acc.add(i + 1, kivi_code_bits<B>(hi16<BF16>(w[k]), zf[2 * k + 1], inv[2 * k + 1]));
       }
     }
-  }
-  uint32_t* region = reinterpret_cast<uint32_t*>(a.codes + a.tab.code_off[id.h][0]);
-  const int t0 = id.blk * kChunk;
-#pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    acc[u].finish();
-    const size_t tok = (size_t)id.b * a.cap + t0 + ta + 16 * u;
-    store_chunk<B>(region + (tok * 4 + q) * B, acc[u].w);
+    acc.finish();
+    const size_t tok = (size_t)id.b * a.cap + t0 + t;
+    store_chunk<B>(region + (tok * 4 + q) * B, acc.w);
   }
 }
 
@@ -381,16 +378,18 @@ __device__ __forceinline__ void kivi_values_lds(const QuantLaunch& a, KiviSmem& 
   store_chunk<B>(dst + B, acc1.w);
 }
 
-template <int BF16>
+template <int BF16, int MAXB>
 __device__ __forceinline__ void kivi_block(const QuantLaunch& a, KiviSmem& sm,
                                            const BlockId& id, int lane) {
   const int bits = a.tab.bits[id.h][id.kind];
 #define RQ_KIVI_CASE(NB)                                          \
   case NB:                                                        \
-    if (id.kind == 0)                                             \
-      kivi_keys_lds<BF16, NB>(a, sm, id, lane);                   \
-    else                                                          \
-      kivi_values_lds<BF16, NB>(a, sm, id, lane);                 \
+    if (NB <= MAXB) {                                             \
+      if (id.kind == 0)                                           \
+        kivi_keys_lds<BF16, NB>(a, sm, id, lane);                 \
+      else                                                        \
+        kivi_values_lds<BF16, NB>(a, sm, id, lane);               \
+    }                                                             \
     break;
   switch (bits) {
     RQ_KIVI_CASE(1)
@@ -406,8 +405,9 @@ __device__ __forceinline__ void kivi_block(const QuantLaunch& a, KiviSmem& sm,
 #undef RQ_KIVI_CASE
 }
 
-template <int BF16>
-__global__ void __launch_bounds__(kQWaves * kWave, kQOcc)
+// MAXB: the widest bit-width of the layer (4 or 8)
+template <int BF16, int MAXB>
+__global__ void __launch_bounds__(kQWaves * kWave, quant_occupancy(MAXB))
 kivi_quant_kernel(QuantLaunch a) {
   __shared__ KiviSmem smem[kQWaves];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -423,7 +423,7 @@ kivi_quant_kernel(QuantLaunch a) {
     const BlockId id = block_id(a, it);
     stage_block(sm, v, lane);
     if (it + stride < total) load_block(a, block_id(a, it + stride), v, lane);
-    kivi_block<BF16>(a, sm, id, lane);
+    kivi_block<BF16, MAXB>(a, sm, id, lane);
     __builtin_amdgcn_wave_barrier();
   }
 }
@@ -571,16 +571,26 @@ ring_kernel(RingLaunch a) {
 hipError_t launch_quantize(const QuantLaunch& a, hipStream_t s) {
   if (a.nblk <= 0) return hipSuccess;
   if (a.family == RQ_KIVI) {
-    // persistent: at most kQOcc workgroups of kQWaves waves per CU
+    int maxb = 1;
+    for (int h = 0; h < a.H; ++h)
+      for (int k = 0; k < 2; ++k) maxb = a.tab.bits[h][k] > maxb ? a.tab.bits[h][k] : maxb;
+    // persistent: as many workgroups of kQWaves waves as fit on the device
     const long waves = (long)a.nblk * a.H * a.B * 2;
     long wg = (waves + kQWaves - 1) / kQWaves;
-    const long cap = (long)(a.n_cu > 0 ? a.n_cu : 256) * kQOcc;
+    const long cap = (long)(a.n_cu > 0 ? a.n_cu : 256) * quant_occupancy(maxb);
     if (wg > cap) wg = cap;
     dim3 grid((unsigned)wg), block(kQWaves * kWave);
-    if (a.is_bf16)
-      hipLaunchKernelGGL(kivi_quant_kernel<1>, grid, block, 0, s, a);
-    else
-      hipLaunchKernelGGL(kivi_quant_kernel<0>, grid, block, 0, s, a);
+    if (maxb <= 4) {
+      if (a.is_bf16)
+        hipLaunchKernelGGL((kivi_quant_kernel<1, 4>), grid, block, 0, s, a);
+      else
+        hipLaunchKernelGGL((kivi_quant_kernel<0, 4>), grid, block, 0, s, a);
+    } else {
+      if (a.is_bf16)
+        hipLaunchKernelGGL((kivi_quant_kernel<1, 8>), grid, block, 0, s, a);
+      else
+        hipLaunchKernelGGL((kivi_quant_kernel<0, 8>), grid, block, 0, s, a);
+    }
   } else {
     dim3 grid(a.nblk, a.H, a.B * 2);
     hipLaunchKernelGGL(quarot_quant_kernel, grid, dim3(kWave), 0, s, a);

@@ -118,6 +118,22 @@ def test_kivi_every_bit_width_ragged(dtype):
     _check_attention(kvc, units, dtype, 2, 8, 2)
 
 
+@pytest.mark.parametrize("wide", [False, True])
+def test_kivi_many_blocks_per_wave(wide):
+    # Enough blocks that every wave of the persistent quantize kernel loops
+    # several times (8192 blocks); layers with widths up to 4 and up to 8
+    # take different kernel instances.
+    H, batch, T = 8, 4, 4128
+    if wide:
+        bits = np.array([[[h + 1, 8 - h] for h in range(H)]])
+    else:
+        bits = np.array([[[1 + h % 4, 4 - h % 4] for h in range(H)]])
+    kvc, ks, vs, _ = _build(workloads.KIVI, workloads.BF16, H, 1, T, 32, bits,
+                            batch=batch)
+    _check_cache(workloads.KIVI, workloads.BF16, kvc, ks, vs, bits, 32, batch,
+                 H, T)
+
+
 def test_kivi_chunked_prefill_equals_one_shot():
     bits = np.array([[[2, 3], [1, 4], [4, 2], [3, 1]]])
     kvc, ks, vs, _ = _build(workloads.KIVI, workloads.BF16, 4, 4, 301, 40,
