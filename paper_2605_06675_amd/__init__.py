@@ -249,10 +249,25 @@ class KVCache:
     """Device buffers (torch) plus the descriptor of one quantized cache."""
 
     def __init__(self, family, dtype, n_layers, batch, n_kv_heads, n_q_heads,
-                 capacity, residual, bits, device="cuda"):
+                 capacity, residual, bits, device="cuda", rotation=None):
+        """rotation (TurboQuant only): device tensor of the bf16 rotations
+        [n_layers][n_kv_heads][128][128] (y = R x); the codebook table is
+        computed by the library and copied to the device here."""
         import torch
         self.desc = make_cache(family, dtype, n_layers, batch, n_kv_heads,
                                n_q_heads, capacity, residual, bits)
+        self.rotation = self.codebook = None
+        if family == RQ_TURBO:
+            if rotation is None:
+                raise ValueError("TurboQuant needs the rotations")
+            if tuple(rotation.shape) != (n_layers, n_kv_heads, 128, 128) \
+                    or rotation.element_size() != 2:
+                raise ValueError("rotation must be 16-bit [L][H][128][128]")
+            self.rotation = rotation.contiguous()
+            self.codebook = torch.from_numpy(
+                rq_turbo_codebook().reshape(-1)).to(device)
+            self.desc.rotation = self.rotation.data_ptr()
+            self.desc.codebook = self.codebook.data_ptr()
         cb, mb, rb = rq_cache_sizes(self.desc)
         self.codes = torch.zeros(max(cb, 1), dtype=torch.uint8, device=device)
         self.meta = torch.zeros(max(mb, 1), dtype=torch.uint8, device=device)

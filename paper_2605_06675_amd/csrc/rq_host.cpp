@@ -43,11 +43,10 @@ int meta_per_block(const rq_cache* c) {
 
 rq_status check_cache(const rq_cache* c) {
   if (!c) return fail(RQ_EINVAL, "cache descriptor is NULL");
-  if (c->family != RQ_KIVI && c->family != RQ_QUAROT) {
-    if (c->family == RQ_TURBO)
-      return fail(RQ_EUNSUPPORTED, "TurboQuant family is not built in this library");
+  if (c->family != RQ_KIVI && c->family != RQ_QUAROT && c->family != RQ_TURBO)
     return fail(RQ_EINVAL, "unknown family %d", c->family);
-  }
+  if (c->family == RQ_TURBO && (!c->rotation || !c->codebook))
+    return fail(RQ_EINVAL, "TurboQuant needs the rotation and codebook pointers");
   if (c->dtype != RQ_F16 && c->dtype != RQ_BF16)
     return fail(RQ_EINVAL, "unknown dtype %d", c->dtype);
   if (c->head_dim != rq::kD)
@@ -257,6 +256,11 @@ rq_status rq_quantize_kv(const rq_cache* c, int32_t layer, int32_t n_past,
   q.is_bf16 = c->dtype == RQ_BF16;
   q.family = c->family;
   q.n_cu = cu_count();
+  if (c->family == RQ_TURBO) {
+    q.rot = static_cast<const uint16_t*>(c->rotation) +
+            (size_t)layer * c->n_kv_heads * rq::kD * rq::kD;
+    q.cb = c->codebook;
+  }
   q.tab = layer_table(c, layer);
   hipError_t e = rq::launch_quantize(q, s);
   if (e != hipSuccess) return hip_fail(e, "quantize launch");
@@ -301,6 +305,8 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
   if (!q || !out || !ws || !c->codes || !c->meta || !c->resid)
     return fail(RQ_EINVAL, "NULL device pointer");
   if (!std::isfinite(scale)) return fail(RQ_EINVAL, "scale is not finite");
+  if (c->family == RQ_TURBO)
+    return fail(RQ_EUNSUPPORTED, "TurboQuant decode attention is not built yet");
   const rq::LayerTable tab = layer_table(c, layer);
   int maxb = 1, maxkv = 0;
   for (int h = 0; h < c->n_kv_heads; ++h) {

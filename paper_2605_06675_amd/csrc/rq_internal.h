@@ -32,6 +32,8 @@ struct QuantLaunch {
   int is_bf16;
   int family;
   int n_cu;               // compute units of the device (grid sizing)
+  const uint16_t* rot;    // TurboQuant: this layer's rotations [H][128][128] bf16
+  const float* cb;        // TurboQuant: codebook table (rq_turbo_codebook)
   LayerTable tab;
 };
 
@@ -72,6 +74,7 @@ struct CalibLaunch {
 };
 
 hipError_t launch_quantize(const QuantLaunch& a, hipStream_t s);
+hipError_t launch_quantize_turbo(const QuantLaunch& a, hipStream_t s);
 hipError_t launch_ring(const RingLaunch& a, hipStream_t s);
 hipError_t launch_attention(const AttnLaunch& a, hipStream_t s);
 // LDS bytes of the attention kernel for a layer (query rows, block slots

@@ -570,6 +570,7 @@ ring_kernel(RingLaunch a) {
 
 hipError_t launch_quantize(const QuantLaunch& a, hipStream_t s) {
   if (a.nblk <= 0) return hipSuccess;
+  if (a.family == RQ_TURBO) return launch_quantize_turbo(a, s);
   if (a.family == RQ_KIVI) {
     int maxb = 1;
     for (int h = 0; h < a.H; ++h)

@@ -144,7 +144,7 @@ def test_descriptor_validation():
         (dict(bits=np.full((1, 8, 2), 9)), rq.RQ_EINVAL),
         (dict(bits=np.full((1, 8, 2), 0)), rq.RQ_EINVAL),
         (dict(family=rq.RQ_QUAROT, bits=np.full((1, 8, 2), 1)), rq.RQ_EINVAL),
-        (dict(family=rq.RQ_TURBO), rq.RQ_EUNSUPPORTED),
+        (dict(family=rq.RQ_TURBO), rq.RQ_EINVAL),   # no rotation/codebook
         (dict(dtype=7), rq.RQ_EINVAL),
         (dict(n_kv_heads=33, n_q_heads=66, bits=np.full((1, 33, 2), 2)),
          rq.RQ_EINVAL),
