@@ -12,6 +12,7 @@ hipError_t launch_attn_kivi_n4_b4(const AttnLaunch&, size_t, hipStream_t);
 hipError_t launch_attn_kivi_n4_b8(const AttnLaunch&, size_t, hipStream_t);
 hipError_t launch_attn_quarot_b4(const AttnLaunch&, size_t, hipStream_t);
 hipError_t launch_attn_quarot_b8(const AttnLaunch&, size_t, hipStream_t);
+hipError_t launch_attn_turbo_b4(const AttnLaunch&, size_t, hipStream_t);
 
 size_t attention_area_bytes(int G, int slot_bytes, int maxb, int n_wg) {
   const size_t merge = (size_t)kWaves * G * (2 + kD) * sizeof(float);
@@ -36,7 +37,9 @@ hipError_t launch_attention(const AttnLaunch& a, hipStream_t s) {
   const size_t lds = attention_lds_bytes(a.G, a.slot_bytes, maxb, a.n_wg);
   const bool wide = maxb > 4;
   hipError_t e;
-  if (a.family == RQ_QUAROT)
+  if (a.family == RQ_TURBO)
+    e = wide ? hipErrorInvalidValue : launch_attn_turbo_b4(a, lds, s);
+  else if (a.family == RQ_QUAROT)
     e = (wide ? launch_attn_quarot_b8 : launch_attn_quarot_b4)(a, lds, s);
   else if (a.GP <= 4)
     e = (wide ? launch_attn_kivi_n1_b8 : launch_attn_kivi_n1_b4)(a, lds, s);

@@ -1,5 +1,5 @@
-// Decode attention over the packed mixed-bit cache (KIVI-style and
-// QuaRot-style quantizers).
+// Decode attention over the packed mixed-bit cache (KIVI-style,
+// QuaRot-style and TurboQuant-style quantizers).
 //
 // Grid (workgroup slot, kv-head, batch), four waves per workgroup.  Slots
 // 0 .. n_wg-1 stream the quantized 32-token blocks of their (batch, kv-head)
@@ -25,6 +25,13 @@
 //   KIVI values  O = sum_t (p_t s_t 2^-P)(1024 + u 2^P)
 //                    + sum_t p_t z_t - 1024 sum_t (p_t s_t 2^-P)
 //   QuaRot       the same with per-token scales and codes u - 2^(b-1).
+//   TurboQuant   codes index the Lloyd-Max centroids, which are not affine
+//                in the code: each pair of codes is looked up in a table of
+//                fp16 centroids held in two to four registers (v_perm_b32,
+//                using the symmetry of the codebook for b >= 3), and the
+//                per-token norm scales the scores and probabilities.  The
+//                query is rotated by R on entry; the merge rotates the
+//                quantized part of the output back by R^T.
 // With G query heads per kv-head the sixteen MFMA columns carry the G
 // queries 16/G times over; the KIVI value side uses the spare rows for the
 // four 32-channel groups of a token, so one A operand serves all of them.
@@ -222,6 +229,64 @@ __device__ __forceinline__ void vpairs(const uint32_t* ch, int r, uint32_t magic
   }
 }
 
+// ------------------------------------------------------------- TurboQuant
+// Codes (i, i + 16) of a chunk as integers at bits 0 and 16 (i < 16 after
+// unrolling, or a per-lane quarter base plus a constant).
+template <int B>
+__device__ __forceinline__ uint32_t tq_code_pair(const uint32_t* wds, int i) {
+  uint32_t f = 0;
+#pragma unroll
+  for (int p = 0; p < plane_n(B); ++p) {
+    const int w = plane_w(B, p), per = 16 / w, off = plane_off(B, p);
+    const uint32_t fld = (wds[off + i / per] >> ((i % per) * w)) & pair_mask(w);
+    f |= fld << off;
+  }
+  return f;
+}
+
+// fp16 centroid pair of a code pair f (codes at bits 0 and 16).  lut: the
+// centroids as fp16 pairs -- b <= 2: all of them in order; b = 3, 4: the
+// positive half (codes 2^(b-1) ..), the negative half being its mirror
+// image (centroid 2^b - 1 - u = -centroid u).
+template <int B>
+__device__ __forceinline__ uint32_t tq_lut(uint32_t f, const uint32_t* lut) {
+  if constexpr (B == 1) {
+    return lut[0] | ((~f & 0x00010001u) << 15);
+  } else if constexpr (B == 2) {
+    return __builtin_amdgcn_perm(lut[1], lut[0], f * 0x202u + 0x01000100u);
+  } else if constexpr (B == 3) {
+    const uint32_t neg = (~f >> 2) & 0x00010001u;
+    const uint32_t m = (f ^ (neg * 3u)) & 0x00030003u;
+    return __builtin_amdgcn_perm(lut[1], lut[0], m * 0x202u + 0x01000100u) | (neg << 15);
+  } else {
+    const uint32_t neg = (~f >> 3) & 0x00010001u;
+    const uint32_t m = (f ^ (neg * 7u)) & 0x00070007u;
+    const uint32_t sel = (m & 0x00030003u) * 0x202u + 0x01000100u;
+    const uint32_t lo = __builtin_amdgcn_perm(lut[1], lut[0], sel);
+    const uint32_t hi = __builtin_amdgcn_perm(lut[3], lut[2], sel);
+    const uint32_t pick = ((m >> 2) & 0x00010001u) * 0xFFFFu;
+    return ((hi & pick) | (lo & ~pick)) | (neg << 15);
+  }
+}
+
+// fp16 lookup table of the b-bit codebook (layout of tq_lut) from the fp32
+// centroid table
+__device__ __forceinline__ void tq_make_lut(const float* cb, int b, uint32_t lut[4]) {
+  const float* c = cb + (b - 1) * 512 + 256;
+  const int first = b <= 2 ? 0 : (1 << (b - 1));
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int e0 = first + 2 * k, e1 = e0 + 1;
+    const float c0 = e0 < (1 << b) ? c[e0] : 0.0f, c1 = e1 < (1 << b) ? c[e1] : 0.0f;
+    const h2 v = {(_Float16)c0, (_Float16)c1};
+    lut[k] = as_u32(v);
+  }
+  if (b == 1) {
+    const h2 v = {(_Float16)c[1], (_Float16)c[1]};
+    lut[0] = as_u32(v);
+  }
+}
+
 // ------------------------------------------------------------ wave state
 template <int NA>
 struct WaveState {
@@ -242,6 +307,8 @@ struct LaneOps {
   uint32_t magic;   // kMagic, kept in a VGPR so that "(x & m) | magic" is one
                     // v_and_or_b32 with the mask in an SGPR (VOP3 takes no
                     // literal operand on this target)
+  uint32_t lutk[4]; // TurboQuant: fp16 centroid tables of the K and V widths
+  uint32_t lutv[4];
   int r, col, lane;
   int gsub;         // col / GP
   int GP;           // queries per replica (power of two >= G)
@@ -296,12 +363,25 @@ __device__ __forceinline__ void kpart(const SlotPtrs& sp, const LaneOps& lo, flo
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb) {
     const h8 Bk = make_h8(Bq[4 * kb], Bq[4 * kb + 1], Bq[4 * kb + 2], Bq[4 * kb + 3]);
-    S0 = mfma(make_h8(kpair<BK>(kw[0], 4 * kb, lo.magic), kpair<BK>(kw[0], 4 * kb + 1, lo.magic),
-                      kpair<BK>(kw[0], 4 * kb + 2, lo.magic), kpair<BK>(kw[0], 4 * kb + 3, lo.magic)),
-              Bk, S0);
-    S1 = mfma(make_h8(kpair<BK>(kw[1], 4 * kb, lo.magic), kpair<BK>(kw[1], 4 * kb + 1, lo.magic),
-                      kpair<BK>(kw[1], 4 * kb + 2, lo.magic), kpair<BK>(kw[1], 4 * kb + 3, lo.magic)),
-              Bk, S1);
+    if constexpr (FAM == RQ_TURBO) {
+      S0 = mfma(make_h8(tq_lut<BK>(tq_code_pair<BK>(kw[0], 4 * kb), lo.lutk),
+                        tq_lut<BK>(tq_code_pair<BK>(kw[0], 4 * kb + 1), lo.lutk),
+                        tq_lut<BK>(tq_code_pair<BK>(kw[0], 4 * kb + 2), lo.lutk),
+                        tq_lut<BK>(tq_code_pair<BK>(kw[0], 4 * kb + 3), lo.lutk)),
+                Bk, S0);
+      S1 = mfma(make_h8(tq_lut<BK>(tq_code_pair<BK>(kw[1], 4 * kb), lo.lutk),
+                        tq_lut<BK>(tq_code_pair<BK>(kw[1], 4 * kb + 1), lo.lutk),
+                        tq_lut<BK>(tq_code_pair<BK>(kw[1], 4 * kb + 2), lo.lutk),
+                        tq_lut<BK>(tq_code_pair<BK>(kw[1], 4 * kb + 3), lo.lutk)),
+                Bk, S1);
+    } else {
+      S0 = mfma(make_h8(kpair<BK>(kw[0], 4 * kb, lo.magic), kpair<BK>(kw[0], 4 * kb + 1, lo.magic),
+                        kpair<BK>(kw[0], 4 * kb + 2, lo.magic), kpair<BK>(kw[0], 4 * kb + 3, lo.magic)),
+                Bk, S0);
+      S1 = mfma(make_h8(kpair<BK>(kw[1], 4 * kb, lo.magic), kpair<BK>(kw[1], 4 * kb + 1, lo.magic),
+                        kpair<BK>(kw[1], 4 * kb + 2, lo.magic), kpair<BK>(kw[1], 4 * kb + 3, lo.magic)),
+                Bk, S1);
+    }
   }
   if constexpr (FAM != RQ_KIVI) {
     // per-token scales: dword 4r+i of the pair-ordered scales holds tokens
@@ -327,8 +407,15 @@ __device__ __forceinline__ void vpart(const SlotPtrs& sp, const LaneOps& lo,
   constexpr int GPA = 4 / NA;   // value groups per A operand (KIVI)
   const int r = lo.r, col = lo.col;
   uint32_t P2[4];
+  if constexpr (FAM == RQ_TURBO) {
+    // the centroid scale n / sqrt(128): 1/sqrt(128) here, n below
+    const h2 c = {(_Float16)kInvSqrtD, (_Float16)kInvSqrtD};
 #pragma unroll
-  for (int i = 0; i < 4; ++i) P2[i] = pk_mul(P[i], h_pair(h_pow2_neg(vpos(BV, i))));
+    for (int i = 0; i < 4; ++i) P2[i] = pk_mul(P[i], as_u32(c));
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) P2[i] = pk_mul(P[i], h_pair(h_pow2_neg(vpos(BV, i))));
+  }
   uint32_t A[NA][4];
   if constexpr (FAM == RQ_KIVI) {
 #pragma unroll
@@ -351,7 +438,13 @@ __device__ __forceinline__ void vpart(const SlotPtrs& sp, const LaneOps& lo,
   for (int nt = 0; nt < 8; ++nt) {
     const int a = (FAM == RQ_KIVI) ? (nt / 2) / GPA : 0;
     uint32_t pr[4];
-    vpairs<BV>(sp.vc + (16 * nt + col) * BV, r, lo.magic, pr);
+    if constexpr (FAM == RQ_TURBO) {
+      const uint32_t* ch = sp.vc + (16 * nt + col) * BV;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) pr[i] = tq_lut<BV>(tq_code_pair<BV>(ch, 4 * r + i), lo.lutv);
+    } else {
+      vpairs<BV>(sp.vc + (16 * nt + col) * BV, r, lo.magic, pr);
+    }
     ws.acc[nt] = mfma(make_h8(A[a][0], A[a][1], A[a][2], A[a][3]),
                       make_h8(pr[0], pr[1], pr[2], pr[3]), ws.acc[nt]);
   }
@@ -365,6 +458,8 @@ __device__ __forceinline__ void vpart(const SlotPtrs& sp, const LaneOps& lo,
     const u4 bz = (col < 4) ? sp.vm[col * 8 + 4 + r]
                             : reinterpret_cast<const u4*>(cst)[col == 4 ? 0 : 1];
     ws.corrZ = mfma(Ph, u4_h8(bz), ws.corrZ);
+  } else if constexpr (FAM == RQ_TURBO) {
+    ws.corrZ = mfma(Ph, make_h8(kOnes, kOnes, kOnes, kOnes), ws.corrZ);
   } else {
     uint32_t c[4];
 #pragma unroll
@@ -641,6 +736,40 @@ __device__ __forceinline__ void store_queries(const AttnLaunch& a, u4 piece, boo
   }
 }
 
+// TurboQuant: qs[j] <- R qs[j] / sqrt(128) for the G query rows (whole
+// workgroup; R of kv-head h, bf16 row-major, read from global memory).
+// Thread t computes coordinate t % 128 of rows t / 128, t / 128 + 2, ...
+__device__ __forceinline__ void rotate_queries(const AttnLaunch& a, int h, float (*qs)[kD]) {
+  const int tid = threadIdx.x, c = tid & (kD - 1), j0 = tid >> 7;
+  const RQ_GLOBAL u4* row = gptr(reinterpret_cast<const u4*>(a.rot + ((size_t)h * kD + c) * kD));
+  float acc[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) acc[k] = 0.0f;
+  for (int p = 0; p < kD / 8; ++p) {
+    const u4 w = row[p];
+    const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float r0 = __uint_as_float(ww[e] << 16), r1 = __uint_as_float(ww[e] & 0xffff0000u);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int j = j0 + 2 * k;
+        if (j < a.G) {
+          acc[k] = __builtin_fmaf(r0, qs[j][8 * p + 2 * e], acc[k]);
+          acc[k] = __builtin_fmaf(r1, qs[j][8 * p + 2 * e + 1], acc[k]);
+        }
+      }
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const int j = j0 + 2 * k;
+    if (j < a.G) qs[j][c] = acc[k] * kInvSqrtD;
+  }
+  __syncthreads();
+}
+
 // Partial of (unit, slot): float [G][2 + 128] = (max, sum, acc[128]).
 __device__ __forceinline__ float* part_ptr(const AttnLaunch& a, size_t unit, int slot) {
   return a.part + (unit * (a.n_wg + 1) + slot) * (size_t)a.G * (2 + kD);
@@ -771,7 +900,7 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
   const int G = a.G;
   const int bk = a.tab.bits[h][0], bv = a.tab.bits[h][1];
   const int nblk_cap = a.cap / kChunk;
-  const int per_blk = FAM == RQ_QUAROT ? kMetaBlockTok : kMetaBlockKivi;
+  const int per_blk = FAM == RQ_KIVI ? kMetaBlockKivi : kMetaBlockTok;
   Geo g;
   g.kreg = a.codes + a.tab.code_off[h][0] + (size_t)b * a.cap * 16 * bk;
   g.vreg = a.codes + a.tab.code_off[h][1] + (size_t)b * a.cap * 16 * bv;
@@ -794,6 +923,7 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
   const u4 qpiece = (int)(threadIdx.x >> 4) < G ? *reinterpret_cast<const u4*>(qr)
                                                  : (u4){0u, 0u, 0u, 0u};
   store_queries(a, qpiece, FAM == RQ_QUAROT, qs);
+  if (FAM == RQ_TURBO) rotate_queries(a, h, qs);
   if (tid < 8) cst[tid] = tid < 4 ? kOnes : 0u;
   __syncthreads();
   LaneOps lo;
@@ -813,7 +943,7 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
       for (int kk = 0; kk < 4; ++kk) {
         const int c0 = 32 * lo.r + 4 * kb + kk;
         const float q0 = j < G ? qs[j][c0] : 0.0f, q1 = j < G ? qs[j][c0 + 16] : 0.0f;
-        const float wgt = __builtin_ldexpf(1.0f, -kpos(bk, 4 * kb + kk));
+        const float wgt = FAM == RQ_TURBO ? 1.0f : __builtin_ldexpf(1.0f, -kpos(bk, 4 * kb + kk));
         const h2 vh = {(_Float16)(q0 * wgt), (_Float16)(q1 * wgt)};
         const h2 vz = {(_Float16)q0, (_Float16)q1};
         lo.qh[4 * kb + kk] = as_u32(vh);
@@ -828,6 +958,10 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
       lo.vq[i] = as_u32(vv);
     }
     lo.corrK = (f4){0.f, 0.f, 0.f, 0.f};
+    if (FAM == RQ_TURBO) {
+      tq_make_lut(a.cb, bk, lo.lutk);
+      tq_make_lut(a.cb, bv, lo.lutv);
+    }
     if (FAM == RQ_QUAROT) {
       const float off = (float)(1 << (bk - 1));
 #pragma unroll
@@ -932,6 +1066,7 @@ __device__ __forceinline__ void merge_unit(const AttnLaunch& a, size_t unit, flo
   const int G = a.G;
   const int ns = a.n_wg + 1;
   const bool quarot = a.family == RQ_QUAROT;
+  const bool rotated = quarot || a.family == RQ_TURBO;
   const size_t stride = (size_t)G * (2 + kD);
   const float* base = part_ptr(a, unit, 0);
   float* rot = lds;
@@ -982,7 +1117,7 @@ __device__ __forceinline__ void merge_unit(const AttnLaunch& a, size_t unit, flo
     for (int k = 0; k < kE; ++k) {
       const int e = e0 + k * kThreads;
       if (e < G * kD) {
-        if (quarot) {
+        if (rotated) {
           rot[e] = num[k];
           rot[G * kD + e] = tail[k] / den[k];
           rot[2 * G * kD + e] = 1.0f / den[k];
@@ -990,6 +1125,29 @@ __device__ __forceinline__ void merge_unit(const AttnLaunch& a, size_t unit, flo
           out[e] = (num[k] + tail[k]) / den[k];
         }
       }
+    }
+  }
+  if (a.family == RQ_TURBO) {
+    // rotate the quantized-domain sums back: x = R^T y (thread t: coordinate
+    // t % 128 of rows t / 128, t / 128 + 2, ...; R read down its columns)
+    __syncthreads();
+    const int c = tid & (kD - 1), j0 = tid >> 7;
+    const uint16_t* rh = a.rot + (size_t)(unit % a.H) * kD * kD;
+    float acc[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) acc[k] = 0.0f;
+    for (int cp = 0; cp < kD; ++cp) {
+      const float r = __uint_as_float((uint32_t)gptr(rh)[cp * kD + c] << 16);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int j = j0 + 2 * k;
+        if (j < G) acc[k] = __builtin_fmaf(r, rot[j * kD + cp], acc[k]);
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int j = j0 + 2 * k;
+      if (j < G) out[j * kD + c] = acc[k] * rot[2 * G * kD + j * kD + c] + rot[G * kD + j * kD + c];
     }
   }
   if (quarot) {

@@ -305,8 +305,6 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
   if (!q || !out || !ws || !c->codes || !c->meta || !c->resid)
     return fail(RQ_EINVAL, "NULL device pointer");
   if (!std::isfinite(scale)) return fail(RQ_EINVAL, "scale is not finite");
-  if (c->family == RQ_TURBO)
-    return fail(RQ_EUNSUPPORTED, "TurboQuant decode attention is not built yet");
   const rq::LayerTable tab = layer_table(c, layer);
   int maxb = 1, maxkv = 0;
   for (int h = 0; h < c->n_kv_heads; ++h) {
@@ -315,6 +313,10 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
     maxb = vb > maxb ? vb : maxb;
     maxkv = kb + vb > maxkv ? kb + vb : maxkv;
   }
+  if (c->family == RQ_TURBO && maxb > 4)
+    return fail(RQ_EUNSUPPORTED,
+                "TurboQuant decode attention handles widths up to 4 bits (layer %d has %d)",
+                layer, maxb);
   const SplitPlan p = plan_splits(c, n_tokens);
   const uint64_t need = attn_ws_bytes(c, p);
   if (ws_bytes < need)
@@ -343,6 +345,11 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
   a.is_bf16 = c->dtype == RQ_BF16;
   a.family = c->family;
   a.qscale = scale * 1.4426950408889634f;
+  if (c->family == RQ_TURBO) {
+    a.rot = static_cast<const uint16_t*>(c->rotation) +
+            (size_t)layer * c->n_kv_heads * rq::kD * rq::kD;
+    a.cb = c->codebook;
+  }
   a.tab = tab;
   a.slot_bytes = 512 * maxkv + 2 * meta_per_block(c);
   a.area_bytes = (int)rq::attention_area_bytes(G, a.slot_bytes, maxb, p.n_wg);

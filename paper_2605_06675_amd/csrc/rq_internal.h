@@ -62,6 +62,8 @@ struct AttnLaunch {
   int area_bytes;         // LDS bytes of the slot/merge/staging area
   int is_bf16, family;
   float qscale;           // scale * log2(e)
+  const uint16_t* rot;    // TurboQuant: this layer's rotations [H][128][128] bf16
+  const float* cb;        // TurboQuant: codebook table (rq_turbo_codebook)
   LayerTable tab;
 };
 

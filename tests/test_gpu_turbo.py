@@ -30,13 +30,13 @@ def _rotations(L, H, seed=42):
     return r16, workloads.u16_to_f32(r16, workloads.BF16).astype(np.float64)
 
 
-def _build(dtype, H, T, R, bits, batch, chunks=None, seed=42):
+def _build(dtype, H, T, R, bits, batch, chunks=None, seed=42, G=2):
     torch = _torch()
     r16, rf = _rotations(1, H, seed)
-    wl = workloads.Workload("t", workloads.TURBO, dtype, 1, batch, H, 2 * H,
+    wl = workloads.Workload("t", workloads.TURBO, dtype, 1, batch, H, G * H,
                             T, R, (1,), 2.0, 0.5, (1.0, 1.0))
     cap = ((T + 31) // 32) * 32
-    kvc = rq.KVCache(rq.RQ_TURBO, dtype, 1, batch, H, 2 * H, cap, R, bits,
+    kvc = rq.KVCache(rq.RQ_TURBO, dtype, 1, batch, H, G * H, cap, R, bits,
                      rotation=gh.dev(r16, workloads.BF16))
     ks, vs = zip(*[workloads.kv_cpu(wl, 0, b, T, seed=seed) for b in range(batch)])
     K, V = gh.dev(np.stack(ks), dtype), gh.dev(np.stack(vs), dtype)
@@ -122,3 +122,47 @@ def test_turbo_quantize_many_blocks_per_wave():
     bits = np.array([[[2 + h % 3, 4 - h % 3] for h in range(8)]])
     kvc, ks, vs, Rf = _build(workloads.BF16, 8, 2048, 0, bits, 4)
     _check(workloads.BF16, kvc, ks, vs, Rf, bits, 0, 4, 8)
+
+
+def _attention(kvc, units, dtype, batch, H, G, seed=7):
+    torch = _torch()
+    from oracle import attention as oatt
+    q16 = np.random.default_rng(seed).standard_normal((batch, H * G, 128))
+    q16 = workloads.bits16_from_f32(q16, dtype)
+    out = kvc.attention(0, gh.dev(q16, dtype))
+    torch.cuda.synchronize()
+    out = out.cpu().numpy()
+    worst = 0.0
+    for (b, h), u in units.items():
+        q = workloads.u16_to_f32(q16[b, h * G:(h + 1) * G], dtype)
+        want = oatt.decode_attention(q, u.keys(), u.values())
+        worst = max(worst, float(np.max(np.abs(out[b, h * G:(h + 1) * G] - want))))
+    print(f"attention max-abs error {worst:.3e}")
+    assert worst < 1e-2
+    return worst
+
+
+@pytest.mark.parametrize("dtype", [workloads.BF16, workloads.F16])
+def test_turbo_attention_every_narrow_width(dtype):
+    bits = np.array([[[1, 2], [2, 3], [3, 4], [4, 1]]])
+    kvc, ks, vs, Rf = _build(dtype, 4, 300, 32, bits, 2)
+    units = _check(dtype, kvc, ks, vs, Rf, bits, 32, 2, 4)
+    _attention(kvc, units, dtype, 2, 4, 2)
+
+
+def test_turbo_attention_eight_queries_per_head_no_window():
+    # the Llama-3-70B shape per kv-head: G = 8, window 0, bits {2, 3, 4}
+    bits = np.array([[[2 + h % 3, 4 - h % 3] for h in range(8)]])
+    kvc, ks, vs, Rf = _build(workloads.BF16, 8, 1500, 0, bits, 2, G=8)
+    units = _check(workloads.BF16, kvc, ks, vs, Rf, bits, 0, 2, 8)
+    _attention(kvc, units, workloads.BF16, 2, 8, 8)
+
+
+def test_turbo_attention_rejects_wide_widths():
+    bits = np.array([[[5, 2], [2, 2]]])
+    kvc, _, _, _ = _build(workloads.BF16, 2, 100, 0, bits, 1)
+    torch = _torch()
+    q = torch.zeros((1, 4, 128), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(rq.RQError) as e:
+        kvc.attention(0, q)
+    assert e.value.status == rq.RQ_EUNSUPPORTED
