@@ -181,6 +181,171 @@ calib_kernel(CalibLaunch a) {
   }
 }
 
+// ---------------------------------------------------------------- Turbo
+// TurboQuant: error in the original domain, x - R^T y_hat (the bf16
+// rotation is orthogonal only to about 2^-8, so the rotated-domain error
+// would differ by a few percent).  One wave per (component, block):
+//   y     = R x^T on bf16 (or fp16) matrix cores, fp32 sums (D[coord][token])
+//   n     = |x| in fp64, t = y sqrt(128) / n, codes as in the quantizer
+//   x_hat = y_hat R on fp32 matrix cores (16x16x4), k-steps taken in the
+//           register order of y: step (ct, i) sums coords 16 ct + 4 g + i
+// R (converted to fp32) and the block sit in LDS.
+constexpr int kRRowF = 132;   // floats per LDS row of R (528 B)
+constexpr int kXRow = 136;    // 16-bit entries per LDS row of the block
+
+typedef __bf16 cbf8 __attribute__((ext_vector_type(8)));
+
+template <int BF16>
+__device__ __forceinline__ f4 mma16(u4 a, u4 b, f4 c) {
+  if constexpr (BF16)
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(cbf8, a),
+                                                   __builtin_bit_cast(cbf8, b), c, 0, 0, 0);
+  else
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8, a),
+                                                  __builtin_bit_cast(h8, b), c, 0, 0, 0);
+}
+
+template <int B>
+__device__ __forceinline__ uint32_t tcode(float t, const RQ_GLOBAL float* th) {
+  constexpr int L = 1 << B, P = L / 2 - 1;
+  const float m = __builtin_fabsf(t);
+  int cnt = 0;
+  for (int j = 0; j < P; ++j) cnt += th[j] < m ? 1 : 0;
+  return (uint32_t)(t > 0.0f ? L / 2 + cnt : L / 2 - 1 - cnt);
+}
+
+template <int B>
+__device__ __forceinline__ void turbo_yhat(const f4 (&y)[8][2], const float (&fs)[2],
+                                           const float (&nq)[2], const float* cb,
+                                           float (&yh)[8][2][4]) {
+  const RQ_GLOBAL float* th = gptr(cb + (B - 1) * 512 + (1 << (B - 1)));
+  const RQ_GLOBAL float* ce = gptr(cb + (B - 1) * 512 + 256);
+#pragma unroll
+  for (int ct = 0; ct < 8; ++ct)
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        yh[ct][tt][i] = ce[tcode<B>(y[ct][tt][i] * fs[tt], th)] * nq[tt];
+}
+
+template <int BF16>
+__global__ void __launch_bounds__(kWave)
+calib_turbo_kernel(CalibLaunch a) {
+  __shared__ float Rf[kD * kRRowF];
+  __shared__ uint16_t xs[kChunk * kXRow];
+  const int blk = blockIdx.x, comp = blockIdx.y, lane = threadIdx.x;
+  const int g = lane >> 4, j = lane & 15;
+  const int n_blk = a.T / kChunk;
+  const uint16_t* x = a.x + ((size_t)comp * a.T + (size_t)blk * kChunk) * kD;
+  double* part = a.partial + ((size_t)comp * n_blk + blk) * a.n_bits;
+  const uint16_t* R = a.rot + (size_t)comp * kD * kD;
+  for (int e = lane; e < kD * kD / 2; e += kWave) {
+    const uint32_t w = gptr(reinterpret_cast<const uint32_t*>(R))[e];
+    const int r = (2 * e) / kD, c = (2 * e) % kD;
+    Rf[r * kRRowF + c] = __uint_as_float(w << 16);
+    Rf[r * kRRowF + c + 1] = __uint_as_float(w & 0xffff0000u);
+  }
+  for (int e = lane; e < kChunk * 16; e += kWave)
+    *reinterpret_cast<u4*>(&xs[(e >> 4) * kXRow + 8 * (e & 15)]) =
+        gptr(reinterpret_cast<const u4*>(x))[e];
+  __syncthreads();
+  // operands of token 16 tt + j, channels 32 ks + 8 g ..
+  u4 xv[8];
+#pragma unroll
+  for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+      xv[4 * tt + ks] = *reinterpret_cast<const u4*>(&xs[(16 * tt + j) * kXRow + 32 * ks + 8 * g]);
+  // norms
+  float fs[2], nq[2];
+#pragma unroll
+  for (int tt = 0; tt < 2; ++tt) {
+    double s = 0.0;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const u4 w = xv[4 * tt + ks];
+      const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const double lo = (double)widen(ww[e] & 0xffffu, BF16);
+        const double hi = (double)widen(ww[e] >> 16, BF16);
+        s = __builtin_fma(lo, lo, s);
+        s = __builtin_fma(hi, hi, s);
+      }
+    }
+    s += __shfl_xor(s, 16, kWave);
+    s += __shfl_xor(s, 32, kWave);
+    const float nf = f16_to_f32(f16_sat((float)__builtin_sqrt(s)));
+    fs[tt] = nf != 0.0f ? 11.313708498984761f / nf : 0.0f;
+    nq[tt] = nf * 0.08838834764831845f;
+  }
+  // y = R x^T: lane holds coords 16 ct + 4 g + i of token 16 tt + j
+  f4 y[8][2];
+#pragma unroll
+  for (int ct = 0; ct < 8; ++ct) {
+    y[ct][0] = y[ct][1] = (f4){0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      // R[16 ct + j][32 ks + 8 g ..] in the input's 16-bit type
+      uint32_t rw[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float r0 = Rf[(16 * ct + j) * kRRowF + 32 * ks + 8 * g + 2 * e];
+        const float r1 = Rf[(16 * ct + j) * kRRowF + 32 * ks + 8 * g + 2 * e + 1];
+        uint32_t b0, b1;
+        if (BF16) {
+          b0 = __float_as_uint(r0) >> 16;
+          b1 = __float_as_uint(r1) >> 16;
+        } else {
+          b0 = __builtin_bit_cast(uint16_t, (_Float16)r0);
+          b1 = __builtin_bit_cast(uint16_t, (_Float16)r1);
+        }
+        rw[e] = b0 | (b1 << 16);
+      }
+      const u4 rop = {rw[0], rw[1], rw[2], rw[3]};
+      y[ct][0] = mma16<BF16>(rop, xv[ks], y[ct][0]);
+      y[ct][1] = mma16<BF16>(rop, xv[4 + ks], y[ct][1]);
+    }
+  }
+  for (int jb = 0; jb < a.n_bits; ++jb) {
+    float yh[8][2][4];
+    switch (a.bits[jb]) {
+      case 1: turbo_yhat<1>(y, fs, nq, a.cb, yh); break;
+      case 2: turbo_yhat<2>(y, fs, nq, a.cb, yh); break;
+      case 3: turbo_yhat<3>(y, fs, nq, a.cb, yh); break;
+      case 4: turbo_yhat<4>(y, fs, nq, a.cb, yh); break;
+      case 5: turbo_yhat<5>(y, fs, nq, a.cb, yh); break;
+      case 6: turbo_yhat<6>(y, fs, nq, a.cb, yh); break;
+      case 7: turbo_yhat<7>(y, fs, nq, a.cb, yh); break;
+      default: turbo_yhat<8>(y, fs, nq, a.cb, yh); break;
+    }
+    // x_hat[token][channel] = sum_coord y_hat[token][coord] R[coord][channel]
+    double acc = 0.0;
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int nt = 0; nt < 8; ++nt) {
+        f4 xh = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int ct = 0; ct < 8; ++ct)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            xh = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                yh[ct][tt][i], Rf[(16 * ct + 4 * g + i) * kRRowF + 16 * nt + j], xh, 0, 0, 0);
+        // lane: tokens 16 tt + 4 g + i, channel 16 nt + j
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float xo = widen(xs[(16 * tt + 4 * g + i) * kXRow + 16 * nt + j], BF16);
+          const double d = (double)xo - (double)xh[i];
+          acc = __builtin_fma(d, d, acc);
+        }
+      }
+    acc = wave_sum(acc);
+    if (lane == 0) part[jb] = acc;
+  }
+}
+
 __global__ void calib_reduce_kernel(CalibLaunch a) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= a.n_comp * a.n_bits) return;
@@ -196,7 +361,14 @@ __global__ void calib_reduce_kernel(CalibLaunch a) {
 
 hipError_t launch_calibrate(const CalibLaunch& a, hipStream_t s) {
   dim3 grid(a.T / kChunk, a.n_comp);
-  hipLaunchKernelGGL(calib_kernel, grid, dim3(kWave), 0, s, a);
+  if (a.family == RQ_TURBO) {
+    if (a.is_bf16)
+      hipLaunchKernelGGL(calib_turbo_kernel<1>, grid, dim3(kWave), 0, s, a);
+    else
+      hipLaunchKernelGGL(calib_turbo_kernel<0>, grid, dim3(kWave), 0, s, a);
+  } else {
+    hipLaunchKernelGGL(calib_kernel, grid, dim3(kWave), 0, s, a);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int n = a.n_comp * a.n_bits;

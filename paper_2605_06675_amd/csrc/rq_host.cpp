@@ -381,10 +381,10 @@ rq_status rq_calibrate_distortion(int32_t family, int32_t dtype, const void* x,
                                   const float* codebook, double* mse, double* alpha,
                                   double* beta, double* r2, void* ws,
                                   uint64_t ws_bytes, rq_stream stream) {
-  if (family == RQ_TURBO)
-    return fail(RQ_EUNSUPPORTED, "TurboQuant family is not built in this library");
-  if (family != RQ_KIVI && family != RQ_QUAROT)
+  if (family != RQ_KIVI && family != RQ_QUAROT && family != RQ_TURBO)
     return fail(RQ_EINVAL, "unknown family %d", family);
+  if (family == RQ_TURBO && (!rotation || !codebook))
+    return fail(RQ_EINVAL, "TurboQuant needs the rotation and codebook pointers");
   if (dtype != RQ_F16 && dtype != RQ_BF16)
     return fail(RQ_EINVAL, "unknown dtype %d", dtype);
   uint64_t need = 0;
@@ -413,6 +413,8 @@ rq_status rq_calibrate_distortion(int32_t family, int32_t dtype, const void* x,
   a.is_value = is_value != 0;
   a.is_bf16 = dtype == RQ_BF16;
   a.family = family;
+  a.rot = static_cast<const uint16_t*>(rotation);
+  a.cb = codebook;
   for (int j = 0; j < n_bits; ++j) a.bits[j] = (uint8_t)bits[j];
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   hipError_t e = rq::launch_calibrate(a, s);

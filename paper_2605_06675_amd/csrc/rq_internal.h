@@ -73,6 +73,8 @@ struct CalibLaunch {
   double* mse;            // [n_comp][n_bits]
   int n_comp, T, n_bits, is_value, is_bf16, family;
   uint8_t bits[16];
+  const uint16_t* rot;    // TurboQuant: [n_comp][128][128] bf16
+  const float* cb;        // TurboQuant: codebook table
 };
 
 hipError_t launch_quantize(const QuantLaunch& a, hipStream_t s);

@@ -190,7 +190,7 @@ def test_device_calls_validate_before_launch():
     m = (C.c_double * 4)()
     assert L.rq_calibrate_distortion(rq.RQ_TURBO, 0, fake, 2, 64, 0, b, 2, None,
                                      None, m, None, None, None, fake, 1 << 20,
-                                     None) == rq.RQ_EUNSUPPORTED
+                                     None) == rq.RQ_EINVAL   # no rotation/codebook
     assert L.rq_calibrate_distortion(rq.RQ_KIVI, 0, fake, 2, 60, 0, b, 2, None,
                                      None, m, None, None, None, fake, 1 << 20,
                                      None) == rq.RQ_EINVAL

@@ -166,3 +166,27 @@ def test_turbo_attention_rejects_wide_widths():
     with pytest.raises(rq.RQError) as e:
         kvc.attention(0, q)
     assert e.value.status == rq.RQ_EUNSUPPORTED
+
+
+@pytest.mark.parametrize("dtype,bits", [(workloads.BF16, [1, 2, 3, 4]),
+                                        (workloads.F16, [2, 3, 4, 5, 6])])
+def test_turbo_calibration_sweep(dtype, bits):
+    """8 components x 512 tokens, each with its own rotation: the error is
+    measured in the original domain (x - R^T y_hat) like the oracle's."""
+    torch = _torch()
+    from oracle import calib as ocalib
+    from oracle import fit as ofit
+    x16 = workloads.calib_cpu(8, 512, dtype)
+    x = workloads.u16_to_f32(x16, dtype)
+    r16 = np.stack([workloads.turbo_rotation(42, 0, i) for i in range(8)])
+    rf = workloads.u16_to_f32(r16, workloads.BF16).astype(np.float64)
+    cb = torch.from_numpy(rq.rq_turbo_codebook().reshape(-1)).cuda()
+    mse, a, b, _ = rq.rq_calibrate_distortion(
+        rq.RQ_TURBO, dtype, gh.dev(x16, dtype), 0, bits,
+        rotation=gh.dev(r16, workloads.BF16), codebook=cb)
+    want = ocalib.sweep(ocalib.TURBO, x, bits, False, rf)
+    rel = np.abs(mse / want - 1)
+    print(f"turbo sweep: max rel {rel.max():.2e}")
+    assert np.all(rel <= 1e-5)
+    wa, wb, _ = ofit.fit_distortion(want, bits)
+    np.testing.assert_allclose(b, wb, rtol=1e-4)
