@@ -14,19 +14,21 @@ hipError_t launch_attn_quarot_b4(const AttnLaunch&, size_t, hipStream_t);
 hipError_t launch_attn_quarot_b8(const AttnLaunch&, size_t, hipStream_t);
 hipError_t launch_attn_turbo_b4(const AttnLaunch&, size_t, hipStream_t);
 
-size_t attention_area_bytes(int G, int slot_bytes, int maxb, int n_wg) {
+size_t attention_area_bytes(int G, int slot_bytes, int maxb, int n_wg, int family) {
   const size_t merge = (size_t)kWaves * G * (2 + kD) * sizeof(float);
   const size_t slots = (size_t)kWaves * attn_depth(maxb) * slot_bytes;
-  // the merging workgroup's scratch and the residual-window staging reuse it
-  const size_t mscratch = (size_t)3 * G * kD * sizeof(float);
+  // the merging workgroup's scratch (and the rotation for TurboQuant) and the
+  // residual-window staging reuse it
+  const size_t mscratch = (size_t)G * kD * sizeof(float) +
+                          (family == RQ_TURBO ? (size_t)kD * kD * sizeof(uint16_t) : 0);
   size_t m = merge > slots ? merge : slots;
   m = m > kResLds ? m : kResLds;
   m = m > mscratch ? m : mscratch;
   return (m + 15) / 16 * 16;
 }
 
-size_t attention_lds_bytes(int G, int slot_bytes, int maxb, int n_wg) {
-  return attention_area_bytes(G, slot_bytes, maxb, n_wg) + (size_t)16 * kD * sizeof(float) +
+size_t attention_lds_bytes(int G, int slot_bytes, int maxb, int n_wg, int family) {
+  return attention_area_bytes(G, slot_bytes, maxb, n_wg, family) + (size_t)16 * kD * sizeof(float) +
          (size_t)16 * kD * sizeof(uint16_t);
 }
 
@@ -34,7 +36,7 @@ hipError_t launch_attention(const AttnLaunch& a, hipStream_t s) {
   int maxb = 1;
   for (int h = 0; h < a.H; ++h)
     for (int k = 0; k < 2; ++k) maxb = a.tab.bits[h][k] > maxb ? a.tab.bits[h][k] : maxb;
-  const size_t lds = attention_lds_bytes(a.G, a.slot_bytes, maxb, a.n_wg);
+  const size_t lds = attention_lds_bytes(a.G, a.slot_bytes, maxb, a.n_wg, a.family);
   const bool wide = maxb > 4;
   hipError_t e;
   if (a.family == RQ_TURBO)

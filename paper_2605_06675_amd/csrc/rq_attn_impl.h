@@ -57,6 +57,9 @@ constexpr uint32_t kNeg1024 = 0xE400E400u; // fp16 pair (-1024, -1024)
 constexpr uint32_t kOnes = 0x3C003C00u;    // fp16 pair (1, 1)
 constexpr float kLazy = 4.0f;              // log2 headroom of the running max
 
+// Streaming slots per merge group (two-level merge above this).
+constexpr int kGroup = kAttnGroup;
+
 // LDS slots per wave (blocks in flight).  Two keep three workgroups per CU
 // inside the LDS for widths up to 4 bits.
 constexpr int attn_depth(int maxb) { return maxb <= 4 ? 2 : 2; }
@@ -771,8 +774,10 @@ __device__ __forceinline__ void rotate_queries(const AttnLaunch& a, int h, float
 }
 
 // Partial of (unit, slot): float [G][2 + 128] = (max, sum, acc[128]).
+// Slots of a unit: 0 .. n_wg-1 streaming, n_wg the window, then the group
+// partials of the two-level merge.
 __device__ __forceinline__ float* part_ptr(const AttnLaunch& a, size_t unit, int slot) {
-  return a.part + (unit * (a.n_wg + 1) + slot) * (size_t)a.G * (2 + kD);
+  return a.part + (unit * a.pstride + slot) * (size_t)a.G * (2 + kD);
 }
 
 // Residual-window staging: 64 tokens of K and of V per chunk, rows padded
@@ -1053,119 +1058,161 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
   }
 }
 
-// Merge the partials of one (batch, kv-head) unit and write its output:
-// slots 0 .. n_wg-1 hold the quantized blocks (QuaRot: rotated domain), slot
-// n_wg the 16-bit window (original domain).  Thread t owns output elements
-// t, t + 256, ... of the G x 128 rows, two at a time; it loads the (max,
-// sum, value) of both for eight slots at once, all loads in flight
-// together.  Whole workgroup; lds: scratch of 128 G floats (QuaRot).
-__device__ __forceinline__ void merge_unit(const AttnLaunch& a, size_t unit, float* lds) {
-  constexpr int kE = 2;   // elements per pass
-  constexpr int kS = 8;   // slots per batch of loads
+// Merge partials of one (batch, kv-head) unit: slots first .. first+count-1
+// (quantized blocks: QuaRot and TurboQuant in the rotated domain) and, when
+// win >= 0, the 16-bit window slot win (original domain).  dst: a partial
+// slot to write the merged (max, sum, acc) to, or NULL to write the unit's
+// output.  Thread t owns E consecutive elements of one query row (E = 128 Gp
+// / 256, Gp the power of two >= G), so a slot's (max, sum) is loaded once
+// per row segment; the loads of several slots are in flight together.
+// Whole workgroup; lds: scratch of 128 G floats, plus the rotation
+// (TurboQuant, 32 KB).
+template <int E>
+__device__ __forceinline__ void merge_rows(const AttnLaunch& a, size_t unit, float* lds,
+                                           int first, int count, int win, float* dst) {
+  constexpr int kS = E <= 2 ? 16 : (E == 4 ? 12 : 6);
+  constexpr int TPR = kD / E;              // threads per row
   const int tid = threadIdx.x;
   const int G = a.G;
-  const int ns = a.n_wg + 1;
-  const bool quarot = a.family == RQ_QUAROT;
-  const bool rotated = quarot || a.family == RQ_TURBO;
+  const int j = tid / TPR, c0 = (tid % TPR) * E;
+  const bool own = j < G;
+  const int ns = count + (win >= 0 ? 1 : 0);
+  const float* base = part_ptr(a, unit, 0) + (size_t)j * (2 + kD);
   const size_t stride = (size_t)G * (2 + kD);
-  const float* base = part_ptr(a, unit, 0);
-  float* rot = lds;
-  float* out = a.out + unit * G * kD;   // (b, h) -> query rows h*G..
-  for (int e0 = tid; e0 < G * kD; e0 += kE * kThreads) {
-    float M[kE], den[kE], num[kE], tail[kE];
+  float M = -INFINITY, den = 0.0f, num[E], tail[E];
 #pragma unroll
-    for (int k = 0; k < kE; ++k) {
-      M[k] = -INFINITY;
-      den[k] = 0.0f;
-      num[k] = 0.0f;
-      tail[k] = 0.0f;
-    }
+  for (int k = 0; k < E; ++k) num[k] = tail[k] = 0.0f;
+  if (own) {
     for (int s0 = 0; s0 < ns; s0 += kS) {
-      float m[kS][kE], l[kS][kE], v[kS][kE];
+      float m[kS], l[kS], v[kS][E];
 #pragma unroll
-      for (int i = 0; i < kS; ++i)
+      for (int i = 0; i < kS; ++i) {
+        m[i] = -INFINITY;
+        l[i] = 0.0f;
 #pragma unroll
-        for (int k = 0; k < kE; ++k) {
-          const int e = e0 + k * kThreads;
-          m[i][k] = -INFINITY;
-          l[i][k] = 0.0f;
-          v[i][k] = 0.0f;
-          if (s0 + i < ns && e < G * kD) {
-            const float* src = base + (s0 + i) * stride + (e / kD) * (2 + kD);
-            m[i][k] = ld_agent(src);
-            l[i][k] = ld_agent(src + 1);
-            v[i][k] = ld_agent(src + 2 + e % kD);
-          }
+        for (int k = 0; k < E; ++k) v[i][k] = 0.0f;
+        if (s0 + i < ns) {
+          const int slot = s0 + i < count ? first + s0 + i : win;
+          const float* src = base + slot * stride;
+          m[i] = ld_agent(src);
+          l[i] = ld_agent(src + 1);
+#pragma unroll
+          for (int k = 0; k < E; ++k) v[i][k] = ld_agent(src + 2 + c0 + k);
         }
+      }
 #pragma unroll
-      for (int i = 0; i < kS; ++i)
+      for (int i = 0; i < kS; ++i) {
+        if (!(l[i] > 0.0f)) continue;
+        const float mn = __builtin_fmaxf(M, m[i]);
+        const float fo = __builtin_amdgcn_exp2f(M - mn);
+        const float fi = __builtin_amdgcn_exp2f(m[i] - mn);
+        M = mn;
+        den = __builtin_fmaf(den, fo, fi * l[i]);
+        // the window slot is in the original domain: kept apart
+        const bool w = s0 + i >= count;
 #pragma unroll
-        for (int k = 0; k < kE; ++k) {
-          if (!(l[i][k] > 0.0f)) continue;
-          const float mn = __builtin_fmaxf(M[k], m[i][k]);
-          const float fo = __builtin_amdgcn_exp2f(M[k] - mn);
-          const float fi = __builtin_amdgcn_exp2f(m[i][k] - mn);
-          M[k] = mn;
-          den[k] = __builtin_fmaf(den[k], fo, fi * l[i][k]);
-          // the window slot (ns - 1) is in the original domain: kept apart
-          const bool win = s0 + i == ns - 1;
-          num[k] = num[k] * fo + (win ? 0.0f : fi * v[i][k]);
-          tail[k] = tail[k] * fo + (win ? fi * v[i][k] : 0.0f);
-        }
-    }
-#pragma unroll
-    for (int k = 0; k < kE; ++k) {
-      const int e = e0 + k * kThreads;
-      if (e < G * kD) {
-        if (rotated) {
-          rot[e] = num[k];
-          rot[G * kD + e] = tail[k] / den[k];
-          rot[2 * G * kD + e] = 1.0f / den[k];
-        } else {
-          out[e] = (num[k] + tail[k]) / den[k];
+        for (int k = 0; k < E; ++k) {
+          num[k] = num[k] * fo + (w ? 0.0f : fi * v[i][k]);
+          tail[k] = tail[k] * fo + (w ? fi * v[i][k] : 0.0f);
         }
       }
     }
   }
-  if (a.family == RQ_TURBO) {
-    // rotate the quantized-domain sums back: x = R^T y (thread t: coordinate
-    // t % 128 of rows t / 128, t / 128 + 2, ...; R read down its columns)
-    __syncthreads();
-    const int c = tid & (kD - 1), j0 = tid >> 7;
-    const uint16_t* rh = a.rot + (size_t)(unit % a.H) * kD * kD;
-    float acc[8];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) acc[k] = 0.0f;
-    for (int cp = 0; cp < kD; ++cp) {
-      const float r = __uint_as_float((uint32_t)gptr(rh)[cp * kD + c] << 16);
-#pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const int j = j0 + 2 * k;
-        if (j < G) acc[k] = __builtin_fmaf(r, rot[j * kD + cp], acc[k]);
+  if (dst) {
+    // a group partial (no window in it)
+    if (own) {
+      float* d = dst + (size_t)j * (2 + kD);
+      if (c0 == 0) {
+        st_agent(d, M);
+        st_agent(d + 1, den);
       }
-    }
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int j = j0 + 2 * k;
-      if (j < G) out[j * kD + c] = acc[k] * rot[2 * G * kD + j * kD + c] + rot[G * kD + j * kD + c];
+      for (int k = 0; k < E; ++k) st_agent(d + 2 + c0 + k, num[k]);
     }
+    return;
   }
-  if (quarot) {
-    // rotate the quantized-domain sums back: x = H y / sqrt(128)
+  float* out = a.out + unit * G * kD + (size_t)j * kD + c0;   // (b, h) -> rows h*G..
+  const float inv = own ? 1.0f / den : 0.0f;
+  if (a.family == RQ_KIVI) {
+    if (own)
+#pragma unroll
+      for (int k = 0; k < E; ++k) out[k] = (num[k] + tail[k]) * inv;
+    return;
+  }
+  float* rot = lds;                        // [G][128] quantized-domain sums
+  if (own)
+#pragma unroll
+    for (int k = 0; k < E; ++k) rot[j * kD + c0 + k] = num[k];
+  if (a.family == RQ_QUAROT) {
+    // x = H y / sqrt(128)
     __syncthreads();
     for (int hh = 1; hh < kD; hh *= 2) {
       for (int e = tid; e < G * (kD / 2); e += kThreads) {
-        const int j = e / (kD / 2), i = e % (kD / 2);
+        const int jj = e / (kD / 2), i = e % (kD / 2);
         const int bse = (i / hh) * 2 * hh + (i % hh);
-        const float x = rot[j * kD + bse], y = rot[j * kD + bse + hh];
-        rot[j * kD + bse] = x + y;
-        rot[j * kD + bse + hh] = x - y;
+        const float x = rot[jj * kD + bse], y = rot[jj * kD + bse + hh];
+        rot[jj * kD + bse] = x + y;
+        rot[jj * kD + bse + hh] = x - y;
       }
       __syncthreads();
     }
-    for (int e = tid; e < G * kD; e += kThreads)
-      out[e] = rot[e] * kInvSqrtD * rot[2 * G * kD + e] + rot[G * kD + e];
+    if (own)
+#pragma unroll
+      for (int k = 0; k < E; ++k)
+        out[k] = rot[j * kD + c0 + k] * kInvSqrtD * inv + tail[k] * inv;
+    return;
   }
+  // TurboQuant: x = R^T y, R staged in LDS (row-major, as stored)
+  uint16_t* Rs = reinterpret_cast<uint16_t*>(lds + G * kD);
+  {
+    const RQ_GLOBAL u4* src = gptr(reinterpret_cast<const u4*>(
+        a.rot + (size_t)(unit % a.H) * kD * kD));
+    for (int i = tid; i < kD * kD / 8; i += kThreads)
+      reinterpret_cast<u4*>(Rs)[i] = src[i];
+  }
+  __syncthreads();
+  if (own) {
+    float acc[E];
+#pragma unroll
+    for (int k = 0; k < E; ++k) acc[k] = 0.0f;
+    for (int cp = 0; cp < kD; ++cp) {
+      const float y = rot[j * kD + cp];
+#pragma unroll
+      for (int k = 0; k < E; ++k)
+        acc[k] = __builtin_fmaf(__uint_as_float((uint32_t)Rs[cp * kD + c0 + k] << 16), y, acc[k]);
+    }
+#pragma unroll
+    for (int k = 0; k < E; ++k) out[k] = acc[k] * inv + tail[k] * inv;
+  }
+}
+
+__device__ __forceinline__ void merge_slots(const AttnLaunch& a, size_t unit, float* lds,
+                                            int first, int count, int win, float* dst) {
+  if (a.GP <= 2)
+    merge_rows<1>(a, unit, lds, first, count, win, dst);
+  else if (a.GP <= 4)
+    merge_rows<2>(a, unit, lds, first, count, win, dst);
+  else if (a.GP <= 8)
+    merge_rows<4>(a, unit, lds, first, count, win, dst);
+  else
+    merge_rows<8>(a, unit, lds, first, count, win, dst);
+}
+
+// Arrival tickets on the unit's counters (agent scope); the caller's
+// partials are published (s_waitcnt 0) before.
+__device__ __forceinline__ uint32_t take_ticket(uint32_t* counter) {
+  __shared__ uint32_t ticket;
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x == 0)
+    ticket = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();
+  return ticket;
+}
+
+__device__ __forceinline__ void reset_counter(uint32_t* counter) {
+  if (threadIdx.x == 0)
+    __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // FAM: quantizer family; NA: A operands of the KIVI value side (G <= 4: 1,
@@ -1194,21 +1241,30 @@ attn_kernel(AttnLaunch a) {
     __syncthreads();   // the merge area and the query rows are read until here
     residual_slot(a, b, h, qs, reinterpret_cast<uint16_t*>(slots), part_ptr(a, unit, a.n_wg));
   }
-  // publish this workgroup's partials, then take a ticket; the last
-  // workgroup of the unit merges and leaves the counter at zero for the
-  // next call
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  __shared__ uint32_t ticket;
-  if (threadIdx.x == 0)
-    ticket = __hip_atomic_fetch_add(a.counters + unit, 1u, __ATOMIC_RELAXED,
-                                    __HIP_MEMORY_SCOPE_AGENT);
-  __syncthreads();
-  if (ticket == (uint32_t)(nwg - 1)) {
-    merge_unit(a, unit, merge);
-    if (threadIdx.x == 0)
-      __hip_atomic_store(a.counters + unit, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  // publish this workgroup's partials and take a ticket.  Up to kGroup
+  // streaming slots: the last to arrive merges every slot and the window.
+  // More: slots report in groups of kGroup; the last of a group merges it
+  // into a group partial, and the last group to finish merges the group
+  // partials and the window.  Every counter is left at zero for the next
+  // call.
+  uint32_t* cnt = a.counters + unit * a.cstride;
+  const int ng = (a.n_wg + kGroup - 1) / kGroup;
+  if (ng <= 1) {
+    if (take_ticket(cnt) == (uint32_t)(nwg - 1)) {
+      merge_slots(a, unit, merge, 0, a.n_wg, a.n_wg, nullptr);
+      reset_counter(cnt);
+    }
+    return;
   }
+  const int g = slot / kGroup;
+  const int gsz = a.n_wg - g * kGroup < kGroup ? a.n_wg - g * kGroup : kGroup;
+  if (take_ticket(cnt + 1 + g) != (uint32_t)(gsz - 1)) return;
+  __syncthreads();   // the merge area is read until here
+  merge_slots(a, unit, merge, g * kGroup, gsz, -1, part_ptr(a, unit, a.n_wg + 1 + g));
+  reset_counter(cnt + 1 + g);
+  if (take_ticket(cnt) != (uint32_t)(ng - 1)) return;
+  merge_slots(a, unit, merge, a.n_wg + 1, ng, a.n_wg, nullptr);
+  reset_counter(cnt);
 }
 
 }  // namespace

@@ -165,7 +165,7 @@ SplitPlan plan_splits(const rq_cache* c, int n_tokens, int wg_per_cu = 3) {
   long per = 0;
   const char* env = std::getenv("RQ_ATTN_WG_BLOCKS");
   if (env && std::atoi(env) > 0) {
-    per = std::atoi(env);
+    per = std::atoi(env) < 4 ? 4 : std::atoi(env);
   } else {
     // the last workgroup of a unit also attends to the residual window,
     // which costs about as much as kResidualBlocks quantized blocks
@@ -180,15 +180,32 @@ SplitPlan plan_splits(const rq_cache* c, int n_tokens, int wg_per_cu = 3) {
   return p;
 }
 
-// Workspace: per-unit arrival counters (zero between calls), padded to 256
-// bytes, then the partials [B][H][n_wg + 1][G][2 + 128] floats.
-uint64_t attn_counter_bytes(const rq_cache* c) {
-  return ((uint64_t)c->batch * c->n_kv_heads * sizeof(uint32_t) + 255) / 256 * 256;
+// Merge groups of a plan (the two-level merge starts above one group).
+int merge_groups(int n_wg) {
+  const int ng = (n_wg + rq::kAttnGroup - 1) / rq::kAttnGroup;
+  return ng <= 1 ? 0 : ng;
 }
+
+// Counters per unit: the final one and one per merge group, for the most
+// workgroups any call on this cache can use (at least 4 blocks each), so
+// that the counter area -- zero between calls -- does not move.
+int counter_stride(const rq_cache* c) {
+  const int max_wg = (c->capacity / rq::kChunk + 3) / 4;
+  return 1 + merge_groups(max_wg);
+}
+
+// Workspace: per-unit arrival counters (zero between calls), padded to 256
+// bytes, then the partials [B][H][n_wg + 1 + groups][G][2 + 128] floats.
+uint64_t attn_counter_bytes(const rq_cache* c) {
+  return ((uint64_t)c->batch * c->n_kv_heads * counter_stride(c) * sizeof(uint32_t) + 255) /
+         256 * 256;
+}
+
+int part_stride(const SplitPlan& p) { return p.n_wg + 1 + merge_groups(p.n_wg); }
 
 uint64_t attn_ws_bytes(const rq_cache* c, const SplitPlan& p) {
   const uint64_t G = c->n_q_heads / c->n_kv_heads;
-  const uint64_t parts = (uint64_t)c->batch * c->n_kv_heads * (p.n_wg + 1);
+  const uint64_t parts = (uint64_t)c->batch * c->n_kv_heads * part_stride(p);
   return attn_counter_bytes(c) + parts * G * (2 + rq::kD) * sizeof(float);
 }
 
@@ -331,6 +348,8 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
   a.out = out;
   a.counters = static_cast<uint32_t*>(ws);
   a.part = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + attn_counter_bytes(c));
+  a.pstride = part_stride(p);
+  a.cstride = counter_stride(c);
   a.B = c->batch;
   a.H = c->n_kv_heads;
   a.G = G;
@@ -352,8 +371,8 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
   }
   a.tab = tab;
   a.slot_bytes = 512 * maxkv + 2 * meta_per_block(c);
-  a.area_bytes = (int)rq::attention_area_bytes(G, a.slot_bytes, maxb, p.n_wg);
-  const size_t lds = rq::attention_lds_bytes(G, a.slot_bytes, maxb, p.n_wg);
+  a.area_bytes = (int)rq::attention_area_bytes(G, a.slot_bytes, maxb, p.n_wg, c->family);
+  const size_t lds = rq::attention_lds_bytes(G, a.slot_bytes, maxb, p.n_wg, c->family);
   if (lds > lds_limit())
     return fail(RQ_EUNSUPPORTED,
                 "layer %d needs %zu bytes of LDS per workgroup (device limit %zu): "

@@ -12,6 +12,7 @@ constexpr int kD = 128;          // head_dim
 constexpr int kChunk = 32;       // codes per packed chunk = tokens per block
 constexpr int kMetaBlockKivi = 512;   // bytes of KIVI metadata per block
 constexpr int kMetaBlockTok = 64;     // bytes of per-token metadata per block
+constexpr int kAttnGroup = 16;        // streaming slots per merge group
 
 // Per-layer view of the bit table: byte offsets of each (head, kind) code
 // region and its bit-width.  Passed by value as a kernel argument, so a
@@ -51,9 +52,12 @@ struct AttnLaunch {
   const uint8_t* meta;    // this layer
   const uint16_t* resid;  // this layer
   float* out;             // [B][Hq][128]
-  float* part;            // [B][H][n_wg + 1][G][2 + 128] (max, sum, acc);
-                          // slot n_wg: the residual window
-  uint32_t* counters;     // [B][H] arrival counters, zero between calls
+  float* part;            // [B][H][pstride][G][2 + 128] (max, sum, acc);
+                          // slots 0..n_wg-1 streaming, n_wg the residual
+                          // window, then one per merge group
+  uint32_t* counters;     // [B][H][cstride] arrival counters, zero between calls
+  int pstride;            // partial slots per unit
+  int cstride;            // counters per unit (final + one per group)
   int B, H, G, cap, R;
   int GP;                 // smallest power of two >= G
   int nq, n_tokens;
@@ -83,8 +87,8 @@ hipError_t launch_ring(const RingLaunch& a, hipStream_t s);
 hipError_t launch_attention(const AttnLaunch& a, hipStream_t s);
 // LDS bytes of the attention kernel for a layer (query rows, block slots
 // and merge area share one allocation)
-size_t attention_area_bytes(int G, int slot_bytes, int maxb, int n_wg);
-size_t attention_lds_bytes(int G, int slot_bytes, int maxb, int n_wg);
+size_t attention_area_bytes(int G, int slot_bytes, int maxb, int n_wg, int family);
+size_t attention_lds_bytes(int G, int slot_bytes, int maxb, int n_wg, int family);
 hipError_t launch_calibrate(const CalibLaunch& a, hipStream_t s);
 
 }  // namespace rq

@@ -182,6 +182,42 @@ def test_kivi_decode_steps_with_flushes():
                  1, H, T)
 
 
+@pytest.mark.parametrize("G", [4, 8])
+def test_kivi_two_level_merge_long_context(G):
+    """Two kv-heads, batch 1, 8000+ tokens: more than 16 workgroups per
+    unit, so partials are merged in groups first.  Attention after the
+    prefill and after appends that change the number of workgroups (the
+    counters must come back to zero every call)."""
+    torch = _torch()
+    H, R, T0 = 2, 128, 8000
+    bits = np.array([[[2, 1], [3, 4]]])
+    T = T0 + 300
+    wl = workloads.Workload("t", workloads.KIVI, workloads.BF16, 1, 1, H,
+                            H * G, T, R, (1,), 2.0, 0.5, (1.0, 1.0))
+    k16, v16 = workloads.kv_cpu(wl, 0, 0, T)
+    K, V = gh.dev(k16[None], workloads.BF16), gh.dev(v16[None], workloads.BF16)
+    kvc = rq.KVCache(workloads.KIVI, workloads.BF16, 1, 1, H, H * G, 8320, R, bits)
+    q16 = workloads.bits16_from_f32(
+        np.random.default_rng(5).standard_normal((1, H * G, 128)), workloads.BF16)
+    qd = gh.dev(q16, workloads.BF16)
+    worst, t = 0.0, 0
+    for n in (T0, 1, 150, 149):
+        kvc.append(0, K[:, :, t:t + n].contiguous(), V[:, :, t:t + n].contiguous())
+        t += n
+        out = kvc.attention(0, qd).cpu().numpy()
+        for h in range(H):
+            u = ocache.Unit(workloads.KIVI,
+                            workloads.u16_to_f32(k16[h, :t], workloads.BF16),
+                            workloads.u16_to_f32(v16[h, :t], workloads.BF16),
+                            int(bits[0, h, 0]), int(bits[0, h, 1]), R)
+            q = workloads.u16_to_f32(q16[0, h * G:(h + 1) * G], workloads.BF16)
+            want = oatt.decode_attention(q, u.keys(), u.values())
+            worst = max(worst, np.max(np.abs(out[0, h * G:(h + 1) * G] - want)))
+    torch.cuda.synchronize()
+    print(f"long-context attention max-abs error {worst:.3e}")
+    assert worst < ATOL
+
+
 def test_short_context_window_only():
     # fewer tokens than the window: nothing quantized, attention is exact
     bits = np.array([[[2, 2], [3, 3]]])

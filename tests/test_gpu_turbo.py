@@ -190,3 +190,11 @@ def test_turbo_calibration_sweep(dtype, bits):
     assert np.all(rel <= 1e-5)
     wa, wb, _ = ofit.fit_distortion(want, bits)
     np.testing.assert_allclose(b, wb, rtol=1e-4)
+
+
+def test_turbo_attention_two_level_merge():
+    # batch 1, two kv-heads, 4096 tokens: partials merged in groups first
+    bits = np.array([[[3, 2], [4, 3]]])
+    kvc, ks, vs, Rf = _build(workloads.BF16, 2, 4096, 64, bits, 1, G=8)
+    units = _check(workloads.BF16, kvc, ks, vs, Rf, bits, 64, 1, 2)
+    _attention(kvc, units, workloads.BF16, 1, 2, 8)
