@@ -270,7 +270,9 @@ def main():
     cal_rot = rot.reshape(L * H, 128, 128) if rot is not None else None
     kvc = rq.KVCache(wl.family, wl.dtype, L, B, H, Hq, T, wl.residual, table,
                      device=dev, rotation=rot)
-    ws = kvc.workspace(T)
+    # the window, and with it the workspace, varies over the decode steps
+    ws = torch.zeros(max(rq.rq_decode_workspace(kvc.desc, T0 + s + 1)
+                         for s in range(nsteps)), dtype=torch.uint8, device=dev)
     outs = [torch.empty((B, Hq, 128), dtype=torch.float32, device=dev)
             for _ in range(L)]
     torch.cuda.synchronize()

@@ -59,6 +59,8 @@ constexpr float kLazy = 4.0f;              // log2 headroom of the running max
 
 // Streaming slots per merge group (two-level merge above this).
 constexpr int kGroup = kAttnGroup;
+// Window tokens per window workgroup.
+constexpr int kResChunk = kAttnResChunk;
 
 // LDS slots per wave (blocks in flight).  Two keep three workgroups per CU
 // inside the LDS for widths up to 4 bits.
@@ -739,43 +741,54 @@ __device__ __forceinline__ void store_queries(const AttnLaunch& a, u4 piece, boo
   }
 }
 
-// TurboQuant: qs[j] <- R qs[j] / sqrt(128) for the G query rows (whole
-// workgroup; R of kv-head h, bf16 row-major, read from global memory).
-// Thread t computes coordinate t % 128 of rows t / 128, t / 128 + 2, ...
-__device__ __forceinline__ void rotate_queries(const AttnLaunch& a, int h, float (*qs)[kD]) {
-  const int tid = threadIdx.x, c = tid & (kD - 1), j0 = tid >> 7;
-  const RQ_GLOBAL u4* row = gptr(reinterpret_cast<const u4*>(a.rot + ((size_t)h * kD + c) * kD));
-  float acc[8];
+// TurboQuant: qs[j] = qscale R q_j / sqrt(128) for the G query rows, on the
+// matrix cores: D[row][coord] = Q . R^T with the 16-bit query rows (qraw,
+// rows >= G unused) as A and rows of R (global memory, bf16; converted to
+// fp16 for fp16 queries) as B.  Wave w computes coordinate tiles 2w, 2w+1.
+typedef __bf16 abf8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ void rotate_queries(const AttnLaunch& a, int h, const uint16_t* qraw,
+                                               float (*qs)[kD]) {
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid & (kWave - 1);
+  const int r = lane & 15, g = lane >> 4;
+  const uint16_t* Rh = a.rot + (size_t)h * kD * kD;
 #pragma unroll
-  for (int k = 0; k < 8; ++k) acc[k] = 0.0f;
-  for (int p = 0; p < kD / 8; ++p) {
-    const u4 w = row[p];
-    const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+  for (int t = 0; t < 2; ++t) {
+    const int nt = 2 * wave + t;
+    f4 d = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float r0 = __uint_as_float(ww[e] << 16), r1 = __uint_as_float(ww[e] & 0xffff0000u);
+    for (int ks = 0; ks < 4; ++ks) {
+      const u4 qa = *reinterpret_cast<const u4*>(&qraw[r * kD + 32 * ks + 8 * g]);
+      u4 rb = gptr(reinterpret_cast<const u4*>(&Rh[(16 * nt + r) * kD + 32 * ks + 8 * g]))[0];
+      if (a.is_bf16) {
+        d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(abf8, qa),
+                                                    __builtin_bit_cast(abf8, rb), d, 0, 0, 0);
+      } else {
+        uint32_t w[4] = {rb.x, rb.y, rb.z, rb.w};
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const int j = j0 + 2 * k;
-        if (j < a.G) {
-          acc[k] = __builtin_fmaf(r0, qs[j][8 * p + 2 * e], acc[k]);
-          acc[k] = __builtin_fmaf(r1, qs[j][8 * p + 2 * e + 1], acc[k]);
+        for (int e = 0; e < 4; ++e) {
+          const _Float16 lo = (_Float16)__uint_as_float(w[e] << 16);
+          const _Float16 hi = (_Float16)__uint_as_float(w[e] & 0xffff0000u);
+          w[e] = (uint32_t)__builtin_bit_cast(uint16_t, lo) |
+                 ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
         }
+        rb = (u4){w[0], w[1], w[2], w[3]};
+        d = mfma(u4_h8(qa), u4_h8(rb), d);
       }
     }
-  }
-  __syncthreads();
+    // lane: coordinate 16 nt + r of query rows 4g .. 4g+3
 #pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    const int j = j0 + 2 * k;
-    if (j < a.G) qs[j][c] = acc[k] * kInvSqrtD;
+    for (int i = 0; i < 4; ++i) {
+      const int j = 4 * g + i;
+      if (j < a.G) qs[j][16 * nt + r] = d[i] * (a.qscale * kInvSqrtD);
+    }
   }
   __syncthreads();
 }
 
 // Partial of (unit, slot): float [G][2 + 128] = (max, sum, acc[128]).
-// Slots of a unit: 0 .. n_wg-1 streaming, n_wg the window, then the group
-// partials of the two-level merge.
+// Slots of a unit: 0 .. n_wg-1 streaming, n_wg .. n_wg+n_rw-1 the window,
+// then the group partials of the two-level merge.
 __device__ __forceinline__ float* part_ptr(const AttnLaunch& a, size_t unit, int slot) {
   return a.part + (unit * a.pstride + slot) * (size_t)a.G * (2 + kD);
 }
@@ -786,15 +799,15 @@ constexpr int kResTok = 64;
 constexpr int kResRow = 136;   // uint16 per padded row
 constexpr size_t kResLds = (size_t)2 * kResTok * kResRow * sizeof(uint16_t);
 
-// 16-bit residual window of one unit, original domain.  The window is read
-// in chunks of 64 tokens staged in LDS; the loads of the next chunk (and of
+// Tokens t_lo .. t_hi-1 of the 16-bit residual window of one unit, original
+// domain.  They are read in chunks of 64 tokens staged in LDS; the loads of the next chunk (and of
 // the queries, before the first) are in flight while a chunk is computed.
 // Wave w takes query rows w, w+4, ...; lane = token for the scores, lane =
 // channel pair for PV.  stage: LDS for one chunk (kResLds bytes), qs: LDS
 // for the query rows.
 __device__ __forceinline__ void residual_slot(const AttnLaunch& a, int b, int h,
                                               float (*qs)[kD], uint16_t* stage,
-                                              float* dst) {
+                                              float* dst, int t_lo, int t_hi) {
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid & (kWave - 1);
   const int cap = a.R + kChunk;
   const uint16_t* kb = a.resid + (((size_t)b * a.H + h) * 2 + 0) * cap * kD;
@@ -804,7 +817,7 @@ __device__ __forceinline__ void residual_slot(const AttnLaunch& a, int b, int h,
   // a chunk is 64 tokens x 16 pieces of 16 bytes: four pieces per thread
   u4 kr[4], vr[4];
   auto load_chunk = [&](int t0) {
-    const int n = (a.n_tokens - t0) < kResTok ? (a.n_tokens - t0) : kResTok;
+    const int n = (t_hi - t0) < kResTok ? (t_hi - t0) : kResTok;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int e = tid + i * kThreads, t = e >> 4, piece = e & 15;
@@ -816,7 +829,7 @@ __device__ __forceinline__ void residual_slot(const AttnLaunch& a, int b, int h,
     }
   };
   const u4 qpiece = query_piece(a, b, h);
-  if (a.nq < a.n_tokens) load_chunk(a.nq);
+  if (t_lo < t_hi) load_chunk(t_lo);
   store_queries(a, qpiece, false, qs);
   float m_run[4], l_run[4], ac0[4], ac1[4];
 #pragma unroll
@@ -826,8 +839,8 @@ __device__ __forceinline__ void residual_slot(const AttnLaunch& a, int b, int h,
     ac0[q] = 0.0f;
     ac1[q] = 0.0f;
   }
-  for (int t0 = a.nq; t0 < a.n_tokens; t0 += kResTok) {
-    const int n = (a.n_tokens - t0) < kResTok ? (a.n_tokens - t0) : kResTok;
+  for (int t0 = t_lo; t0 < t_hi; t0 += kResTok) {
+    const int n = (t_hi - t0) < kResTok ? (t_hi - t0) : kResTok;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int e = tid + i * kThreads, t = e >> 4, piece = e & 15;
@@ -837,7 +850,7 @@ __device__ __forceinline__ void residual_slot(const AttnLaunch& a, int b, int h,
       }
     }
     __syncthreads();
-    if (t0 + kResTok < a.n_tokens) load_chunk(t0 + kResTok);
+    if (t0 + kResTok < t_hi) load_chunk(t0 + kResTok);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int j = wave + kWaves * q;
@@ -927,8 +940,10 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
   const uint16_t* qr = qraw + (threadIdx.x >> 4) * kD + 8 * (threadIdx.x & 15);
   const u4 qpiece = (int)(threadIdx.x >> 4) < G ? *reinterpret_cast<const u4*>(qr)
                                                  : (u4){0u, 0u, 0u, 0u};
-  store_queries(a, qpiece, FAM == RQ_QUAROT, qs);
-  if (FAM == RQ_TURBO) rotate_queries(a, h, qs);
+  if (FAM == RQ_TURBO)
+    rotate_queries(a, h, qraw, qs);
+  else
+    store_queries(a, qpiece, FAM == RQ_QUAROT, qs);
   if (tid < 8) cst[tid] = tid < 4 ? kOnes : 0u;
   __syncthreads();
   LaneOps lo;
@@ -1059,8 +1074,8 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
 }
 
 // Merge partials of one (batch, kv-head) unit: slots first .. first+count-1
-// (quantized blocks: QuaRot and TurboQuant in the rotated domain) and, when
-// win >= 0, the 16-bit window slot win (original domain).  dst: a partial
+// (quantized blocks: QuaRot and TurboQuant in the rotated domain) and the
+// nwin window slots win .. win+nwin-1 (original domain).  dst: a partial
 // slot to write the merged (max, sum, acc) to, or NULL to write the unit's
 // output.  Thread t owns E consecutive elements of one query row (E = 128 Gp
 // / 256, Gp the power of two >= G), so a slot's (max, sum) is loaded once
@@ -1069,14 +1084,15 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
 // (TurboQuant, 32 KB).
 template <int E>
 __device__ __forceinline__ void merge_rows(const AttnLaunch& a, size_t unit, float* lds,
-                                           int first, int count, int win, float* dst) {
+                                           int first, int count, int win, int nwin,
+                                           float* dst) {
   constexpr int kS = E <= 2 ? 16 : (E == 4 ? 12 : 6);
   constexpr int TPR = kD / E;              // threads per row
   const int tid = threadIdx.x;
   const int G = a.G;
   const int j = tid / TPR, c0 = (tid % TPR) * E;
   const bool own = j < G;
-  const int ns = count + (win >= 0 ? 1 : 0);
+  const int ns = count + nwin;
   const float* base = part_ptr(a, unit, 0) + (size_t)j * (2 + kD);
   const size_t stride = (size_t)G * (2 + kD);
   float M = -INFINITY, den = 0.0f, num[E], tail[E];
@@ -1092,7 +1108,7 @@ __device__ __forceinline__ void merge_rows(const AttnLaunch& a, size_t unit, flo
 #pragma unroll
         for (int k = 0; k < E; ++k) v[i][k] = 0.0f;
         if (s0 + i < ns) {
-          const int slot = s0 + i < count ? first + s0 + i : win;
+          const int slot = s0 + i < count ? first + s0 + i : win + (s0 + i - count);
           const float* src = base + slot * stride;
           m[i] = ld_agent(src);
           l[i] = ld_agent(src + 1);
@@ -1187,15 +1203,16 @@ __device__ __forceinline__ void merge_rows(const AttnLaunch& a, size_t unit, flo
 }
 
 __device__ __forceinline__ void merge_slots(const AttnLaunch& a, size_t unit, float* lds,
-                                            int first, int count, int win, float* dst) {
+                                            int first, int count, int win, int nwin,
+                                            float* dst) {
   if (a.GP <= 2)
-    merge_rows<1>(a, unit, lds, first, count, win, dst);
+    merge_rows<1>(a, unit, lds, first, count, win, nwin, dst);
   else if (a.GP <= 4)
-    merge_rows<2>(a, unit, lds, first, count, win, dst);
+    merge_rows<2>(a, unit, lds, first, count, win, nwin, dst);
   else if (a.GP <= 8)
-    merge_rows<4>(a, unit, lds, first, count, win, dst);
+    merge_rows<4>(a, unit, lds, first, count, win, nwin, dst);
   else
-    merge_rows<8>(a, unit, lds, first, count, win, dst);
+    merge_rows<8>(a, unit, lds, first, count, win, nwin, dst);
 }
 
 // Arrival tickets on the unit's counters (agent scope); the caller's
@@ -1232,38 +1249,43 @@ attn_kernel(AttnLaunch a) {
   uint16_t* qraw = reinterpret_cast<uint16_t*>(slots + a.area_bytes + 16 * kD * sizeof(float));
   const int slot = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const size_t unit = (size_t)b * a.H + h;
-  const int nwg = a.n_wg > 0 ? a.n_wg : 1;
-
-  if (slot < a.n_wg) stream_slot<FAM, NA, MAXB>(a, slot, h, b, qs, qraw, cst, slots, merge);
-  // the unit's last workgroup (given fewer blocks) also attends to the
-  // 16-bit residual window
-  if (slot == nwg - 1) {
-    __syncthreads();   // the merge area and the query rows are read until here
-    residual_slot(a, b, h, qs, reinterpret_cast<uint16_t*>(slots), part_ptr(a, unit, a.n_wg));
+  // slots 0 .. n_wg-1 stream the quantized blocks; slots n_wg .. n_wg +
+  // n_rw - 1 take kResChunk tokens of the 16-bit window each, alongside
+  if (slot < a.n_wg) {
+    stream_slot<FAM, NA, MAXB>(a, slot, h, b, qs, qraw, cst, slots, merge);
+  } else {
+    const int t_lo = a.nq + (slot - a.n_wg) * kResChunk;
+    const int t_hi = t_lo + kResChunk < a.n_tokens ? t_lo + kResChunk : a.n_tokens;
+    residual_slot(a, b, h, qs, reinterpret_cast<uint16_t*>(slots), part_ptr(a, unit, slot),
+                  t_lo, t_hi);
   }
   // publish this workgroup's partials and take a ticket.  Up to kGroup
-  // streaming slots: the last to arrive merges every slot and the window.
-  // More: slots report in groups of kGroup; the last of a group merges it
-  // into a group partial, and the last group to finish merges the group
+  // streaming slots: the last workgroup to arrive merges every slot.  More:
+  // streaming slots report in groups of kGroup, the last of a group merges
+  // it into a group partial; the group mergers and the window slots then
+  // report on the final counter, whose last arrival merges the group
   // partials and the window.  Every counter is left at zero for the next
   // call.
   uint32_t* cnt = a.counters + unit * a.cstride;
   const int ng = (a.n_wg + kGroup - 1) / kGroup;
   if (ng <= 1) {
-    if (take_ticket(cnt) == (uint32_t)(nwg - 1)) {
-      merge_slots(a, unit, merge, 0, a.n_wg, a.n_wg, nullptr);
+    if (take_ticket(cnt) == (uint32_t)(a.n_wg + a.n_rw - 1)) {
+      merge_slots(a, unit, merge, 0, a.n_wg, a.n_wg, a.n_rw, nullptr);
       reset_counter(cnt);
     }
     return;
   }
-  const int g = slot / kGroup;
-  const int gsz = a.n_wg - g * kGroup < kGroup ? a.n_wg - g * kGroup : kGroup;
-  if (take_ticket(cnt + 1 + g) != (uint32_t)(gsz - 1)) return;
-  __syncthreads();   // the merge area is read until here
-  merge_slots(a, unit, merge, g * kGroup, gsz, -1, part_ptr(a, unit, a.n_wg + 1 + g));
-  reset_counter(cnt + 1 + g);
-  if (take_ticket(cnt) != (uint32_t)(ng - 1)) return;
-  merge_slots(a, unit, merge, a.n_wg + 1, ng, a.n_wg, nullptr);
+  if (slot < a.n_wg) {
+    const int g = slot / kGroup;
+    const int gsz = a.n_wg - g * kGroup < kGroup ? a.n_wg - g * kGroup : kGroup;
+    if (take_ticket(cnt + 1 + g) != (uint32_t)(gsz - 1)) return;
+    __syncthreads();   // the merge area is read until here
+    merge_slots(a, unit, merge, g * kGroup, gsz, 0, 0,
+                part_ptr(a, unit, a.n_wg + a.n_rw + g));
+    reset_counter(cnt + 1 + g);
+  }
+  if (take_ticket(cnt) != (uint32_t)(ng + a.n_rw - 1)) return;
+  merge_slots(a, unit, merge, a.n_wg + a.n_rw, ng, a.n_wg, a.n_rw, nullptr);
   reset_counter(cnt);
 }
 
@@ -1276,7 +1298,7 @@ attn_kernel(AttnLaunch a) {
 #define RQ_DEFINE_ATTN_LAUNCHER(FAM, NA, MAXB, NAME)                            \
   namespace rq {                                                                \
   hipError_t NAME(const AttnLaunch& a, size_t lds, hipStream_t s) {             \
-    dim3 grid(a.n_wg > 0 ? a.n_wg : 1, a.H, a.B);                               \
+    dim3 grid(a.n_wg + a.n_rw, a.H, a.B);                                       \
     hipLaunchKernelGGL((attn_kernel<FAM, NA, MAXB>), grid, dim3(kThreads), lds, \
                        s, a);                                                   \
     return hipGetLastError();                                                   \

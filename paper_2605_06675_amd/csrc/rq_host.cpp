@@ -130,10 +130,8 @@ size_t lds_limit() {
   return n;
 }
 
-constexpr long kResidualBlocks = 12;
-
 struct SplitPlan {
-  int nq, n_wg, blk_per_wg;
+  int nq, n_wg, blk_per_wg, n_rw;
 };
 
 // Compute units of the current device (queried once; 256 when no device
@@ -155,11 +153,13 @@ int cu_count() {
 
 // Workgroups (four waves each) per (batch, kv-head) unit.  The grid is sized
 // to one resident round with every CU busy: three workgroups per CU (the
-// attention kernel runs three waves per SIMD), split evenly over the units;
-// the last workgroup of a unit also takes its residual window.
+// attention kernel runs three waves per SIMD), split evenly over the units.
+// The 16-bit window goes to n_rw more workgroups per unit, 32 tokens each,
+// which run alongside.
 SplitPlan plan_splits(const rq_cache* c, int n_tokens, int wg_per_cu = 3) {
   SplitPlan p;
   p.nq = n_quantized(n_tokens, c->residual);
+  p.n_rw = (n_tokens - p.nq + rq::kAttnResChunk - 1) / rq::kAttnResChunk;
   const long nblk = p.nq / rq::kChunk;
   const long units = (long)c->batch * c->n_kv_heads;
   long per = 0;
@@ -167,12 +167,10 @@ SplitPlan plan_splits(const rq_cache* c, int n_tokens, int wg_per_cu = 3) {
   if (env && std::atoi(env) > 0) {
     per = std::atoi(env) < 4 ? 4 : std::atoi(env);
   } else {
-    // the last workgroup of a unit also attends to the residual window,
-    // which costs about as much as kResidualBlocks quantized blocks
-    long target = (long)cu_count() * wg_per_cu / units;
+    // one resident round: the window workgroups take their places in it
+    long target = (long)cu_count() * wg_per_cu / units - p.n_rw;
     if (target < 1) target = 1;
-    const long work = nblk + (nblk > 0 ? kResidualBlocks : 0);
-    per = (work + target - 1) / target;
+    per = (nblk + target - 1) / target;
     if (per < 4) per = 4;
   }
   p.blk_per_wg = (int)per;
@@ -195,13 +193,13 @@ int counter_stride(const rq_cache* c) {
 }
 
 // Workspace: per-unit arrival counters (zero between calls), padded to 256
-// bytes, then the partials [B][H][n_wg + 1 + groups][G][2 + 128] floats.
+// bytes, then the partials [B][H][n_wg + n_rw + groups][G][2 + 128] floats.
 uint64_t attn_counter_bytes(const rq_cache* c) {
   return ((uint64_t)c->batch * c->n_kv_heads * counter_stride(c) * sizeof(uint32_t) + 255) /
          256 * 256;
 }
 
-int part_stride(const SplitPlan& p) { return p.n_wg + 1 + merge_groups(p.n_wg); }
+int part_stride(const SplitPlan& p) { return p.n_wg + p.n_rw + merge_groups(p.n_wg); }
 
 uint64_t attn_ws_bytes(const rq_cache* c, const SplitPlan& p) {
   const uint64_t G = c->n_q_heads / c->n_kv_heads;
@@ -360,6 +358,7 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
   a.nq = p.nq;
   a.n_tokens = n_tokens;
   a.n_wg = p.n_wg;
+  a.n_rw = p.n_rw;
   a.blk_per_wg = p.blk_per_wg;
   a.is_bf16 = c->dtype == RQ_BF16;
   a.family = c->family;

@@ -13,6 +13,7 @@ constexpr int kChunk = 32;       // codes per packed chunk = tokens per block
 constexpr int kMetaBlockKivi = 512;   // bytes of KIVI metadata per block
 constexpr int kMetaBlockTok = 64;     // bytes of per-token metadata per block
 constexpr int kAttnGroup = 16;        // streaming slots per merge group
+constexpr int kAttnResChunk = 32;     // window tokens per window workgroup
 
 // Per-layer view of the bit table: byte offsets of each (head, kind) code
 // region and its bit-width.  Passed by value as a kernel argument, so a
@@ -53,8 +54,8 @@ struct AttnLaunch {
   const uint16_t* resid;  // this layer
   float* out;             // [B][Hq][128]
   float* part;            // [B][H][pstride][G][2 + 128] (max, sum, acc);
-                          // slots 0..n_wg-1 streaming, n_wg the residual
-                          // window, then one per merge group
+                          // slots 0..n_wg-1 streaming, n_wg..n_wg+n_rw-1
+                          // the residual window, then one per merge group
   uint32_t* counters;     // [B][H][cstride] arrival counters, zero between calls
   int pstride;            // partial slots per unit
   int cstride;            // counters per unit (final + one per group)
@@ -62,6 +63,7 @@ struct AttnLaunch {
   int GP;                 // smallest power of two >= G
   int nq, n_tokens;
   int n_wg, blk_per_wg;   // workgroups per unit streaming blocks
+  int n_rw;               // workgroups per unit on the 16-bit window
   int slot_bytes;         // LDS bytes per wave for one block of this layer
   int area_bytes;         // LDS bytes of the slot/merge/staging area
   int is_bf16, family;
