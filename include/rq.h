@@ -164,7 +164,8 @@ rq_status rq_quantize_kv(const rq_cache* c, int32_t layer, int32_t n_past,
                          const void* k, const void* v, int32_t n_new,
                          rq_stream stream);
 
-/* Workspace bytes rq_decode_attention needs for n_tokens cached tokens. */
+/* Workspace bytes rq_decode_attention needs for n_tokens cached tokens
+ * (it varies with n_tokens; size for the largest call, or re-query). */
 rq_status rq_decode_workspace(const rq_cache* c, int32_t n_tokens,
                               uint64_t* bytes);
 
@@ -174,11 +175,14 @@ rq_status rq_decode_workspace(const rq_cache* c, int32_t n_tokens,
  * K_hat/V_hat the dequantized prefix plus the 16-bit window, query head j
  * reading kv-head j / (n_q_heads / n_kv_heads).  q: device
  * [batch][n_q_heads][128] in dtype; out: device fp32, same shape; ws:
- * device scratch of at least rq_decode_workspace bytes.  Its first
- * 4 * batch * n_kv_heads bytes are arrival counters that must be zero
- * before the first call on a workspace (zero the whole buffer once); every
- * call leaves them zero again.  The rest holds per-call partial results.
- * Calls that share a workspace must not overlap.  Asynchronous. */
+ * device scratch of at least rq_decode_workspace bytes.  Its start holds
+ * arrival counters (a fixed number per (batch, kv-head), set by the cache's
+ * capacity) that must be zero before the first call on a workspace (zero
+ * the whole buffer once); every call leaves them zero again.  The rest
+ * holds per-call partial results.  Calls that share a workspace must not
+ * overlap.  RQ_TURBO: handles kv-heads of 1..4 bits; a layer with a wider
+ * head returns RQ_EUNSUPPORTED.  A layer whose K+V widths need more LDS
+ * than the device offers returns RQ_EUNSUPPORTED.  Asynchronous. */
 rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
                               int32_t n_tokens, const void* q, float* out,
                               float scale, void* ws, uint64_t ws_bytes,
