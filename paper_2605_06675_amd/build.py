@@ -23,6 +23,10 @@ COMMON = [
     # the quantizer decides codes with separately rounded fp32 steps
     "-ffp-contract=off", "-fhip-fp32-correctly-rounded-divide-sqrt",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # keep each atomic as written: the atomic optimizer turns a uniform-
+    # address atomic into a single-lane one whose result is broadcast at
+    # once, which waits for it where the attention kernel means to overlap
+    "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
     "-Wall", "-Wno-unused-function", "-Wno-unused-variable",
 ]
 

@@ -588,17 +588,19 @@ __device__ __forceinline__ void wait_vm() {
   asm volatile("" ::: "memory");
 }
 
-// The first DEPTH blocks of a wave, issued before the workgroup prologue so
-// that their latency overlaps it (bytes and pieces as in Slot<>, at run time).
+// The first DEPTH blocks of a wave (blk0, blk0 + stride, ... below nblk),
+// issued before the workgroup prologue so that their latency overlaps it
+// (bytes and pieces as in Slot<>, at run time).  Returns the copy
+// instructions issued.
 __device__ __forceinline__ int issue_first(const Geo& g, int bk, int bv, int mb, int depth,
-                                           int blk_lo, int blk_hi, int lane, uint8_t* slots,
-                                           int slot_bytes) {
+                                           int blk0, int stride, int nblk, int lane,
+                                           uint8_t* slots, int slot_bytes) {
   const int kb = 512 * bk, vb = 512 * bv, bytes = kb + vb + 2 * mb;
   const int pieces = (bytes + 1023) / 1024;
   int issued = 0;
   for (int j = 0; j < depth; ++j) {
-    const int blk = blk_lo + kWaves * j;
-    if (blk >= blk_hi) break;
+    const int blk = blk0 + stride * j;
+    if (blk >= nblk) break;
     issued += pieces;
     uint8_t* slot = slots + j * slot_bytes;
     for (int k = 0; k < pieces; ++k) {
@@ -629,47 +631,89 @@ __device__ __forceinline__ void wait_vm_rt(int n) {
   }
 }
 
-// The wave's blocks blk_lo, blk_lo + 4, ... < blk_hi, DEPTH of them in
-// flight: block i lives in slot i mod DEPTH, and the slot is refilled with
-// block i + DEPTH once block i has been computed.
+// Block claims of a wave: the unit's blocks beyond the statically assigned
+// first ones go to whichever wave asks next (an agent-scope counter), so
+// that waves and workgroups that run faster take more of them.
+struct Claims {
+  uint32_t* ctr;       // the unit's claim counter (zero between calls)
+  int base;            // first dynamically assigned block
+  int nblk;            // blocks of the unit
+  uint32_t pending;    // result of the claim in flight (lane 0)
+  bool live;           // a claim is in flight
+};
+
+// Lane 0 claims; its result is read -- and waited for -- only where the
+// caller takes lane 0's value.
+__device__ __forceinline__ uint32_t claim_issue(uint32_t* ctr, int lane) {
+  uint32_t r = 0;
+  if (lane == 0) r = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return r;
+}
+
+// The wave's blocks, DEPTH in flight: the static ones issued by
+// issue_first (n_first of them, in slots 0..), then claimed ones.  Each
+// slot is refilled after it has been computed; the claim for the block
+// after that is issued just before the refill, so its result has a whole
+// block's time to come back.  `issued` counts this wave's vector-memory
+// operations (copies and claims) so that the wait for a slot leaves
+// everything issued after it in flight.
 template <int FAM, int NA, int BK, int BV, int DEPTH>
-__device__ __forceinline__ void stream_blocks(const Geo& g, int blk_lo, int blk_hi,
+__device__ __forceinline__ void stream_blocks(const Geo& g, int n_first, Claims& cl, int issued,
                                               uint8_t* slots, int slot_bytes, const LaneOps& lo,
                                               const uint32_t* cst, WaveState<NA>& ws) {
   using S = Slot<FAM, BK, BV>;
-  static_assert(DEPTH >= 1 && DEPTH <= 3, "wait counts below cover up to three slots");
-  // the first DEPTH blocks were issued by issue_first
-  const int n = blk_lo < blk_hi ? (blk_hi - blk_lo + kWaves - 1) / kWaves : 0;
+  static_assert(DEPTH == 2, "the slot marks below assume two slots");
+  // copies of the first blocks end at `issued` minus the later ones
+  int mark0 = issued - (n_first > 1 ? S::pieces : 0);
+  int mark1 = issued;
+  // the first blocks were issued before the claim: see stream_slot
+  int inflight = n_first;
   int cur = 0;
-  for (int i = 0; i < n; ++i) {
-    // blocks i+1 .. i+ahead were issued after block i
-    const int ahead = (n - 1 - i) < (DEPTH - 1) ? (n - 1 - i) : (DEPTH - 1);
-    if (ahead >= 2) wait_vm<2 * S::pieces>();
-    else if (ahead == 1) wait_vm<S::pieces>();
-    else wait_vm<0>();
+  while (inflight > 0) {
+    const int mark = cur == 0 ? mark0 : mark1;
+    wait_vm_rt(issued - mark);
     uint8_t* slot = slots + cur * slot_bytes;
     block_step<FAM, NA, BK, BV>(slot, lo, cst, ws);
-    if (i + DEPTH < n) {
+    --inflight;
+    int next = -1;
+    if (cl.live) {
+      // pinned here: read before the block, the claim would be waited for
+      // one block early
+      asm volatile("" : "+v"(cl.pending) : : "memory");
+      const int v = __builtin_amdgcn_readfirstlane((int)cl.pending);
+      if (cl.base + v < cl.nblk) {
+        next = cl.base + v;
+        cl.pending = claim_issue(cl.ctr, lo.lane);
+        issued += 1;
+      } else {
+        cl.live = false;
+      }
+    }
+    if (next >= 0) {
       // every LDS read of this slot has returned before it is refilled
       __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
       asm volatile("" ::: "memory");
-      issue_block<FAM, BK, BV>(g, blk_lo + kWaves * (i + DEPTH), lo.lane, slot);
+      issue_block<FAM, BK, BV>(g, next, lo.lane, slot);
+      issued += S::pieces;
+      if (cur == 0) mark0 = issued; else mark1 = issued;
+      ++inflight;
     }
-    cur = cur + 1 == DEPTH ? 0 : cur + 1;
+    cur ^= 1;
   }
 }
 
 // Dispatch on the unit's (K bits, V bits), uniform per workgroup; widths
 // above MAXB are not instantiated.
 template <int FAM, int NA, int MAXB, int DEPTH>
-__device__ __forceinline__ void dispatch(int bk, int bv, const Geo& g, int lo_blk, int hi_blk,
-                                         uint8_t* slots, int slot_bytes, const LaneOps& lo,
-                                         const uint32_t* cst, WaveState<NA>& ws) {
+__device__ __forceinline__ void dispatch(int bk, int bv, const Geo& g, int n_first, Claims& cl,
+                                         int issued, uint8_t* slots, int slot_bytes,
+                                         const LaneOps& lo, const uint32_t* cst,
+                                         WaveState<NA>& ws) {
 #define RQ_CASE(K, V)                                                              \
   case (K - 1) * 8 + (V - 1):                                                      \
     if (K <= MAXB && V <= MAXB)                                                    \
       stream_blocks<FAM, NA, (K <= MAXB ? K : 1), (V <= MAXB ? V : 1), DEPTH>(     \
-          g, lo_blk, hi_blk, slots, slot_bytes, lo, cst, ws);                      \
+          g, n_first, cl, issued, slots, slot_bytes, lo, cst, ws);                 \
     break;
 #define RQ_ROW(K) RQ_CASE(K, 1) RQ_CASE(K, 2) RQ_CASE(K, 3) RQ_CASE(K, 4) \
                   RQ_CASE(K, 5) RQ_CASE(K, 6) RQ_CASE(K, 7) RQ_CASE(K, 8)
@@ -925,17 +969,38 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
   g.kmeta = a.meta + (((size_t)h * 2 + 0) * a.B + b) * nblk_cap * per_blk;
   g.vmeta = a.meta + (((size_t)h * 2 + 1) * a.B + b) * nblk_cap * per_blk;
   const int nblk = a.nq / kChunk;
-  const int blo = slot * a.blk_per_wg;
-  int bhi = blo + a.blk_per_wg;
-  if (bhi > nblk) bhi = nblk;
   constexpr int DEPTH = attn_depth(MAXB);
   uint8_t* my_slots = slots + (size_t)wave * DEPTH * a.slot_bytes;
-  // query copy first, then the first blocks: waiting for the queries then
-  // leaves the block copies in flight
+  // The unit's blocks are split between its claim groups (kGroup
+  // workgroups each) in proportion to their sizes.  Inside a group the
+  // first DEPTH blocks of every wave are assigned statically (wave k of the
+  // group's 4 n waves: blocks lo + k, lo + k + 4 n, ...) and the rest are
+  // claimed from the group's counter.  Query copy first, then the first
+  // claim, then the first blocks: waiting for the queries leaves the
+  // others in flight.
+  const int grp = slot / kGroup;
+  const int gw0 = grp * kGroup;
+  const int gn = a.n_wg - gw0 < kGroup ? a.n_wg - gw0 : kGroup;
+  const int g_lo = (int)((long)nblk * gw0 / a.n_wg);
+  const int g_hi = (int)((long)nblk * (gw0 + gn) / a.n_wg);
+  const int wk = (slot - gw0) * kWaves + wave, wstride = gn * kWaves;
+  const int n_first = g_lo + wk < g_hi ? (g_lo + wk + wstride < g_hi ? 2 : 1) : 0;
+  Claims cl;
+  cl.ctr = a.counters + unit * a.cstride + a.claim_off + 32 * grp;
+  cl.base = g_lo + DEPTH * wstride;
+  cl.nblk = g_hi;
+  cl.live = cl.base < g_hi;
+  cl.pending = 0;
   const int nq_ops = issue_query(a, b, h, wave, lane, qraw);
-  const int nb_ops = issue_first(g, bk, bv, per_blk, DEPTH, blo + wave, bhi, lane, my_slots,
-                                 a.slot_bytes);
-  if (nq_ops) wait_vm_rt(nb_ops);
+  int issued = 0;
+  if (cl.live) {
+    cl.pending = claim_issue(cl.ctr, lane);
+    issued += 1;
+  }
+  const int nb_ops = issue_first(g, bk, bv, per_blk, DEPTH, g_lo + wk, wstride, g_hi, lane,
+                                 my_slots, a.slot_bytes);
+  if (nq_ops) wait_vm_rt(issued + nb_ops);
+  issued += nb_ops;
   __syncthreads();
   const uint16_t* qr = qraw + (threadIdx.x >> 4) * kD + 8 * (threadIdx.x & 15);
   const u4 qpiece = (int)(threadIdx.x >> 4) < G ? *reinterpret_cast<const u4*>(qr)
@@ -1008,7 +1073,8 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
   ws.corrZ = (f4){0.f, 0.f, 0.f, 0.f};
   ws.m_run = -INFINITY;
 
-  dispatch<FAM, NA, MAXB, DEPTH>(bk, bv, g, blo + wave, bhi, my_slots, a.slot_bytes, lo, cst, ws);
+  dispatch<FAM, NA, MAXB, DEPTH>(bk, bv, g, n_first, cl, issued, my_slots, a.slot_bytes, lo, cst,
+                                 ws);
 
   // ---- this wave's result per query row: (m, l, out[128]) in canonical form
   const int r = lo.r, col = lo.col, GP = a.GP;
@@ -1272,6 +1338,7 @@ attn_kernel(AttnLaunch a) {
     if (take_ticket(cnt) == (uint32_t)(a.n_wg + a.n_rw - 1)) {
       merge_slots(a, unit, merge, 0, a.n_wg, a.n_wg, a.n_rw, nullptr);
       reset_counter(cnt);
+      reset_counter(cnt + a.claim_off);
     }
     return;
   }
@@ -1283,6 +1350,8 @@ attn_kernel(AttnLaunch a) {
     merge_slots(a, unit, merge, g * kGroup, gsz, 0, 0,
                 part_ptr(a, unit, a.n_wg + a.n_rw + g));
     reset_counter(cnt + 1 + g);
+    // every wave of the group has stopped claiming
+    reset_counter(cnt + a.claim_off + 32 * g);
   }
   if (take_ticket(cnt) != (uint32_t)(ng + a.n_rw - 1)) return;
   merge_slots(a, unit, merge, a.n_wg + a.n_rw, ng, a.n_wg, a.n_rw, nullptr);

@@ -184,13 +184,17 @@ int merge_groups(int n_wg) {
   return ng <= 1 ? 0 : ng;
 }
 
-// Counters per unit: the final one and one per merge group, for the most
-// workgroups any call on this cache can use (at least 4 blocks each), so
-// that the counter area -- zero between calls -- does not move.
-int counter_stride(const rq_cache* c) {
+// Counters per unit, sized for the most workgroups any call on this cache
+// can use (at least 4 blocks each), so that the counter area -- zero
+// between calls -- does not move: the tickets (final, one per merge group)
+// in whole 128-byte lines, then one 128-byte line per claim group of
+// kAttnGroup workgroups (claims contend only within their line).
+int max_groups(const rq_cache* c) {
   const int max_wg = (c->capacity / rq::kChunk + 3) / 4;
-  return 1 + merge_groups(max_wg);
+  return (max_wg + rq::kAttnGroup - 1) / rq::kAttnGroup;
 }
+int claim_offset(const rq_cache* c) { return 32 * ((1 + max_groups(c) + 31) / 32); }
+int counter_stride(const rq_cache* c) { return claim_offset(c) + 32 * max_groups(c); }
 
 // Workspace: per-unit arrival counters (zero between calls), padded to 256
 // bytes, then the partials [B][H][n_wg + n_rw + groups][G][2 + 128] floats.
@@ -348,6 +352,7 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
   a.part = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + attn_counter_bytes(c));
   a.pstride = part_stride(p);
   a.cstride = counter_stride(c);
+  a.claim_off = claim_offset(c);
   a.B = c->batch;
   a.H = c->n_kv_heads;
   a.G = G;

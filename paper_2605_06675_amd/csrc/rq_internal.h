@@ -58,7 +58,10 @@ struct AttnLaunch {
                           // the residual window, then one per merge group
   uint32_t* counters;     // [B][H][cstride] arrival counters, zero between calls
   int pstride;            // partial slots per unit
-  int cstride;            // counters per unit (final + one per group)
+  int cstride;            // counters per unit: tickets (final, one per
+                          // merge group) in the first 128-byte lines, then
+                          // one 128-byte line per claim group
+  int claim_off;          // first claim counter of a unit (in counters)
   int B, H, G, cap, R;
   int GP;                 // smallest power of two >= G
   int nq, n_tokens;
