@@ -14,29 +14,33 @@ hipError_t launch_attn_quarot_b4(const AttnLaunch&, size_t, hipStream_t);
 hipError_t launch_attn_quarot_b8(const AttnLaunch&, size_t, hipStream_t);
 hipError_t launch_attn_turbo_b4(const AttnLaunch&, size_t, hipStream_t);
 
-size_t attention_area_bytes(int G, int slot_bytes, int maxb, int n_wg, int family) {
+size_t attention_area_bytes(int G, int wave_bytes, int family) {
   const size_t merge = (size_t)kWaves * G * (2 + kD) * sizeof(float);
-  const size_t slots = (size_t)kWaves * attn_depth(maxb) * slot_bytes;
-  // the merging workgroup's scratch (and the rotation for TurboQuant) and the
-  // residual-window staging reuse it
+  const size_t rings = (size_t)kWaves * wave_bytes;
+  // the merging workgroup's scratch (and the rotation for TurboQuant) and
+  // the window staging with its scaled query rows reuse it
   const size_t mscratch = (size_t)G * kD * sizeof(float) +
                           (family == RQ_TURBO ? (size_t)kD * kD * sizeof(uint16_t) : 0);
-  size_t m = merge > slots ? merge : slots;
-  m = m > kResLds ? m : kResLds;
+  const size_t window = kResLds + (size_t)16 * kD * sizeof(float);
+  size_t m = merge > rings ? merge : rings;
+  m = m > window ? m : window;
   m = m > mscratch ? m : mscratch;
   return (m + 15) / 16 * 16;
 }
 
-size_t attention_lds_bytes(int G, int slot_bytes, int maxb, int n_wg, int family) {
-  return attention_area_bytes(G, slot_bytes, maxb, n_wg, family) + (size_t)16 * kD * sizeof(float) +
-         (size_t)16 * kD * sizeof(uint16_t);
+size_t attention_tail_bytes(int G, int family) {
+  return (size_t)G * kD * sizeof(uint16_t) + (family == RQ_TURBO ? (size_t)G * kD * sizeof(float) : 0);
+}
+
+size_t attention_lds_bytes(int G, int wave_bytes, int family) {
+  return attention_area_bytes(G, wave_bytes, family) + attention_tail_bytes(G, family);
 }
 
 hipError_t launch_attention(const AttnLaunch& a, hipStream_t s) {
   int maxb = 1;
   for (int h = 0; h < a.H; ++h)
     for (int k = 0; k < 2; ++k) maxb = a.tab.bits[h][k] > maxb ? a.tab.bits[h][k] : maxb;
-  const size_t lds = attention_lds_bytes(a.G, a.slot_bytes, maxb, a.n_wg, a.family);
+  const size_t lds = attention_lds_bytes(a.G, a.wave_bytes, a.family);
   const bool wide = maxb > 4;
   hipError_t e;
   if (a.family == RQ_TURBO)

@@ -49,7 +49,7 @@ namespace rq {
 namespace {
 
 constexpr int kWave = 64;
-constexpr int kWaves = 4;
+constexpr int kWaves = kAttnWaves;
 constexpr int kThreads = kWave * kWaves;
 constexpr float kInvSqrtD = 0.08838834764831845f;
 constexpr uint32_t kMagic = 0x64006400u;   // fp16 pair (1024, 1024)
@@ -62,9 +62,10 @@ constexpr int kGroup = kAttnGroup;
 // Window tokens per window workgroup.
 constexpr int kResChunk = kAttnResChunk;
 
-// LDS slots per wave (blocks in flight).  Two keep three workgroups per CU
-// inside the LDS for widths up to 4 bits.
-constexpr int attn_depth(int maxb) { return maxb <= 4 ? 2 : 2; }
+// Most LDS slots of a wave (blocks in flight).  A wave's region holds as
+// many whole blocks of its unit's widths as fit, up to this many; the host
+// sizes the regions so that at least two fit.
+constexpr int kMaxDepth = kAttnMaxDepth;
 // waves per SIMD the attention kernel is compiled for
 constexpr int kAttnOcc = 3;
 
@@ -560,6 +561,11 @@ struct Geo {
 
 typedef __attribute__((address_space(3))) void lds_void;
 
+// Cache policy of the block copies: non-temporal (the NT bit), so that the
+// cache blocks streamed once per call are the first to leave the L2 and
+// the kernel's code and small shared data stay there across calls.
+constexpr int kStreamPolicy = 2;
+
 template <int FAM, int BK, int BV>
 __device__ __forceinline__ void issue_block(const Geo& g, int blk, int lane, uint8_t* slot) {
   using S = Slot<FAM, BK, BV>;
@@ -572,7 +578,7 @@ __device__ __forceinline__ void issue_block(const Geo& g, int blk, int lane, uin
       else if (o < S::kb + S::vb) src = g.vreg + (size_t)blk * S::vb + (o - S::kb);
       else if (o < S::kb + S::vb + S::mb) src = g.kmeta + (size_t)blk * S::mb + (o - S::kb - S::vb);
       else src = g.vmeta + (size_t)blk * S::mb + (o - S::kb - S::vb - S::mb);
-      __builtin_amdgcn_global_load_lds(src, (lds_void*)(slot + 1024 * k), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(src, (lds_void*)(slot + 1024 * k), 16, 0, kStreamPolicy);
     }
   }
 }
@@ -588,21 +594,20 @@ __device__ __forceinline__ void wait_vm() {
   asm volatile("" ::: "memory");
 }
 
-// The first DEPTH blocks of a wave (blk0, blk0 + stride, ... below nblk),
-// issued before the workgroup prologue so that their latency overlaps it
-// (bytes and pieces as in Slot<>, at run time).  Returns the copy
-// instructions issued.
-__device__ __forceinline__ int issue_first(const Geo& g, int bk, int bv, int mb, int depth,
+// Static blocks j0 .. j1-1 of a wave's ring (block blk0 + j stride, below
+// nblk, into slot j at j * bytes; bytes and pieces as in Slot<>, at run
+// time).  Returns the copy instructions issued.
+__device__ __forceinline__ int issue_first(const Geo& g, int bk, int bv, int mb, int j0, int j1,
                                            int blk0, int stride, int nblk, int lane,
-                                           uint8_t* slots, int slot_bytes) {
+                                           uint8_t* slots) {
   const int kb = 512 * bk, vb = 512 * bv, bytes = kb + vb + 2 * mb;
   const int pieces = (bytes + 1023) / 1024;
   int issued = 0;
-  for (int j = 0; j < depth; ++j) {
+  for (int j = j0; j < j1; ++j) {
     const int blk = blk0 + stride * j;
     if (blk >= nblk) break;
     issued += pieces;
-    uint8_t* slot = slots + j * slot_bytes;
+    uint8_t* slot = slots + j * bytes;
     for (int k = 0; k < pieces; ++k) {
       const int o = 16 * lane + 1024 * k;
       if (o < bytes) {
@@ -611,7 +616,7 @@ __device__ __forceinline__ int issue_first(const Geo& g, int bk, int bv, int mb,
         else if (o < kb + vb) src = g.vreg + (size_t)blk * vb + (o - kb);
         else if (o < kb + vb + mb) src = g.kmeta + (size_t)blk * mb + (o - kb - vb);
         else src = g.vmeta + (size_t)blk * mb + (o - kb - vb - mb);
-        __builtin_amdgcn_global_load_lds(src, (lds_void*)(slot + 1024 * k), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(src, (lds_void*)(slot + 1024 * k), 16, 0, kStreamPolicy);
       }
     }
   }
@@ -650,29 +655,38 @@ __device__ __forceinline__ uint32_t claim_issue(uint32_t* ctr, int lane) {
   return r;
 }
 
-// The wave's blocks, DEPTH in flight: the static ones issued by
-// issue_first (n_first of them, in slots 0..), then claimed ones.  Each
-// slot is refilled after it has been computed; the claim for the block
-// after that is issued just before the refill, so its result has a whole
-// block's time to come back.  `issued` counts this wave's vector-memory
-// operations (copies and claims) so that the wait for a slot leaves
-// everything issued after it in flight.
-template <int FAM, int NA, int BK, int BV, int DEPTH>
-__device__ __forceinline__ void stream_blocks(const Geo& g, int n_first, Claims& cl, int issued,
-                                              uint8_t* slots, int slot_bytes, const LaneOps& lo,
+// The wave's blocks, up to `depth` (2 .. kMaxDepth) in flight in a ring of
+// slots of the block's exact size.  Its n_static statically assigned blocks
+// (blk0 + j stride into slot j) come first: the prologue issued the first
+// two, the others follow one per computed block, so that the ring fills
+// while the first blocks are computed rather than in one burst that would
+// hold the wave's issue behind full memory queues.  Then claimed blocks:
+// each slot is refilled after it has been computed; the claim for the
+// block after that is issued just before the refill, so its result has a
+// whole block's time to come back.  `issued` counts this wave's
+// vector-memory operations (copies and claims) so that the wait for a slot
+// leaves everything issued after it in flight.  Claims exist only when all
+// `depth` slots receive a static block, so blocks are always consumed in
+// ring order.
+template <int FAM, int NA, int BK, int BV>
+__device__ __forceinline__ void stream_blocks(const Geo& g, int depth, int n_static, int blk0,
+                                              int stride, Claims& cl, int issued,
+                                              uint8_t* slots, const LaneOps& lo,
                                               const uint32_t* cst, WaveState<NA>& ws) {
   using S = Slot<FAM, BK, BV>;
-  static_assert(DEPTH == 2, "the slot marks below assume two slots");
-  // copies of the first blocks end at `issued` minus the later ones
-  int mark0 = issued - (n_first > 1 ? S::pieces : 0);
-  int mark1 = issued;
-  // the first blocks were issued before the claim: see stream_slot
-  int inflight = n_first;
-  int cur = 0;
+  static_assert(kMaxDepth == 4, "the ring below rotates four marks");
+  // m0: `issued` just after the copies of the block in the current slot,
+  // m1.. those of the next slots in ring order
+  const int n0 = n_static < 2 ? n_static : 2;
+  int m0 = issued - (n0 - 1) * S::pieces;
+  int m1 = m0 + S::pieces, m2 = m1, m3 = m1;
+  int inflight = n0;
+  int ramp = n0;   // next static block (and slot), two ahead of the current
+  int off = 0;
+  const int ring = depth * S::bytes;
   while (inflight > 0) {
-    const int mark = cur == 0 ? mark0 : mark1;
-    wait_vm_rt(issued - mark);
-    uint8_t* slot = slots + cur * slot_bytes;
+    wait_vm_rt(issued - m0);
+    uint8_t* slot = slots + off;
     block_step<FAM, NA, BK, BV>(slot, lo, cst, ws);
     --inflight;
     int next = -1;
@@ -681,39 +695,48 @@ __device__ __forceinline__ void stream_blocks(const Geo& g, int n_first, Claims&
       // one block early
       asm volatile("" : "+v"(cl.pending) : : "memory");
       const int v = __builtin_amdgcn_readfirstlane((int)cl.pending);
-      if (cl.base + v < cl.nblk) {
-        next = cl.base + v;
-        cl.pending = claim_issue(cl.ctr, lo.lane);
-        issued += 1;
-      } else {
-        cl.live = false;
-      }
+      if (cl.base + v < cl.nblk) next = cl.base + v;
+      else cl.live = false;
     }
-    if (next >= 0) {
-      // every LDS read of this slot has returned before it is refilled
-      __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
-      asm volatile("" ::: "memory");
-      issue_block<FAM, BK, BV>(g, next, lo.lane, slot);
+    // every LDS read of this slot has returned before it is refilled
+    __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+    asm volatile("" ::: "memory");
+    if (ramp < n_static) {
+      issue_block<FAM, BK, BV>(g, blk0 + ramp * stride, lo.lane, slots + ramp * S::bytes);
       issued += S::pieces;
-      if (cur == 0) mark0 = issued; else mark1 = issued;
+      m2 = issued;
+      ++ramp;
       ++inflight;
     }
-    cur ^= 1;
+    int mnew = m0;
+    if (next >= 0) {
+      cl.pending = claim_issue(cl.ctr, lo.lane);
+      issued += 1;
+      issue_block<FAM, BK, BV>(g, next, lo.lane, slot);
+      issued += S::pieces;
+      mnew = issued;
+      ++inflight;
+    }
+    m0 = m1;
+    m1 = depth == 2 ? mnew : m2;
+    m2 = depth == 3 ? mnew : m3;
+    m3 = mnew;
+    off = off + S::bytes == ring ? 0 : off + S::bytes;
   }
 }
 
 // Dispatch on the unit's (K bits, V bits), uniform per workgroup; widths
 // above MAXB are not instantiated.
-template <int FAM, int NA, int MAXB, int DEPTH>
-__device__ __forceinline__ void dispatch(int bk, int bv, const Geo& g, int n_first, Claims& cl,
-                                         int issued, uint8_t* slots, int slot_bytes,
-                                         const LaneOps& lo, const uint32_t* cst,
+template <int FAM, int NA, int MAXB>
+__device__ __forceinline__ void dispatch(int bk, int bv, const Geo& g, int depth, int n_static,
+                                         int blk0, int stride, Claims& cl, int issued,
+                                         uint8_t* slots, const LaneOps& lo, const uint32_t* cst,
                                          WaveState<NA>& ws) {
 #define RQ_CASE(K, V)                                                              \
   case (K - 1) * 8 + (V - 1):                                                      \
     if (K <= MAXB && V <= MAXB)                                                    \
-      stream_blocks<FAM, NA, (K <= MAXB ? K : 1), (V <= MAXB ? V : 1), DEPTH>(     \
-          g, n_first, cl, issued, slots, slot_bytes, lo, cst, ws);                 \
+      stream_blocks<FAM, NA, (K <= MAXB ? K : 1), (V <= MAXB ? V : 1)>(            \
+          g, depth, n_static, blk0, stride, cl, issued, slots, lo, cst, ws);       \
     break;
 #define RQ_ROW(K) RQ_CASE(K, 1) RQ_CASE(K, 2) RQ_CASE(K, 3) RQ_CASE(K, 4) \
                   RQ_CASE(K, 5) RQ_CASE(K, 6) RQ_CASE(K, 7) RQ_CASE(K, 8)
@@ -793,7 +816,7 @@ typedef __bf16 abf8 __attribute__((ext_vector_type(8)));
 
 __device__ __forceinline__ void rotate_queries(const AttnLaunch& a, int h, const uint16_t* qraw,
                                                float (*qs)[kD]) {
-  const int tid = threadIdx.x, wave = tid / kWave, lane = tid & (kWave - 1);
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid / kWave), lane = tid & (kWave - 1);
   const int r = lane & 15, g = lane >> 4;
   const uint16_t* Rh = a.rot + (size_t)h * kD * kD;
 #pragma unroll
@@ -802,7 +825,8 @@ __device__ __forceinline__ void rotate_queries(const AttnLaunch& a, int h, const
     f4 d = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
-      const u4 qa = *reinterpret_cast<const u4*>(&qraw[r * kD + 32 * ks + 8 * g]);
+      // rows >= G (outputs unused) read row 0: qraw holds G rows
+      const u4 qa = *reinterpret_cast<const u4*>(&qraw[(r < a.G ? r : 0) * kD + 32 * ks + 8 * g]);
       u4 rb = gptr(reinterpret_cast<const u4*>(&Rh[(16 * nt + r) * kD + 32 * ks + 8 * g]))[0];
       if (a.is_bf16) {
         d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(abf8, qa),
@@ -852,7 +876,7 @@ constexpr size_t kResLds = (size_t)2 * kResTok * kResRow * sizeof(uint16_t);
 __device__ __forceinline__ void residual_slot(const AttnLaunch& a, int b, int h,
                                               float (*qs)[kD], uint16_t* stage,
                                               float* dst, int t_lo, int t_hi) {
-  const int tid = threadIdx.x, wave = tid / kWave, lane = tid & (kWave - 1);
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid / kWave), lane = tid & (kWave - 1);
   const int cap = a.R + kChunk;
   const uint16_t* kb = a.resid + (((size_t)b * a.H + h) * 2 + 0) * cap * kD;
   const uint16_t* vb = a.resid + (((size_t)b * a.H + h) * 2 + 1) * cap * kD;
@@ -957,7 +981,7 @@ template <int FAM, int NA, int MAXB>
 __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h, int b,
                                             float (*qs)[kD], uint16_t* qraw, uint32_t* cst,
                                             uint8_t* slots, float* merge) {
-  const int tid = threadIdx.x, wave = tid / kWave, lane = tid & (kWave - 1);
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid / kWave), lane = tid & (kWave - 1);
   const size_t unit = (size_t)b * a.H + h;
   const int G = a.G;
   const int bk = a.tab.bits[h][0], bv = a.tab.bits[h][1];
@@ -969,25 +993,30 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
   g.kmeta = a.meta + (((size_t)h * 2 + 0) * a.B + b) * nblk_cap * per_blk;
   g.vmeta = a.meta + (((size_t)h * 2 + 1) * a.B + b) * nblk_cap * per_blk;
   const int nblk = a.nq / kChunk;
-  constexpr int DEPTH = attn_depth(MAXB);
-  uint8_t* my_slots = slots + (size_t)wave * DEPTH * a.slot_bytes;
+  // this unit's ring: as many whole blocks as the wave's region holds
+  const int blk_bytes = 512 * (bk + bv) + 2 * per_blk;
+  int depth = a.wave_bytes / blk_bytes;
+  depth = depth < kMaxDepth ? depth : kMaxDepth;
+  uint8_t* my_slots = slots + (size_t)wave * a.wave_bytes;
   // The unit's blocks are split between its claim groups (kGroup
   // workgroups each) in proportion to their sizes.  Inside a group the
-  // first DEPTH blocks of every wave are assigned statically (wave k of the
-  // group's 4 n waves: blocks lo + k, lo + k + 4 n, ...) and the rest are
-  // claimed from the group's counter.  Query copy first, then the first
-  // claim, then the first blocks: waiting for the queries leaves the
-  // others in flight.
+  // first `depth` blocks of every wave are assigned statically (wave k of
+  // the group's 4 n waves: blocks lo + k, lo + k + 4 n, ...) and the rest
+  // are claimed from the group's counter.  Query copy first, then the first
+  // claim and the first block: waiting for the queries leaves those in
+  // flight.  The second block follows once the query operands are built,
+  // the others while the first ones are computed.
   const int grp = slot / kGroup;
   const int gw0 = grp * kGroup;
   const int gn = a.n_wg - gw0 < kGroup ? a.n_wg - gw0 : kGroup;
   const int g_lo = (int)((long)nblk * gw0 / a.n_wg);
   const int g_hi = (int)((long)nblk * (gw0 + gn) / a.n_wg);
   const int wk = (slot - gw0) * kWaves + wave, wstride = gn * kWaves;
-  const int n_first = g_lo + wk < g_hi ? (g_lo + wk + wstride < g_hi ? 2 : 1) : 0;
+  int n_static = 0;
+  for (int j = 0; j < depth; ++j) n_static += g_lo + wk + j * wstride < g_hi ? 1 : 0;
   Claims cl;
   cl.ctr = a.counters + unit * a.cstride + a.claim_off + 32 * grp;
-  cl.base = g_lo + DEPTH * wstride;
+  cl.base = g_lo + depth * wstride;
   cl.nblk = g_hi;
   cl.live = cl.base < g_hi;
   cl.pending = 0;
@@ -997,18 +1026,10 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
     cl.pending = claim_issue(cl.ctr, lane);
     issued += 1;
   }
-  const int nb_ops = issue_first(g, bk, bv, per_blk, DEPTH, g_lo + wk, wstride, g_hi, lane,
-                                 my_slots, a.slot_bytes);
+  const int nb_ops = issue_first(g, bk, bv, per_blk, 0, 1, g_lo + wk, wstride, g_hi, lane,
+                                 my_slots);
   if (nq_ops) wait_vm_rt(issued + nb_ops);
   issued += nb_ops;
-  __syncthreads();
-  const uint16_t* qr = qraw + (threadIdx.x >> 4) * kD + 8 * (threadIdx.x & 15);
-  const u4 qpiece = (int)(threadIdx.x >> 4) < G ? *reinterpret_cast<const u4*>(qr)
-                                                 : (u4){0u, 0u, 0u, 0u};
-  if (FAM == RQ_TURBO)
-    rotate_queries(a, h, qraw, qs);
-  else
-    store_queries(a, qpiece, FAM == RQ_QUAROT, qs);
   if (tid < 8) cst[tid] = tid < 4 ? kOnes : 0u;
   __syncthreads();
   LaneOps lo;
@@ -1019,15 +1040,62 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
   lo.GP = a.GP;
   lo.gsub = lo.col / a.GP;
   {
-    // static QK operands: k-slot pair (kb, k') = channels 32r + 4kb + k'
-    // and 32r + 16 + 4kb + k' of query col mod GP
+    // this lane's query row j = col mod GP, channels 32 r .. 32 r + 31
+    // (the rotated row for QuaRot and TurboQuant), scaled
     const int j = lo.col & (a.GP - 1);
+    float qv[32];
+    if (FAM == RQ_TURBO) {
+      rotate_queries(a, h, qraw, qs);
+#pragma unroll
+      for (int i = 0; i < 32; ++i) qv[i] = j < G ? qs[j][32 * lo.r + i] : 0.0f;
+    } else {
+      const u4* src = reinterpret_cast<const u4*>(qraw + j * kD + 32 * lo.r);
+#pragma unroll
+      for (int c8 = 0; c8 < 4; ++c8) {
+        const u4 w4 = j < G ? src[c8] : (u4){0u, 0u, 0u, 0u};
+        const uint32_t w[4] = {w4.x, w4.y, w4.z, w4.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          qv[8 * c8 + 2 * e] = widen(w[e] & 0xffffu, a.is_bf16);
+          qv[8 * c8 + 2 * e + 1] = widen(w[e] >> 16, a.is_bf16);
+        }
+      }
+      float f = a.qscale;
+      if (FAM == RQ_QUAROT) {
+        // unnormalised Walsh-Hadamard transform of the row, stages of
+        // stride 1, 2, .., 64 (lower index x + y, upper x - y): strides up
+        // to 16 inside the lane's 32 channels, 32 and 64 across the lanes
+        // holding the other quarters (r ^ 1, r ^ 2)
+#pragma unroll
+        for (int hh = 1; hh < 32; hh *= 2)
+#pragma unroll
+          for (int i = 0; i < 32; ++i)
+            if ((i & hh) == 0) {
+              const float x = qv[i], y = qv[i + hh];
+              qv[i] = x + y;
+              qv[i + hh] = x - y;
+            }
+#pragma unroll
+        for (int st = 1; st <= 2; st *= 2) {
+          const bool upper = (lo.r & st) != 0;
+#pragma unroll
+          for (int i = 0; i < 32; ++i) {
+            const float o = xor_shfl(qv[i], 16 * st);
+            qv[i] = upper ? o - qv[i] : qv[i] + o;
+          }
+        }
+        f *= kInvSqrtD;
+      }
+#pragma unroll
+      for (int i = 0; i < 32; ++i) qv[i] *= f;
+    }
+    // static QK operands: k-slot pair (kb, k') = channels 32r + 4kb + k'
+    // and 32r + 16 + 4kb + k'
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
-        const int c0 = 32 * lo.r + 4 * kb + kk;
-        const float q0 = j < G ? qs[j][c0] : 0.0f, q1 = j < G ? qs[j][c0 + 16] : 0.0f;
+        const float q0 = qv[4 * kb + kk], q1 = qv[16 + 4 * kb + kk];
         const float wgt = FAM == RQ_TURBO ? 1.0f : __builtin_ldexpf(1.0f, -kpos(bk, 4 * kb + kk));
         const h2 vh = {(_Float16)(q0 * wgt), (_Float16)(q1 * wgt)};
         const h2 vz = {(_Float16)q0, (_Float16)q1};
@@ -1065,6 +1133,7 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
       }
     }
   }
+  issued += issue_first(g, bk, bv, per_blk, 1, 2, g_lo + wk, wstride, g_hi, lane, my_slots);
   WaveState<NA> ws;
 #pragma unroll
   for (int nt = 0; nt < 8; ++nt) ws.acc[nt] = (f4){0.f, 0.f, 0.f, 0.f};
@@ -1073,8 +1142,8 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
   ws.corrZ = (f4){0.f, 0.f, 0.f, 0.f};
   ws.m_run = -INFINITY;
 
-  dispatch<FAM, NA, MAXB, DEPTH>(bk, bv, g, n_first, cl, issued, my_slots, a.slot_bytes, lo, cst,
-                                 ws);
+  dispatch<FAM, NA, MAXB>(bk, bv, g, depth, n_static, g_lo + wk, wstride, cl, issued, my_slots,
+                          lo, cst, ws);
 
   // ---- this wave's result per query row: (m, l, out[128]) in canonical form
   const int r = lo.r, col = lo.col, GP = a.GP;
@@ -1305,14 +1374,16 @@ __global__ void __launch_bounds__(kThreads, kAttnOcc)
 attn_kernel(AttnLaunch a) {
   __shared__ u4 cst4[2];             // fp16 ones (4 dwords), zeros (4 dwords)
   uint32_t* cst = reinterpret_cast<uint32_t*>(cst4);
-  // one area used in turn for the per-wave block slots while streaming and
-  // the wave merge area [kWaves][G][2 + 128] floats; behind it the query
-  // rows (float [16][128]) and their 16-bit copy (uint16 [16][128])
+  // one area used in turn for the waves' block rings while streaming and
+  // the wave merge area [kWaves][G][2 + 128] floats (window workgroups:
+  // staging, then their scaled query rows); behind it the G 16-bit query
+  // rows (uint16 [G][128]) and, for TurboQuant, the G rotated rows (float
+  // [G][128])
   extern __shared__ u4 dyn[];
   uint8_t* slots = reinterpret_cast<uint8_t*>(dyn);
   float* merge = reinterpret_cast<float*>(dyn);
-  float (*qs)[kD] = reinterpret_cast<float (*)[kD]>(slots + a.area_bytes);
-  uint16_t* qraw = reinterpret_cast<uint16_t*>(slots + a.area_bytes + 16 * kD * sizeof(float));
+  uint16_t* qraw = reinterpret_cast<uint16_t*>(slots + a.area_bytes);
+  float (*qs)[kD] = reinterpret_cast<float (*)[kD]>(slots + a.area_bytes + a.G * kD * 2);
   const int slot = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const size_t unit = (size_t)b * a.H + h;
   // slots 0 .. n_wg-1 stream the quantized blocks; slots n_wg .. n_wg +
@@ -1322,8 +1393,8 @@ attn_kernel(AttnLaunch a) {
   } else {
     const int t_lo = a.nq + (slot - a.n_wg) * kResChunk;
     const int t_hi = t_lo + kResChunk < a.n_tokens ? t_lo + kResChunk : a.n_tokens;
-    residual_slot(a, b, h, qs, reinterpret_cast<uint16_t*>(slots), part_ptr(a, unit, slot),
-                  t_lo, t_hi);
+    residual_slot(a, b, h, reinterpret_cast<float (*)[kD]>(slots + kResLds),
+                  reinterpret_cast<uint16_t*>(slots), part_ptr(a, unit, slot), t_lo, t_hi);
   }
   // publish this workgroup's partials and take a ticket.  Up to kGroup
   // streaming slots: the last workgroup to arrive merges every slot.  More:

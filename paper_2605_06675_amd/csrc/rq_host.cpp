@@ -130,9 +130,55 @@ size_t lds_limit() {
   return n;
 }
 
+// LDS bytes of one CU (queried once; 160 KiB, the gfx950 size, when no
+// device can be queried).
+size_t lds_per_cu() {
+  static size_t n = 0;
+  if (n == 0) {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) ==
+            hipSuccess &&
+        v > 0)
+      n = (size_t)v;
+    else
+      n = 163840;
+  }
+  return n;
+}
+
 struct SplitPlan {
   int nq, n_wg, blk_per_wg, n_rw;
 };
+
+// LDS shape of the attention kernel for one layer: the most workgroups per
+// CU (three, the kernel's occupancy, down to one) whose share of the CU's
+// LDS gives every wave a ring of at least two blocks of the layer's widest
+// kv-head.  A share is rounded down to whole 2 KiB (an allocation granule
+// coarser than 512 bytes was measured to lose the third workgroup), less
+// 64 bytes for the static LDS.  False when not even one workgroup per CU
+// fits.
+struct AttnShape {
+  int wg_per_cu, wave_bytes;
+  size_t lds;
+};
+
+bool attn_shape(const rq_cache* c, int max_blk_bytes, AttnShape* out) {
+  const int G = c->n_q_heads / c->n_kv_heads;
+  const size_t tail = rq::attention_tail_bytes(G, c->family);
+  for (int w = 3; w >= 1; --w) {
+    size_t share = (lds_per_cu() / w) / 2048 * 2048 - 64;
+    share = share < lds_limit() ? share : lds_limit();
+    if (share <= tail) continue;
+    const int wave = (int)((share - tail) / rq::kAttnWaves / 16 * 16);
+    if (wave < 2 * max_blk_bytes) continue;
+    const size_t lds = rq::attention_lds_bytes(G, wave, c->family);
+    if (lds > share) continue;
+    *out = AttnShape{w, wave, lds};
+    return true;
+  }
+  return false;
+}
 
 // Compute units of the current device (queried once; 256 when no device
 // can be queried, e.g. for host-only sizing calls).
@@ -325,18 +371,27 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
     return fail(RQ_EINVAL, "NULL device pointer");
   if (!std::isfinite(scale)) return fail(RQ_EINVAL, "scale is not finite");
   const rq::LayerTable tab = layer_table(c, layer);
-  int maxb = 1, maxkv = 0;
+  int maxb = 1;
   for (int h = 0; h < c->n_kv_heads; ++h) {
     const int kb = tab.bits[h][0], vb = tab.bits[h][1];
     maxb = kb > maxb ? kb : maxb;
     maxb = vb > maxb ? vb : maxb;
-    maxkv = kb + vb > maxkv ? kb + vb : maxkv;
   }
   if (c->family == RQ_TURBO && maxb > 4)
     return fail(RQ_EUNSUPPORTED,
                 "TurboQuant decode attention handles widths up to 4 bits (layer %d has %d)",
                 layer, maxb);
-  const SplitPlan p = plan_splits(c, n_tokens);
+  int max_blk = 0;
+  for (int h = 0; h < c->n_kv_heads; ++h) {
+    const int bb = 512 * (tab.bits[h][0] + tab.bits[h][1]) + 2 * meta_per_block(c);
+    max_blk = bb > max_blk ? bb : max_blk;
+  }
+  AttnShape shape;
+  if (!attn_shape(c, max_blk, &shape))
+    return fail(RQ_EUNSUPPORTED,
+                "layer %d: two %d-byte blocks per wave do not fit the LDS of a CU "
+                "(K+V bit-widths of one kv-head are too wide)", layer, max_blk);
+  const SplitPlan p = plan_splits(c, n_tokens, shape.wg_per_cu);
   const uint64_t need = attn_ws_bytes(c, p);
   if (ws_bytes < need)
     return fail(RQ_ESMALLWS, "workspace %llu bytes < %llu needed",
@@ -374,13 +429,8 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
     a.cb = c->codebook;
   }
   a.tab = tab;
-  a.slot_bytes = 512 * maxkv + 2 * meta_per_block(c);
-  a.area_bytes = (int)rq::attention_area_bytes(G, a.slot_bytes, maxb, p.n_wg, c->family);
-  const size_t lds = rq::attention_lds_bytes(G, a.slot_bytes, maxb, p.n_wg, c->family);
-  if (lds > lds_limit())
-    return fail(RQ_EUNSUPPORTED,
-                "layer %d needs %zu bytes of LDS per workgroup (device limit %zu): "
-                "K+V bit-widths of one kv-head are too wide", layer, lds, lds_limit());
+  a.wave_bytes = shape.wave_bytes;
+  a.area_bytes = (int)rq::attention_area_bytes(G, a.wave_bytes, c->family);
   hipError_t e = rq::launch_attention(a, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "attention launch");
   return ok();

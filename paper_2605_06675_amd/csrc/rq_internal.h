@@ -14,6 +14,8 @@ constexpr int kMetaBlockKivi = 512;   // bytes of KIVI metadata per block
 constexpr int kMetaBlockTok = 64;     // bytes of per-token metadata per block
 constexpr int kAttnGroup = 16;        // streaming slots per merge group
 constexpr int kAttnResChunk = 32;     // window tokens per window workgroup
+constexpr int kAttnMaxDepth = 4;      // most blocks in flight per attention wave
+constexpr int kAttnWaves = 4;         // waves per attention workgroup
 
 // Per-layer view of the bit table: byte offsets of each (head, kind) code
 // region and its bit-width.  Passed by value as a kernel argument, so a
@@ -67,8 +69,8 @@ struct AttnLaunch {
   int nq, n_tokens;
   int n_wg, blk_per_wg;   // workgroups per unit streaming blocks
   int n_rw;               // workgroups per unit on the 16-bit window
-  int slot_bytes;         // LDS bytes per wave for one block of this layer
-  int area_bytes;         // LDS bytes of the slot/merge/staging area
+  int wave_bytes;         // LDS bytes of one wave's block ring
+  int area_bytes;         // LDS bytes of the ring/merge/staging area
   int is_bf16, family;
   float qscale;           // scale * log2(e)
   const uint16_t* rot;    // TurboQuant: this layer's rotations [H][128][128] bf16
@@ -90,10 +92,14 @@ hipError_t launch_quantize(const QuantLaunch& a, hipStream_t s);
 hipError_t launch_quantize_turbo(const QuantLaunch& a, hipStream_t s);
 hipError_t launch_ring(const RingLaunch& a, hipStream_t s);
 hipError_t launch_attention(const AttnLaunch& a, hipStream_t s);
-// LDS bytes of the attention kernel for a layer (query rows, block slots
-// and merge area share one allocation)
-size_t attention_area_bytes(int G, int slot_bytes, int maxb, int n_wg, int family);
-size_t attention_lds_bytes(int G, int slot_bytes, int maxb, int n_wg, int family);
+// LDS of the attention kernel: the area (the waves' block rings while
+// streaming; the wave merge, window staging and merging scratch after or
+// instead), then the 16-bit query rows and, for TurboQuant, the rotated
+// query rows.  attention_area_bytes: the area for rings of wave_bytes each.
+size_t attention_area_bytes(int G, int wave_bytes, int family);
+size_t attention_lds_bytes(int G, int wave_bytes, int family);
+// LDS after the area: G 16-bit query rows, then (TurboQuant) G rotated rows
+size_t attention_tail_bytes(int G, int family);
 hipError_t launch_calibrate(const CalibLaunch& a, hipStream_t s);
 
 }  // namespace rq
