@@ -62,6 +62,8 @@ constexpr int kGroup = kAttnGroup;
 // Window tokens per window workgroup.
 constexpr int kResChunk = kAttnResChunk;
 
+// Wave priority of everything but the block loop (s_setprio operand).
+constexpr int kSetupPrio = 2;
 // Most LDS slots of a wave (blocks in flight).  A wave's region holds as
 // many whole blocks of its unit's widths as fit, up to this many; the host
 // sizes the regions so that at least two fit.
@@ -123,6 +125,22 @@ __host__ __device__ __forceinline__ constexpr int vpos(int b, int i) {
   const int w = plane_w(b, 0);
   return (w == 8 ? 8 * (i & 1) : i * w) - vshift(b, i);
 }
+// kpos and vpos of every width as a table, for set-up code where the width
+// is a run-time value (the helpers above loop and divide)
+struct FieldPos {
+  int8_t k[9][16];
+  int8_t v[9][4];
+};
+__host__ __device__ constexpr FieldPos make_field_pos() {
+  FieldPos t{};
+  for (int b = 1; b <= 8; ++b) {
+    for (int i = 0; i < 16; ++i) t.k[b][i] = (int8_t)kpos(b, i);
+    for (int i = 0; i < 4; ++i) t.v[b][i] = (int8_t)vpos(b, i);
+  }
+  return t;
+}
+__constant__ const FieldPos kFieldPos = make_field_pos();
+
 // fp16 bits of 2^-e (0 <= e <= 14), exact
 constexpr uint32_t h_pow2_neg(int e) { return (uint32_t)(15 - e) << 10; }
 constexpr uint32_t h_pair(uint32_t h) { return h | (h << 16); }
@@ -364,8 +382,10 @@ __device__ __forceinline__ void kpart(const SlotPtrs& sp, const LaneOps& lo, flo
     for (int i = 0; i < 16; ++i) Bq[i] = lo.qh[i];
     X = lo.corrK;
   }
-  S0 = X;
-  S1 = X;
+  // KIVI: the score chains start from zero and take the (block-constant)
+  // X chain at the end, so the two run side by side on the matrix cores
+  S0 = FAM == RQ_KIVI ? (f4){0.f, 0.f, 0.f, 0.f} : X;
+  S1 = S0;
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb) {
     const h8 Bk = make_h8(Bq[4 * kb], Bq[4 * kb + 1], Bq[4 * kb + 2], Bq[4 * kb + 3]);
@@ -389,7 +409,13 @@ __device__ __forceinline__ void kpart(const SlotPtrs& sp, const LaneOps& lo, flo
                 Bk, S1);
     }
   }
-  if constexpr (FAM != RQ_KIVI) {
+  if constexpr (FAM == RQ_KIVI) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      S0[i] += X[i];
+      S1[i] += X[i];
+    }
+  } else {
     // per-token scales: dword 4r+i of the pair-ordered scales holds tokens
     // (4r+i, 16+4r+i)
     const u4 sv = sp.km[r];
@@ -1091,12 +1117,14 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
     }
     // static QK operands: k-slot pair (kb, k') = channels 32r + 4kb + k'
     // and 32r + 16 + 4kb + k'
+    const int8_t* kp = kFieldPos.k[bk];
+    const int8_t* vp = kFieldPos.v[bv];
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
         const float q0 = qv[4 * kb + kk], q1 = qv[16 + 4 * kb + kk];
-        const float wgt = FAM == RQ_TURBO ? 1.0f : __builtin_ldexpf(1.0f, -kpos(bk, 4 * kb + kk));
+        const float wgt = FAM == RQ_TURBO ? 1.0f : __builtin_ldexpf(1.0f, -kp[4 * kb + kk]);
         const h2 vh = {(_Float16)(q0 * wgt), (_Float16)(q1 * wgt)};
         const h2 vz = {(_Float16)q0, (_Float16)q1};
         lo.qh[4 * kb + kk] = as_u32(vh);
@@ -1104,7 +1132,7 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
       }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int e = vpos(bv, i);
+      const int e = vp[i];
       lo.wv[i] = h_pair((uint32_t)(15 - e) << 10);
       const _Float16 v = (_Float16)(-(1024.0f + (float)(1 << (bv - 1)) * __builtin_ldexpf(1.0f, e)));
       const h2 vv = {v, v};
@@ -1122,7 +1150,7 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
         uint32_t c[4];
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
-          const _Float16 v = (_Float16)(-(1024.0f + off * __builtin_ldexpf(1.0f, kpos(bk, 4 * kb + kk))));
+          const _Float16 v = (_Float16)(-(1024.0f + off * __builtin_ldexpf(1.0f, kp[4 * kb + kk])));
           const h2 vv = {v, v};
           c[kk] = as_u32(vv);
         }
@@ -1142,8 +1170,12 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
   ws.corrZ = (f4){0.f, 0.f, 0.f, 0.f};
   ws.m_run = -INFINITY;
 
+  // blocks at normal priority; what comes before and after at raised
+  // priority (see attn_kernel)
+  __builtin_amdgcn_s_setprio(0);
   dispatch<FAM, NA, MAXB>(bk, bv, g, depth, n_static, g_lo + wk, wstride, cl, issued, my_slots,
                           lo, cst, ws);
+  __builtin_amdgcn_s_setprio(kSetupPrio);
 
   // ---- this wave's result per query row: (m, l, out[128]) in canonical form
   const int r = lo.r, col = lo.col, GP = a.GP;
@@ -1386,6 +1418,11 @@ attn_kernel(AttnLaunch a) {
   float (*qs)[kD] = reinterpret_cast<float (*)[kD]>(slots + a.area_bytes + a.G * kD * 2);
   const int slot = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const size_t unit = (size_t)b * a.H + h;
+  // Set-up, the window, the partial write and the merges run at a raised
+  // wave priority: they share SIMDs with other workgroups' block loops, and
+  // a unit finishes only after its slowest set-up and its merge, so they
+  // go first; the block loops run at normal priority.
+  __builtin_amdgcn_s_setprio(kSetupPrio);
   // slots 0 .. n_wg-1 stream the quantized blocks; slots n_wg .. n_wg +
   // n_rw - 1 take kResChunk tokens of the 16-bit window each, alongside
   if (slot < a.n_wg) {
