@@ -3,8 +3,8 @@
 //
 // Grid (workgroup slot, kv-head, batch), four waves per workgroup.  Slots
 // 0 .. n_wg-1 stream the quantized 32-token blocks of their (batch, kv-head)
-// unit (about three workgroups per CU in all); the last slot, given fewer
-// blocks, also attends to the 16-bit residual window.  Each workgroup
+// unit (about three workgroups per CU in all); the first slots first attend
+// to the 16-bit residual window, 32 tokens each.  Each workgroup
 // writes a partial (max, sum, acc) with cache-coherent stores and takes a
 // ticket from a per-unit counter; the last to arrive merges the unit's
 // partials and writes the output (QuaRot: rotated back).  A wave streams every
@@ -1423,34 +1423,42 @@ attn_kernel(AttnLaunch a) {
   // a unit finishes only after its slowest set-up and its merge, so they
   // go first; the block loops run at normal priority.
   __builtin_amdgcn_s_setprio(kSetupPrio);
-  // slots 0 .. n_wg-1 stream the quantized blocks; slots n_wg .. n_wg +
-  // n_rw - 1 take kResChunk tokens of the 16-bit window each, alongside
-  if (slot < a.n_wg) {
-    stream_slot<FAM, NA, MAXB>(a, slot, h, b, qs, qraw, cst, slots, merge);
-  } else {
-    const int t_lo = a.nq + (slot - a.n_wg) * kResChunk;
+  // The unit's nx workgroups: slot s first takes the 16-bit window chunks
+  // s, s + nx, .. (kResChunk tokens each, partial n_wg + chunk; the area is
+  // their staging), then streams its share of the quantized blocks (slots
+  // 0 .. n_wg-1).  The window thus costs a few workgroups some of their
+  // blocks (the claims hand those to the others) instead of holding
+  // workgroups of its own.
+  const int nx = a.n_wg > 0 ? a.n_wg : 1;
+  for (int c = slot; c < a.n_rw; c += nx) {
+    const int t_lo = a.nq + c * kResChunk;
     const int t_hi = t_lo + kResChunk < a.n_tokens ? t_lo + kResChunk : a.n_tokens;
     residual_slot(a, b, h, reinterpret_cast<float (*)[kD]>(slots + kResLds),
-                  reinterpret_cast<uint16_t*>(slots), part_ptr(a, unit, slot), t_lo, t_hi);
+                  reinterpret_cast<uint16_t*>(slots), part_ptr(a, unit, a.n_wg + c), t_lo, t_hi);
+    __syncthreads();   // the staging area is reused
   }
+  // the block stream counts this wave's memory operations from zero: the
+  // window's partial stores complete first
+  if (slot < a.n_rw) wait_vm<0>();
+  if (slot < a.n_wg) stream_slot<FAM, NA, MAXB>(a, slot, h, b, qs, qraw, cst, slots, merge);
   // publish this workgroup's partials and take a ticket.  Up to kGroup
-  // streaming slots: the last workgroup to arrive merges every slot.  More:
-  // streaming slots report in groups of kGroup, the last of a group merges
-  // it into a group partial; the group mergers and the window slots then
-  // report on the final counter, whose last arrival merges the group
-  // partials and the window.  Every counter is left at zero for the next
-  // call.
+  // workgroups: the last to arrive merges every slot and the window.  More:
+  // they report in groups of kGroup, the last of a group merges it into a
+  // group partial; the group mergers then report on the final counter,
+  // whose last arrival merges the group partials and the window.  Every
+  // counter is left at zero for the next call.
   uint32_t* cnt = a.counters + unit * a.cstride;
   const int ng = (a.n_wg + kGroup - 1) / kGroup;
   if (ng <= 1) {
-    if (take_ticket(cnt) == (uint32_t)(a.n_wg + a.n_rw - 1)) {
+    if (take_ticket(cnt) == (uint32_t)(nx - 1)) {
       merge_slots(a, unit, merge, 0, a.n_wg, a.n_wg, a.n_rw, nullptr);
       reset_counter(cnt);
       reset_counter(cnt + a.claim_off);
     }
     return;
   }
-  if (slot < a.n_wg) {
+  {
+    // two levels: every workgroup streams (nx = n_wg > kGroup)
     const int g = slot / kGroup;
     const int gsz = a.n_wg - g * kGroup < kGroup ? a.n_wg - g * kGroup : kGroup;
     if (take_ticket(cnt + 1 + g) != (uint32_t)(gsz - 1)) return;
@@ -1461,7 +1469,7 @@ attn_kernel(AttnLaunch a) {
     // every wave of the group has stopped claiming
     reset_counter(cnt + a.claim_off + 32 * g);
   }
-  if (take_ticket(cnt) != (uint32_t)(ng + a.n_rw - 1)) return;
+  if (take_ticket(cnt) != (uint32_t)(ng - 1)) return;
   merge_slots(a, unit, merge, a.n_wg + a.n_rw, ng, a.n_wg, a.n_rw, nullptr);
   reset_counter(cnt);
 }
@@ -1475,7 +1483,7 @@ attn_kernel(AttnLaunch a) {
 #define RQ_DEFINE_ATTN_LAUNCHER(FAM, NA, MAXB, NAME)                            \
   namespace rq {                                                                \
   hipError_t NAME(const AttnLaunch& a, size_t lds, hipStream_t s) {             \
-    dim3 grid(a.n_wg + a.n_rw, a.H, a.B);                                       \
+    dim3 grid(a.n_wg > 0 ? a.n_wg : 1, a.H, a.B);                               \
     hipLaunchKernelGGL((attn_kernel<FAM, NA, MAXB>), grid, dim3(kThreads), lds, \
                        s, a);                                                   \
     return hipGetLastError();                                                   \

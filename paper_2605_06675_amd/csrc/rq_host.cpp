@@ -200,8 +200,8 @@ int cu_count() {
 // Workgroups (four waves each) per (batch, kv-head) unit.  The grid is sized
 // to one resident round with every CU busy: three workgroups per CU (the
 // attention kernel runs three waves per SIMD), split evenly over the units.
-// The 16-bit window goes to n_rw more workgroups per unit, 32 tokens each,
-// which run alongside.
+// The 16-bit window is n_rw chunks of 32 tokens, taken by the unit's first
+// workgroups before their blocks.
 SplitPlan plan_splits(const rq_cache* c, int n_tokens, int wg_per_cu = 3) {
   SplitPlan p;
   p.nq = n_quantized(n_tokens, c->residual);
@@ -213,8 +213,8 @@ SplitPlan plan_splits(const rq_cache* c, int n_tokens, int wg_per_cu = 3) {
   if (env && std::atoi(env) > 0) {
     per = std::atoi(env) < 4 ? 4 : std::atoi(env);
   } else {
-    // one resident round: the window workgroups take their places in it
-    long target = (long)cu_count() * wg_per_cu / units - p.n_rw;
+    // one resident round
+    long target = (long)cu_count() * wg_per_cu / units;
     if (target < 1) target = 1;
     per = (nblk + target - 1) / target;
     if (per < 4) per = 4;
