@@ -899,9 +899,10 @@ constexpr size_t kResLds = (size_t)2 * kResTok * kResRow * sizeof(uint16_t);
 // Wave w takes query rows w, w+4, ...; lane = token for the scores, lane =
 // channel pair for PV.  stage: LDS for one chunk (kResLds bytes), qs: LDS
 // for the query rows.
-__device__ __forceinline__ void residual_slot(const AttnLaunch& a, int b, int h,
-                                              float (*qs)[kD], uint16_t* stage,
-                                              float* dst, int t_lo, int t_hi) {
+template <bool BF16>
+__device__ __forceinline__ void residual_slot_t(const AttnLaunch& a, int b, int h,
+                                                float (*qs)[kD], uint16_t* stage,
+                                                float* dst, int t_lo, int t_hi) {
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid / kWave), lane = tid & (kWave - 1);
   const int cap = a.R + kChunk;
   const uint16_t* kb = a.resid + (((size_t)b * a.H + h) * 2 + 0) * cap * kD;
@@ -959,8 +960,8 @@ __device__ __forceinline__ void residual_slot(const AttnLaunch& a, int b, int h,
           const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            s = __builtin_fmaf(qs[j][8 * c8 + 2 * e], widen(ww[e] & 0xffffu, a.is_bf16), s);
-            s = __builtin_fmaf(qs[j][8 * c8 + 2 * e + 1], widen(ww[e] >> 16, a.is_bf16), s);
+            s = __builtin_fmaf(qs[j][8 * c8 + 2 * e], widen_t<BF16>(ww[e] & 0xffffu), s);
+            s = __builtin_fmaf(qs[j][8 * c8 + 2 * e + 1], widen_t<BF16>(ww[e] >> 16), s);
           }
         }
       }
@@ -979,8 +980,8 @@ __device__ __forceinline__ void residual_slot(const AttnLaunch& a, int b, int h,
         const uint32_t w = *reinterpret_cast<const uint32_t*>(vs + i * kResRow + 2 * lane);
         const float pi = __builtin_bit_cast(
             float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, p), i));
-        c0 = __builtin_fmaf(pi, widen(w & 0xffffu, a.is_bf16), c0);
-        c1 = __builtin_fmaf(pi, widen(w >> 16, a.is_bf16), c1);
+        c0 = __builtin_fmaf(pi, widen_t<BF16>(w & 0xffffu), c0);
+        c1 = __builtin_fmaf(pi, widen_t<BF16>(w >> 16), c1);
       }
       ac0[q] = c0;
       ac1[q] = c1;
@@ -999,6 +1000,13 @@ __device__ __forceinline__ void residual_slot(const AttnLaunch& a, int b, int h,
     st_agent(d + 2 + 2 * lane, ac0[q]);
     st_agent(d + 2 + 2 * lane + 1, ac1[q]);
   }
+}
+
+__device__ __forceinline__ void residual_slot(const AttnLaunch& a, int b, int h,
+                                              float (*qs)[kD], uint16_t* stage,
+                                              float* dst, int t_lo, int t_hi) {
+  if (a.is_bf16) residual_slot_t<true>(a, b, h, qs, stage, dst, t_lo, t_hi);
+  else residual_slot_t<false>(a, b, h, qs, stage, dst, t_lo, t_hi);
 }
 
 // Quantized blocks of workgroup slot `slot` of unit (b, h): stream, merge the

@@ -24,10 +24,16 @@ __device__ __forceinline__ RQ_GLOBAL T* gptr(T* p) {
   return (RQ_GLOBAL T*)p;
 }
 
-__device__ __forceinline__ float widen(uint32_t bits16, int is_bf16) {
-  if (is_bf16) return __uint_as_float(bits16 << 16);
-  _Float16 h = __builtin_bit_cast(_Float16, (uint16_t)bits16);
+template <bool BF16>
+__device__ __forceinline__ float widen_t(uint32_t bits16) {
+  if constexpr (BF16) return __uint_as_float(bits16 << 16);
+  const _Float16 h = __builtin_bit_cast(_Float16, (uint16_t)bits16);
   return (float)h;
+}
+// run-time dtype: both conversions and a select, no branch
+__device__ __forceinline__ float widen(uint32_t bits16, int is_bf16) {
+  const float b = widen_t<true>(bits16), f = widen_t<false>(bits16);
+  return is_bf16 ? b : f;
 }
 
 // fp32 -> fp16, nearest-even, saturated at +-65504.  Returns raw bits.
