@@ -230,6 +230,20 @@ def test_short_context_window_only():
         _check_attention(kvc, units, workloads.F16, 1, 2, 4)
 
 
+@pytest.mark.parametrize("T", [100, 200, 700])
+def test_window_chunks_outnumber_workgroups(T):
+    # a 160-token window is 5 or 6 chunks of 32 tokens, more than the few
+    # streaming workgroups of these short caches, so a workgroup takes
+    # several chunks before its blocks (T=100: nothing quantized, one
+    # workgroup takes every chunk; T=700: 5 workgroups, 6 chunks)
+    bits = np.array([[[2, 3], [4, 1]]])
+    kvc, ks, vs, _ = _build(workloads.KIVI, workloads.F16, 2, 4, T, 160,
+                            bits, batch=2, cap=768)
+    units = _check_cache(workloads.KIVI, workloads.F16, kvc, ks, vs, bits,
+                         160, 2, 2, T)
+    _check_attention(kvc, units, workloads.F16, 2, 2, 4)
+
+
 def test_no_window():
     bits = np.array([[[1, 2], [4, 3]]])
     kvc, ks, vs, _ = _build(workloads.KIVI, workloads.BF16, 2, 16, 256, 0,
