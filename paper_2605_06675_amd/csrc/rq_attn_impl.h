@@ -662,6 +662,18 @@ __device__ __forceinline__ void wait_vm_rt(int n) {
   }
 }
 
+// The wait before a block of P copy instructions: in steady state n, the
+// operations issued after its copies, is (depth - 1) (P + 1) (the later
+// slots' copies and claims), tested first so that the block loop usually
+// takes one compare; any other n goes through wait_vm_rt.
+template <int P>
+__device__ __forceinline__ void wait_slot(int n) {
+  if (n == 3 * (P + 1)) wait_vm<3 * (P + 1)>();
+  else if (n == 2 * (P + 1)) wait_vm<2 * (P + 1)>();
+  else if (n == P + 1) wait_vm<P + 1>();
+  else wait_vm_rt(n);
+}
+
 // Block claims of a wave: the unit's blocks beyond the statically assigned
 // first ones go to whichever wave asks next (an agent-scope counter), so
 // that waves and workgroups that run faster take more of them.
@@ -711,7 +723,7 @@ __device__ __forceinline__ void stream_blocks(const Geo& g, int depth, int n_sta
   int off = 0;
   const int ring = depth * S::bytes;
   while (inflight > 0) {
-    wait_vm_rt(issued - m0);
+    wait_slot<S::pieces>(issued - m0);
     uint8_t* slot = slots + off;
     block_step<FAM, NA, BK, BV>(slot, lo, cst, ws);
     --inflight;
