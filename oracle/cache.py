@@ -24,7 +24,7 @@ import numpy as np
 
 from . import fmt, quant
 
-KIVI, QUAROT, TURBO = 0, 1, 2
+KIVI, QUAROT, TURBO, RTN = 0, 1, 2, 3
 
 
 def n_quantized(T, R):
@@ -104,6 +104,13 @@ class Unit:
             uv, sv = quant.quarot_quant(vq, bv)
             self.k_hat = quant.quarot_dequant(uk, sk, bk)
             self.v_hat = quant.quarot_dequant(uv, sv, bv)
+            self.k_meta = token_meta(sk)
+            self.v_meta = token_meta(sv)
+        elif family == RTN:
+            uk, sk = quant.rtn_quant(kq, bk)
+            uv, sv = quant.rtn_quant(vq, bv)
+            self.k_hat = quant.rtn_dequant(uk, sk, bk)
+            self.v_hat = quant.rtn_dequant(uv, sv, bv)
             self.k_meta = token_meta(sk)
             self.v_meta = token_meta(sv)
         elif family == TURBO:

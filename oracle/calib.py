@@ -12,7 +12,7 @@ import numpy as np
 
 from . import quant
 
-KIVI, QUAROT, TURBO = 0, 1, 2
+KIVI, QUAROT, TURBO, RTN = 0, 1, 2, 3
 
 
 def roundtrip(family, x, b, is_value, rotation=None):
@@ -25,6 +25,9 @@ def roundtrip(family, x, b, is_value, rotation=None):
     if family == QUAROT:
         u, s = quant.quarot_quant(x, b)
         return quant.quarot_dequant(u, s, b)
+    if family == RTN:
+        u, s = quant.rtn_quant(x, b)
+        return quant.rtn_dequant(u, s, b)
     if family == TURBO:
         u, n, _ = quant.turbo_quant(x, rotation, b)
         return quant.turbo_dequant(u, n, rotation, b)

@@ -5,7 +5,9 @@ distortion curve (Sec. 3.4) and names three: KIVI (keys grouped per channel
 across tokens, values per token), QuaRot (a Hadamard rotation, then
 symmetric per-token quantization) and TurboQuant (a random rotation, then a
 per-coordinate codebook) -- Sec. 2, Sec. 3.1, Appendix "Implementation
-Details" and "Quantizer Implementation".  It gives no rounding rules; the ones below are
+Details" and "Quantizer Implementation" -- and, as the weakest base
+quantizer, plain per-token symmetric round-to-nearest (Appendix "RTN Base
+Quantizer").  It gives no rounding rules; the ones below are
 this library's readings (each is listed in the design notes) and both the
 oracle and the GPU kernels follow them bit for bit wherever a floating-point
 decision yields an integer code:
@@ -127,14 +129,15 @@ def quarot_rotate(x):
     return fwht_f32(x) * INV_SQRT_D_F32
 
 
-def quarot_quant(x, b):
-    """Symmetric per-token quantization of the rotated vector.
-    x float32[T][128] -> codes[T][128] (offset binary), s fp16[T].
-      y = rotate(x);  a = max|y|;  s = fp16(a / (2^(b-1) - 1));
-      q = rint(clamp(y * (1/s), -qm, qm));  code = q + 2^(b-1)."""
+def sym_per_token(y, b):
+    """Symmetric per-token quantization of y float32[T][128] over all 128
+    channels -> codes[T][128] (offset binary), s fp16[T].
+      a = max|y|;  s = fp16(a / (2^(b-1) - 1));
+      q = rint(clamp(y * (1/s), -qm, qm));  code = q + 2^(b-1).
+    A token with s == 0 gets q = 0 everywhere."""
     if b < 2:
         raise ValueError("symmetric quantizer needs b >= 2")
-    y = quarot_rotate(x)
+    y = np.asarray(y, dtype=F32)
     qm = F32((1 << (b - 1)) - 1)
     a = np.max(np.abs(y), axis=-1)
     s = fmt.f16_sat(a / qm)
@@ -146,11 +149,34 @@ def quarot_quant(x, b):
     return q + (1 << (b - 1)), s
 
 
+def quarot_quant(x, b):
+    """Symmetric per-token quantization of the rotated vector:
+    sym_per_token(rotate(x), b)."""
+    if b < 2:
+        raise ValueError("symmetric quantizer needs b >= 2")
+    return sym_per_token(quarot_rotate(x), b)
+
+
 def quarot_dequant(u, s, b):
     """x_hat = (1/sqrt(128)) H ((u - 2^(b-1)) s)  (fp64, H symmetric)."""
     yhat = (np.asarray(u, np.float64) - (1 << (b - 1))) * np.asarray(
         s, np.float64)[..., None]
     return yhat @ hadamard() / math.sqrt(D)
+
+
+# ---------------------------------------------------------------------- RTN
+# Round-to-nearest, per-token symmetric (Appendix "RTN Base Quantizer",
+# Table "RTN per-token symmetric on Qwen3-8B"): QuaRot's symmetric step
+# applied to the vector itself, one scale per token over its 128 channels.
+def rtn_quant(x, b):
+    """codes[T][128] (offset binary), s fp16[T] = sym_per_token(x, b)."""
+    return sym_per_token(x, b)
+
+
+def rtn_dequant(u, s, b):
+    """x_hat = (u - 2^(b-1)) s  (fp64)."""
+    return (np.asarray(u, np.float64) - (1 << (b - 1))) * np.asarray(
+        s, np.float64)[..., None]
 
 
 # --------------------------------------------------------------- TurboQuant
