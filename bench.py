@@ -146,6 +146,8 @@ def cpu_baseline(wl, bits_table, seconds):
                     nv = fmt.from_pair_order(u.v_meta).reshape(-1)
                     if wl.family == workloads.QUAROT:
                         kh, vh = oq.quarot_dequant(kc, nk, bk), oq.quarot_dequant(vc, nv, bv)
+                    elif wl.family == workloads.RTN:
+                        kh, vh = oq.rtn_dequant(kc, nk, bk), oq.rtn_dequant(vc, nv, bv)
                     else:
                         kh = oq.turbo_dequant(kc, nk, rot, bk)
                         vh = oq.turbo_dequant(vc, nv, rot, bv)
@@ -183,10 +185,10 @@ def _kivi_meta_values(m):
     return s, z
 
 
-QUANT_KERNEL = {0: "kivi_quant_kernel", 1: "quarot_quant_kernel",
-                2: "turbo_quant_kernel"}
+QUANT_KERNEL = {0: "kivi_quant_kernel", 1: "sym_quant_kernel",
+                2: "turbo_quant_kernel", 3: "sym_quant_kernel"}
 KERNEL_SOURCES = {"kivi_quant_kernel": ["rq_quant.hip"],
-                  "quarot_quant_kernel": ["rq_quant.hip"],
+                  "sym_quant_kernel": ["rq_quant.hip"],
                   "turbo_quant_kernel": ["rq_quant_turbo.hip"],
                   "attn_kernel": ["rq_attn*.hip", "rq_attn_impl.h"]}
 
@@ -378,7 +380,7 @@ def main():
                    "kv_heads": H, "q_heads": Hq, "head_dim": 128,
                    "context": T, "decode_steps": nsteps,
                    "residual_window": wl.residual,
-                   "family": ["kivi", "quarot", "turbo"][wl.family],
+                   "family": ["kivi", "quarot", "turbo", "rtn"][wl.family],
                    "avg_bits": wl.avg_bits, "bit_set": list(wl.bit_set),
                    "attention_bytes_per_step": att_bytes,
                    "quantize_bytes_per_step": q_bytes,

@@ -19,7 +19,7 @@
  *    a call that returns an error has written nothing.  rq_last_error()
  *    then describes the problem (thread-local, valid until the next call
  *    on the same thread).
- *  - head_dim is 128.  Bit-widths are 1..8 (QuaRot needs >= 2).
+ *  - head_dim is 128.  Bit-widths are 1..8 (QuaRot and RTN need >= 2).
  *
  * Numeric formats (bit-exact contract shared with the test oracle)
  *  - K/V inputs are fp16 or bf16 (rq_dtype).  Metadata (scale, zero) is
@@ -34,6 +34,9 @@
  *             stages h = 1, 2, ..., 64 in that order; s = fp16(max|y| /
  *             (2^(b-1) - 1)); code = rint(clamp(y * fp32(1/s), -q, q)) +
  *             2^(b-1), q = 2^(b-1) - 1 (all codes 2^(b-1) when s == 0).
+ *      RTN    the QuaRot step on y = x itself (per-token symmetric
+ *             round-to-nearest, no rotation; Appendix "RTN Base
+ *             Quantizer").
  *      Turbo  n = fp16(fp32(|x|)) (sum of squares and root in fp64);
  *             y = R x, t = y * (sqrt(128) / n) (0 when n == 0); code =
  *             number of thresholds of the b-bit codebook below t.  y is
@@ -59,7 +62,8 @@
  *  meta   KIVI:   [l][h][kind][batch][block][4][s(32), z(32)] fp16, pair
  *                 order; K: group index = chunk q, entries = channels;
  *                 V: group index = channel group cg, entries = tokens.
- *         QuaRot: [l][h][kind][batch][block][s(32 tokens)] fp16, pair order.
+ *         QuaRot, RTN: [l][h][kind][batch][block][s(32 tokens)] fp16,
+ *                 pair order.
  *         Turbo:  [l][h][kind][batch][block][n(32 tokens)] fp16, pair order.
  *  resid  [l][batch][h][kind][R + 32][128] in the input dtype; token t of
  *         the 16-bit window lives in slot t mod (R + 32).
@@ -87,6 +91,7 @@ typedef int32_t rq_status;
 #define RQ_KIVI 0
 #define RQ_QUAROT 1
 #define RQ_TURBO 2
+#define RQ_RTN 3
 
 #define RQ_F16 0
 #define RQ_BF16 1
@@ -104,7 +109,7 @@ typedef void* rq_stream;
  * "static lookup table", Appendix "Runtime Analysis"): host int8
  * [n_layers][n_kv_heads][2], K then V. */
 typedef struct rq_cache {
-  int32_t family;        /* RQ_KIVI, RQ_QUAROT or RQ_TURBO                */
+  int32_t family;        /* RQ_KIVI, RQ_QUAROT, RQ_TURBO or RQ_RTN        */
   int32_t dtype;         /* RQ_F16 or RQ_BF16: K/V/q input type           */
   int32_t n_layers;
   int32_t batch;

@@ -45,7 +45,7 @@ hipError_t launch_attention(const AttnLaunch& a, hipStream_t s) {
   hipError_t e;
   if (a.family == RQ_TURBO)
     e = wide ? hipErrorInvalidValue : launch_attn_turbo_b4(a, lds, s);
-  else if (a.family == RQ_QUAROT)
+  else if (a.family == RQ_QUAROT || a.family == RQ_RTN)   // same kernel, no rotation
     e = (wide ? launch_attn_quarot_b8 : launch_attn_quarot_b4)(a, lds, s);
   else if (a.GP <= 4)
     e = (wide ? launch_attn_kivi_n1_b8 : launch_attn_kivi_n1_b4)(a, lds, s);

@@ -1,5 +1,5 @@
 // Decode attention over the packed mixed-bit cache (KIVI-style,
-// QuaRot-style and TurboQuant-style quantizers).
+// QuaRot-style, TurboQuant-style and per-token symmetric RTN quantizers).
 //
 // Grid (workgroup slot, kv-head, batch), four waves per workgroup.  Slots
 // 0 .. n_wg-1 stream the quantized 32-token blocks of their (batch, kv-head)
@@ -25,6 +25,7 @@
 //   KIVI values  O = sum_t (p_t s_t 2^-P)(1024 + u 2^P)
 //                    + sum_t p_t z_t - 1024 sum_t (p_t s_t 2^-P)
 //   QuaRot       the same with per-token scales and codes u - 2^(b-1).
+//   RTN          QuaRot's path with no rotation of the query or the output.
 //   TurboQuant   codes index the Lloyd-Max centroids, which are not affine
 //                in the code: each pair of codes is looked up in a table of
 //                fp16 centroids held in two to four registers (v_perm_b32,
@@ -1107,7 +1108,8 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
         }
       }
       float f = a.qscale;
-      if (FAM == RQ_QUAROT) {
+      // RTN runs this instantiation with codes in the original domain
+      if (FAM == RQ_QUAROT && a.family == RQ_QUAROT) {
         // unnormalised Walsh-Hadamard transform of the row, stages of
         // stride 1, 2, .., 64 (lower index x + y, upper x - y): strides up
         // to 16 inside the lane's 32 channels, 32 and 64 across the lanes
@@ -1336,7 +1338,7 @@ __device__ __forceinline__ void merge_rows(const AttnLaunch& a, size_t unit, flo
   }
   float* out = a.out + unit * G * kD + (size_t)j * kD + c0;   // (b, h) -> rows h*G..
   const float inv = own ? 1.0f / den : 0.0f;
-  if (a.family == RQ_KIVI) {
+  if (a.family == RQ_KIVI || a.family == RQ_RTN) {
     if (own)
 #pragma unroll
       for (int k = 0; k < E; ++k) out[k] = (num[k] + tail[k]) * inv;

@@ -116,7 +116,7 @@ calib_kernel(CalibLaunch a) {
   // QuaRot: rotate each token (same butterflies as the quantizer), then
   // measure the error of the symmetric levels in the rotated domain, which
   // equals the original-domain error up to fp32 rounding (the rotation is
-  // orthonormal).
+  // orthonormal).  RTN: the same symmetric levels on the token itself.
   const int t = lane >> 1, hb = lane & 1;
   float v[64];
 #pragma unroll
@@ -133,36 +133,37 @@ calib_kernel(CalibLaunch a) {
       }
     }
   }
+  if (a.family == RQ_QUAROT) {
 #pragma unroll
-  for (int hh = 1; hh < 32; hh *= 2) {
+    for (int hh = 1; hh < 32; hh *= 2) {
 #pragma unroll
-    for (int base = 0; base < 64; base += 2 * hh) {
+      for (int base = 0; base < 64; base += 2 * hh) {
 #pragma unroll
-      for (int i = 0; i < hh; ++i) {
-        const float p = v[base + i], q = v[base + i + hh];
-        v[base + i] = p + q;
-        v[base + i + hh] = p - q;
+        for (int i = 0; i < hh; ++i) {
+          const float p = v[base + i], q = v[base + i + hh];
+          v[base + i] = p + q;
+          v[base + i + hh] = p - q;
+        }
       }
     }
-  }
 #pragma unroll
-  for (int i = 0; i < 64; ++i) {
-    const float o = dpp_xor1(v[i]);
-    v[i] = hb ? (o - v[i]) : (v[i] + o);
-  }
+    for (int i = 0; i < 64; ++i) {
+      const float o = dpp_xor1(v[i]);
+      v[i] = hb ? (o - v[i]) : (v[i] + o);
+    }
 #pragma unroll
-  for (int i = 0; i < 32; ++i) {
-    const float p = v[i], q = v[32 + i];
-    v[i] = p + q;
-    v[32 + i] = p - q;
+    for (int i = 0; i < 32; ++i) {
+      const float p = v[i], q = v[32 + i];
+      v[i] = p + q;
+      v[32 + i] = p - q;
+    }
+    const float c = 0.08838834764831845f;
+#pragma unroll
+    for (int i = 0; i < 64; ++i) v[i] = v[i] * c;
   }
-  const float c = 0.08838834764831845f;
   float amax = 0.0f;
 #pragma unroll
-  for (int i = 0; i < 64; ++i) {
-    v[i] = v[i] * c;
-    amax = __builtin_fmaxf(amax, __builtin_fabsf(v[i]));
-  }
+  for (int i = 0; i < 64; ++i) amax = __builtin_fmaxf(amax, __builtin_fabsf(v[i]));
   amax = __builtin_fmaxf(amax, dpp_xor1(amax));
   for (int j = 0; j < a.n_bits; ++j) {
     const float qm = (float)((1 << (a.bits[j] - 1)) - 1);

@@ -43,7 +43,8 @@ int meta_per_block(const rq_cache* c) {
 
 rq_status check_cache(const rq_cache* c) {
   if (!c) return fail(RQ_EINVAL, "cache descriptor is NULL");
-  if (c->family != RQ_KIVI && c->family != RQ_QUAROT && c->family != RQ_TURBO)
+  if (c->family != RQ_KIVI && c->family != RQ_QUAROT && c->family != RQ_TURBO &&
+      c->family != RQ_RTN)
     return fail(RQ_EINVAL, "unknown family %d", c->family);
   if (c->family == RQ_TURBO && (!c->rotation || !c->codebook))
     return fail(RQ_EINVAL, "TurboQuant needs the rotation and codebook pointers");
@@ -66,7 +67,7 @@ rq_status check_cache(const rq_cache* c) {
                 c->capacity);
   if (c->residual < 0) return fail(RQ_EINVAL, "residual window must be >= 0");
   if (!c->bits) return fail(RQ_EINVAL, "bit table is NULL");
-  const int lo = c->family == RQ_QUAROT ? 2 : 1;
+  const int lo = (c->family == RQ_QUAROT || c->family == RQ_RTN) ? 2 : 1;
   for (int i = 0; i < c->n_layers * c->n_kv_heads * 2; ++i) {
     const int b = c->bits[i];
     if (b < lo || b > 8)
@@ -454,7 +455,8 @@ rq_status rq_calibrate_distortion(int32_t family, int32_t dtype, const void* x,
                                   const float* codebook, double* mse, double* alpha,
                                   double* beta, double* r2, void* ws,
                                   uint64_t ws_bytes, rq_stream stream) {
-  if (family != RQ_KIVI && family != RQ_QUAROT && family != RQ_TURBO)
+  if (family != RQ_KIVI && family != RQ_QUAROT && family != RQ_TURBO &&
+      family != RQ_RTN)
     return fail(RQ_EINVAL, "unknown family %d", family);
   if (family == RQ_TURBO && (!rotation || !codebook))
     return fail(RQ_EINVAL, "TurboQuant needs the rotation and codebook pointers");
@@ -466,7 +468,7 @@ rq_status rq_calibrate_distortion(int32_t family, int32_t dtype, const void* x,
   if (!x || !bits || !mse || !ws) return fail(RQ_EINVAL, "NULL pointer");
   if ((alpha || beta || r2) && n_bits < 2)
     return fail(RQ_EINVAL, "the fit needs at least two bit-widths");
-  const int lo = family == RQ_QUAROT ? 2 : 1;
+  const int lo = (family == RQ_QUAROT || family == RQ_RTN) ? 2 : 1;
   for (int j = 0; j < n_bits; ++j) {
     if (bits[j] < lo || bits[j] > 8)
       return fail(RQ_EINVAL, "bit-width %d outside %d..8", bits[j], lo);

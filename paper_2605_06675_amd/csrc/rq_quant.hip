@@ -1,5 +1,5 @@
-// Quantize + pack kernels (KIVI-style and QuaRot-style) and the residual
-// window append.  One wave quantizes one 32-token block of one
+// Quantize + pack kernels (KIVI-style, QuaRot-style and plain per-token
+// symmetric RTN) and the residual window append.  One wave quantizes one 32-token block of one
 // (batch entry, kv-head, K|V) unit; the unit's bit-width and code region come
 // from the per-layer table in the kernel arguments.
 //
@@ -428,7 +428,10 @@ kivi_quant_kernel(QuantLaunch a) {
   }
 }
 
-// ---------------------------------------------------------------- QuaRot
+// ------------------------------------------------------- QuaRot and RTN
+// Per-token symmetric quantization over the token's 128 channels; QuaRot
+// (ROT = 1) first applies the orthonormal Hadamard rotation, RTN (ROT = 0)
+// quantizes the vector as it is.
 __device__ __forceinline__ float dpp_xor1(float v) {
   // quad_perm [1,0,3,2]: exchange with lane ^ 1
   return __builtin_bit_cast(
@@ -436,8 +439,9 @@ __device__ __forceinline__ float dpp_xor1(float v) {
                                       0xF, true));
 }
 
-__device__ __forceinline__ void quarot_block(const QuantLaunch& a, Smem& sm, int b, int h,
-                             int kind, int blk, int lane) {
+template <int ROT>
+__device__ __forceinline__ void sym_block(const QuantLaunch& a, Smem& sm, int b, int h,
+                                          int kind, int blk, int lane) {
   const int bits = a.tab.bits[h][kind];
   const int off = 1 << (bits - 1);
   const float qm = (float)(off - 1);
@@ -460,39 +464,40 @@ __device__ __forceinline__ void quarot_block(const QuantLaunch& a, Smem& sm, int
       }
     }
   }
-  // butterflies h = 1..16 inside each 32-channel run
+  if constexpr (ROT) {
+    // butterflies h = 1..16 inside each 32-channel run
 #pragma unroll
-  for (int hh = 1; hh < 32; hh *= 2) {
+    for (int hh = 1; hh < 32; hh *= 2) {
 #pragma unroll
-    for (int base = 0; base < 64; base += 2 * hh) {
+      for (int base = 0; base < 64; base += 2 * hh) {
 #pragma unroll
-      for (int i = 0; i < hh; ++i) {
-        const float x = v[base + i], y = v[base + i + hh];
-        v[base + i] = x + y;
-        v[base + i + hh] = x - y;
+        for (int i = 0; i < hh; ++i) {
+          const float x = v[base + i], y = v[base + i + hh];
+          v[base + i] = x + y;
+          v[base + i + hh] = x - y;
+        }
       }
     }
-  }
-  // h = 32: partner lane holds channel + 32
+    // h = 32: partner lane holds channel + 32
 #pragma unroll
-  for (int i = 0; i < 64; ++i) {
-    const float o = dpp_xor1(v[i]);
-    v[i] = hb ? (o - v[i]) : (v[i] + o);
-  }
-  // h = 64: v[j] <-> v[32 + j] in this lane
+    for (int i = 0; i < 64; ++i) {
+      const float o = dpp_xor1(v[i]);
+      v[i] = hb ? (o - v[i]) : (v[i] + o);
+    }
+    // h = 64: v[j] <-> v[32 + j] in this lane
 #pragma unroll
-  for (int i = 0; i < 32; ++i) {
-    const float x = v[i], y = v[32 + i];
-    v[i] = x + y;
-    v[32 + i] = x - y;
+    for (int i = 0; i < 32; ++i) {
+      const float x = v[i], y = v[32 + i];
+      v[i] = x + y;
+      v[32 + i] = x - y;
+    }
+    const float c = 0.08838834764831845f;  // fp32 nearest to 1/sqrt(128)
+#pragma unroll
+    for (int i = 0; i < 64; ++i) v[i] = v[i] * c;
   }
-  const float c = 0.08838834764831845f;  // fp32 nearest to 1/sqrt(128)
   float amax = 0.0f;
 #pragma unroll
-  for (int i = 0; i < 64; ++i) {
-    v[i] = v[i] * c;
-    amax = __builtin_fmaxf(amax, __builtin_fabsf(v[i]));
-  }
+  for (int i = 0; i < 64; ++i) amax = __builtin_fmaxf(amax, __builtin_fabsf(v[i]));
   amax = __builtin_fmaxf(amax, dpp_xor1(amax));
   const uint16_t s16 = f16_sat(amax / qm);
   const float sf = f16_to_f32(s16);
@@ -535,14 +540,15 @@ __device__ __forceinline__ void quarot_block(const QuantLaunch& a, Smem& sm, int
   }
 }
 
+template <int ROT>
 __global__ void __launch_bounds__(kWave)
-quarot_quant_kernel(QuantLaunch a) {
+sym_quant_kernel(QuantLaunch a) {
   __shared__ Smem sm;
   const int blk = a.blk0 + blockIdx.x;
   const int h = blockIdx.y;
   const int b = blockIdx.z >> 1, kind = blockIdx.z & 1;
   const int lane = threadIdx.x;
-  quarot_block(a, sm, b, h, kind, blk, lane);
+  sym_block<ROT>(a, sm, b, h, kind, blk, lane);
   __syncthreads();
   // metadata of this block
   const int nblk_cap = a.cap / kChunk;
@@ -594,7 +600,10 @@ hipError_t launch_quantize(const QuantLaunch& a, hipStream_t s) {
     }
   } else {
     dim3 grid(a.nblk, a.H, a.B * 2);
-    hipLaunchKernelGGL(quarot_quant_kernel, grid, dim3(kWave), 0, s, a);
+    if (a.family == RQ_QUAROT)
+      hipLaunchKernelGGL(sym_quant_kernel<1>, grid, dim3(kWave), 0, s, a);
+    else
+      hipLaunchKernelGGL(sym_quant_kernel<0>, grid, dim3(kWave), 0, s, a);
   }
   return hipGetLastError();
 }

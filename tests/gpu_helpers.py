@@ -7,7 +7,7 @@ import numpy as np
 import workloads
 from oracle import cache as ocache
 
-KIVI, QUAROT, TURBO = 0, 1, 2
+KIVI, QUAROT, TURBO, RTN = 0, 1, 2, 3
 
 
 def dev(bits16, dtype, device="cuda"):

@@ -137,6 +137,10 @@ def test_descriptor_validation():
                 n_kv_heads=8, n_q_heads=32, capacity=1024, residual=32,
                 bits=bits)
     rq.rq_cache_sizes(rq.make_cache(**good))
+    # RTN shares QuaRot's layout: 64 metadata bytes per block and stream
+    r = rq.rq_cache_sizes(rq.make_cache(**dict(good, family=rq.RQ_RTN)))
+    q = rq.rq_cache_sizes(rq.make_cache(**dict(good, family=rq.RQ_QUAROT)))
+    assert r == q
     cases = [
         (dict(capacity=1000), rq.RQ_EINVAL),
         (dict(n_q_heads=30), rq.RQ_EINVAL),
@@ -144,6 +148,8 @@ def test_descriptor_validation():
         (dict(bits=np.full((1, 8, 2), 9)), rq.RQ_EINVAL),
         (dict(bits=np.full((1, 8, 2), 0)), rq.RQ_EINVAL),
         (dict(family=rq.RQ_QUAROT, bits=np.full((1, 8, 2), 1)), rq.RQ_EINVAL),
+        (dict(family=rq.RQ_RTN, bits=np.full((1, 8, 2), 1)), rq.RQ_EINVAL),
+        (dict(family=4), rq.RQ_EINVAL),
         (dict(family=rq.RQ_TURBO), rq.RQ_EINVAL),   # no rotation/codebook
         (dict(dtype=7), rq.RQ_EINVAL),
         (dict(n_kv_heads=33, n_q_heads=66, bits=np.full((1, 33, 2), 2)),

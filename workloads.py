@@ -29,7 +29,7 @@ import numpy as np
 HEAD_DIM = 128
 SEEDS = (42, 123, 2026)
 
-KIVI, QUAROT, TURBO = 0, 1, 2
+KIVI, QUAROT, TURBO, RTN = 0, 1, 2, 3
 F16, BF16 = 0, 1
 
 
@@ -71,6 +71,13 @@ LLAMA3_8B = Workload("llama3-8b-kv-b16-t8192-kivi-2.5b", KIVI, BF16, 32, 16,
 # at 4.0 average.
 QWEN3_8B = Workload("qwen3-8b-kv-b8-t32768-quarot-4b", QUAROT, BF16, 36, 8, 8,
                     32, 32768, 0, (2, 3, 4, 5, 6), 4.0, 0.76, (13.18, 13.04))
+# Qwen3-8B shaped KV, per-token symmetric RTN (QuaRot's quantizer without the
+# rotation; the paper's weakest base quantizer, run on Qwen3-8B at 3.5 and
+# 4.0 bits), bits {2..6} at 4.0 average; the paper gives no RTN alpha, so
+# QuaRot's planted values stand in.
+QWEN3_8B_RTN = Workload("qwen3-8b-kv-b8-t32768-rtn-4b", RTN, BF16, 36, 8, 8,
+                        32, 32768, 0, (2, 3, 4, 5, 6), 4.0, 0.76,
+                        (13.18, 13.04))
 # Llama-3-70B shaped KV, TurboQuant-style rotation + codebook, bits {2,3,4}
 # at 3.0 average.
 LLAMA3_70B = Workload("llama3-70b-kv-b4-t32768-turbo-3b", TURBO, BF16, 80, 4,
@@ -81,7 +88,7 @@ QWEN3_32B = Workload("qwen3-32b-kv-b1-t131072-kivi-2b", KIVI, BF16, 64, 1, 8,
                      64, 131072, 128, (1, 2, 3, 4), 2.0, 0.81, (17.87, 4.65))
 
 WORKLOADS = {w.name: w for w in (SMALL, LLAMA3_8B, QWEN3_8B, LLAMA3_70B,
-                                 QWEN3_32B)}
+                                 QWEN3_32B, QWEN3_8B_RTN)}
 
 
 def _rng(seed, *stream):
