@@ -11,8 +11,9 @@ Modules
   alloc      reverse waterfilling, greedy integer allocation, brute force
   lloydmax   Lloyd-Max scalar quantizer of N(0,1) (the TurboQuant codebook)
   fmt        fp16/bf16 rounding helpers and the packed code format
-  quant      KIVI-, QuaRot- and TurboQuant-style quantize / dequantize
+  quant      KIVI-, QuaRot-, TurboQuant-style and RTN quantize / dequantize
   cache      residual-window rule and packed-cache assembly for one unit
   attention  fp64 decode attention over a dequantized cache
   calib      per-component distortion sweep
+  sensitivity  Stage-1 gradient sensitivity, weight cap, fit fallback
 """
