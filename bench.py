@@ -221,6 +221,40 @@ def measured_traffic(workload, name):
                + rec["write_bytes"] * rec["write_factor"])
 
 
+def sensitivity_rate(args, wl, dev):
+    """Stage-1 sensitivity (outside the step: it runs once, offline, on
+    gradients of a calibration set): rq_sensitivity over fp32 gradients of
+    16 sequences x calib_tokens positions for every component of the model,
+    timed per call (kernel, reduction, the copy of w and the wait) with HIP
+    events, median of 5 after one warm-up."""
+    import torch
+
+    import paper_2605_06675_amd as rq
+    S, T, n = 16, args.calib_tokens, wl.n_comp
+    g = torch.Generator(device=dev).manual_seed(7)
+    grad = torch.randn((S, n, T, 128), generator=g, device=dev,
+                       dtype=torch.float32)
+    ws = torch.empty(rq.rq_sensitivity_workspace(rq.RQ_F32, S, n, T),
+                     dtype=torch.uint8, device=dev)
+    rq.rq_sensitivity(rq.RQ_F32, grad, ws=ws)
+    times = []
+    for _ in range(5):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        rq.rq_sensitivity(rq.RQ_F32, grad, ws=ws)
+        b.record()
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(b) * 1e3)
+    us = float(np.median(times))
+    nbytes = grad.numel() * 4
+    del grad
+    gbs = nbytes / (us * 1e-6) / 1e9
+    return {"call": f"rq_sensitivity over fp32 gradients [{S}][{n}][{T}][128]",
+            "kernel": "sens_kernel", "bound": "hbm", "bytes": nbytes,
+            "us": round(us, 2), "achieved": round(gbs, 1), "unit": "GB/s",
+            "peak": PEAK_HBM_GBS, "frac": round(gbs / PEAK_HBM_GBS, 4)}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -323,6 +357,8 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 
+    sens = sensitivity_rate(args, wl, dev)
+
     el = lambda p: p[0].elapsed_time(p[1])
     ms = {"calib": float(np.mean([el(r[0]["calib"]) for r in rec])),
           "quantize": float(np.mean([el(r[0]["quantize"]) for r in rec])),
@@ -387,6 +423,7 @@ def main():
                    "fitted_beta_median": round(float(np.nanmedian(beta_fit)), 3)},
         "roofline": rooflines[dom],
         "roofline_by_kernel": rooflines,
+        "sensitivity": sens,
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl, table, args.cpu_seconds)

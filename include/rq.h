@@ -95,6 +95,7 @@ typedef int32_t rq_status;
 
 #define RQ_F16 0
 #define RQ_BF16 1
+#define RQ_F32 2              /* gradients of rq_sensitivity only            */
 
 #define RQ_MAX_KV_HEADS 32
 
@@ -244,6 +245,42 @@ rq_status rq_allocate_bits(int32_t n, const double* w, const double* alpha,
                            const double* beta, double avg_bits, int32_t bmin,
                            int32_t bmax, int32_t* bits_out,
                            double* bits_cont_out, double* J_out);
+
+/* Workspace bytes rq_sensitivity needs. */
+rq_status rq_sensitivity_workspace(int32_t gdtype, int32_t n_seq,
+                                   int32_t n_comp, int32_t n_tokens,
+                                   uint64_t* bytes);
+
+/* Stage-1 gradient sensitivity (Alg. 1 Stage 1; Sec. 3.3 "Sensitivity
+ * Estimation"; Appendix "Temporal aggregation").  grad: device
+ * [n_seq][n_comp][n_tokens][128] in gdtype (RQ_F32, RQ_F16 or RQ_BF16),
+ * 16-byte aligned: the gradient of the loss with respect to each
+ * component's cache (one kv-head's keys or values) at every position of
+ * each calibration sequence, as a backward pass produces it.  For every
+ * component i:
+ *   w[i] = (1/n_seq) sum_s (1/n_tokens) sum_t sum_c grad[s][i][t][c]^2
+ * with the squares and sums in fp64 in a fixed order (deterministic).
+ * w: host [n_comp].  ws: device scratch of rq_sensitivity_workspace bytes.
+ * n_seq and n_comp are at most 65535.  Synchronous: waits for the stream
+ * and copies w to the host. */
+rq_status rq_sensitivity(int32_t gdtype, const void* grad, int32_t n_seq,
+                         int32_t n_comp, int32_t n_tokens, double* w,
+                         void* ws, uint64_t ws_bytes, rq_stream stream);
+
+/* Sensitivity cap (Appendix "Failure modes", mitigation of extreme
+ * outliers): w[i] <- min(w[i], factor * mean(w)) in place, the mean of the
+ * uncapped weights summed in index order in double; the paper uses
+ * factor = 5.  Requires n >= 1, every w finite and >= 0, factor finite and
+ * > 0.  Host only. */
+rq_status rq_cap_weights(int32_t n, double* w, double factor);
+
+/* Fit fallback for poorly fitting components (Appendix "Distortion Model
+ * Parameters", outlier heads): where r2[i] < r2_min, beta[i] <- min(beta[i],
+ * mean(beta)) in place, the mean over all n fitted betas summed in index
+ * order in double; the paper uses r2_min = 0.96.  Requires n >= 1 and
+ * finite beta, r2 and r2_min.  Host only. */
+rq_status rq_fallback_beta(int32_t n, double* beta, const double* r2,
+                           double r2_min);
 
 #ifdef __cplusplus
 }

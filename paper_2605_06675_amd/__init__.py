@@ -18,13 +18,15 @@ LIB_PATH = os.path.join(HERE, "librq.so")
 RQ_OK, RQ_EINVAL, RQ_EINFEASIBLE, RQ_EUNSUPPORTED, RQ_EDEVICE, RQ_ESMALLWS = (
     0, -1, -2, -3, -4, -5)
 RQ_KIVI, RQ_QUAROT, RQ_TURBO, RQ_RTN = 0, 1, 2, 3
-RQ_F16, RQ_BF16 = 0, 1
+RQ_F16, RQ_BF16, RQ_F32 = 0, 1, 2
 RQ_MAX_KV_HEADS = 32
 
 EXPORTS = ("rq_version", "rq_last_error", "rq_cache_sizes", "rq_region_offset",
            "rq_quantize_kv", "rq_decode_workspace", "rq_decode_attention",
            "rq_calibrate_workspace", "rq_calibrate_distortion",
-           "rq_fit_distortion", "rq_allocate_bits", "rq_turbo_codebook")
+           "rq_fit_distortion", "rq_allocate_bits", "rq_turbo_codebook",
+           "rq_sensitivity_workspace", "rq_sensitivity", "rq_cap_weights",
+           "rq_fallback_beta")
 RQ_TURBO_TABLE_FLOATS = 8 * 2 * 256
 
 
@@ -79,6 +81,10 @@ def lib():
             "rq_allocate_bits": (i32, [i32, pd, pd, pd, C.c_double, i32, i32,
                                        pi, pd, pd]),
             "rq_turbo_codebook": (i32, [C.POINTER(C.c_float)]),
+            "rq_sensitivity_workspace": (i32, [i32, i32, i32, i32, pu64]),
+            "rq_sensitivity": (i32, [i32, vp, i32, i32, i32, pd, vp, u64, vp]),
+            "rq_cap_weights": (i32, [i32, pd, C.c_double]),
+            "rq_fallback_beta": (i32, [i32, pd, pd, C.c_double]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)
@@ -243,6 +249,49 @@ def rq_calibrate_distortion(family, dtype, x, is_value, bits, ws=None,
         _tptr(ws),
         ws.numel() * ws.element_size(), _stream(stream)))
     return (mse, *outs)
+
+
+def rq_sensitivity_workspace(gdtype, n_seq, n_comp, n_tokens):
+    v = C.c_uint64()
+    _check(lib().rq_sensitivity_workspace(gdtype, n_seq, n_comp, n_tokens,
+                                          C.byref(v)))
+    return v.value
+
+
+def rq_sensitivity(gdtype, grad, ws=None, stream=None):
+    """grad: torch [n_seq][n_comp][n_tokens][128] on the device (float32,
+    float16 or bfloat16 as gdtype says).  Returns w float64[n_comp]."""
+    import torch
+    n_seq, n_comp, T = grad.shape[0], grad.shape[1], grad.shape[2]
+    need = rq_sensitivity_workspace(gdtype, n_seq, n_comp, T)
+    if ws is None:
+        ws = torch.empty(need, dtype=torch.uint8, device=grad.device)
+    w = np.empty(n_comp)
+    _check(lib().rq_sensitivity(
+        gdtype, _tptr(grad), n_seq, n_comp, T,
+        w.ctypes.data_as(C.POINTER(C.c_double)), _tptr(ws),
+        ws.numel() * ws.element_size(), _stream(stream)))
+    return w
+
+
+def rq_cap_weights(w, factor=5.0):
+    """Returns a capped copy of w."""
+    w = np.array(w, dtype=np.float64)
+    _check(lib().rq_cap_weights(w.size, w.ctypes.data_as(C.POINTER(C.c_double)),
+                                float(factor)))
+    return w
+
+
+def rq_fallback_beta(beta, r2, r2_min=0.96):
+    """Returns a copy of beta with the fallback applied."""
+    beta = np.array(beta, dtype=np.float64)
+    r, rp = _dptr(r2, np.float64)
+    if r.size != beta.size:
+        raise ValueError("beta and r2 differ in length")
+    _check(lib().rq_fallback_beta(beta.size,
+                                  beta.ctypes.data_as(C.POINTER(C.c_double)),
+                                  rp, float(r2_min)))
+    return beta
 
 
 class KVCache:

@@ -566,4 +566,85 @@ rq_status rq_allocate_bits(int32_t n, const double* w, const double* alpha,
   return ok();
 }
 
+rq_status rq_sensitivity_workspace(int32_t gdtype, int32_t n_seq,
+                                   int32_t n_comp, int32_t n_tokens,
+                                   uint64_t* bytes) {
+  if (gdtype != RQ_F32 && gdtype != RQ_F16 && gdtype != RQ_BF16)
+    return fail(RQ_EINVAL, "unknown gradient dtype %d", gdtype);
+  if (n_seq < 1 || n_seq > 65535 || n_comp < 1 || n_comp > 65535 ||
+      n_tokens < 1 || !bytes)
+    return fail(RQ_EINVAL, "bad sensitivity shape (%d, %d, %d)", n_seq, n_comp,
+                n_tokens);
+  const int64_t vecs = (int64_t)n_tokens * rq::kD * (gdtype == RQ_F32 ? 4 : 2) / 16;
+  const int64_t chunks = (vecs + rq::kSensChunkVecs - 1) / rq::kSensChunkVecs;
+  if (chunks > 0x7fffffff) return fail(RQ_EINVAL, "n_tokens %d too large", n_tokens);
+  *bytes = sizeof(double) * ((uint64_t)n_seq * n_comp * chunks + n_comp);
+  return ok();
+}
+
+rq_status rq_sensitivity(int32_t gdtype, const void* grad, int32_t n_seq,
+                         int32_t n_comp, int32_t n_tokens, double* w,
+                         void* ws, uint64_t ws_bytes, rq_stream stream) {
+  uint64_t need = 0;
+  rq_status st = rq_sensitivity_workspace(gdtype, n_seq, n_comp, n_tokens, &need);
+  if (st != RQ_OK) return st;
+  if (!grad || !w || !ws) return fail(RQ_EINVAL, "NULL pointer");
+  if (reinterpret_cast<uintptr_t>(grad) % 16)
+    return fail(RQ_EINVAL, "gradient pointer is not 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(ws) % 8)
+    return fail(RQ_EINVAL, "workspace pointer is not 8-byte aligned");
+  if (ws_bytes < need)
+    return fail(RQ_ESMALLWS, "workspace %llu bytes < %llu needed",
+                (unsigned long long)ws_bytes, (unsigned long long)need);
+  rq::SensLaunch a{};
+  a.grad = grad;
+  a.slab_vecs = (int64_t)n_tokens * rq::kD * (gdtype == RQ_F32 ? 4 : 2) / 16;
+  a.chunks = (int)((a.slab_vecs + rq::kSensChunkVecs - 1) / rq::kSensChunkVecs);
+  a.w = static_cast<double*>(ws);
+  a.partial = a.w + n_comp;
+  a.n_seq = n_seq;
+  a.n_comp = n_comp;
+  a.T = n_tokens;
+  a.dtype = gdtype;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = rq::launch_sensitivity(a, s);
+  if (e != hipSuccess) return hip_fail(e, "sensitivity launch");
+  e = hipMemcpyAsync(w, a.w, sizeof(double) * n_comp, hipMemcpyDeviceToHost, s);
+  if (e != hipSuccess) return hip_fail(e, "sensitivity copy");
+  e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "sensitivity sync");
+  return ok();
+}
+
+rq_status rq_cap_weights(int32_t n, double* w, double factor) {
+  if (n < 1 || !w) return fail(RQ_EINVAL, "need n >= 1 weights");
+  if (!std::isfinite(factor) || !(factor > 0))
+    return fail(RQ_EINVAL, "cap factor must be finite and > 0");
+  double sum = 0.0;
+  for (int i = 0; i < n; ++i) {
+    if (!std::isfinite(w[i]) || w[i] < 0)
+      return fail(RQ_EINVAL, "weight %d is not finite and >= 0", i);
+    sum += w[i];
+  }
+  const double cap = factor * (sum / n);
+  for (int i = 0; i < n; ++i) w[i] = w[i] < cap ? w[i] : cap;
+  return ok();
+}
+
+rq_status rq_fallback_beta(int32_t n, double* beta, const double* r2,
+                           double r2_min) {
+  if (n < 1 || !beta || !r2) return fail(RQ_EINVAL, "need n >= 1 components");
+  if (!std::isfinite(r2_min)) return fail(RQ_EINVAL, "r2_min is not finite");
+  double sum = 0.0;
+  for (int i = 0; i < n; ++i) {
+    if (!std::isfinite(beta[i]) || !std::isfinite(r2[i]))
+      return fail(RQ_EINVAL, "component %d: beta or r2 is not finite", i);
+    sum += beta[i];
+  }
+  const double mean = sum / n;
+  for (int i = 0; i < n; ++i)
+    if (r2[i] < r2_min && mean < beta[i]) beta[i] = mean;
+  return ok();
+}
+
 }  // extern "C"

@@ -102,4 +102,15 @@ size_t attention_lds_bytes(int G, int wave_bytes, int family);
 size_t attention_tail_bytes(int G, int family);
 hipError_t launch_calibrate(const CalibLaunch& a, hipStream_t s);
 
+constexpr int kSensChunkVecs = 8192;  // 16-byte vectors per sensitivity workgroup
+
+struct SensLaunch {
+  const void* grad;       // [n_seq][n_comp][T][128] in dtype
+  double* partial;        // [n_seq][n_comp][chunks]
+  double* w;              // [n_comp]
+  int64_t slab_vecs;      // 16-byte vectors per (sequence, component)
+  int n_seq, n_comp, T, chunks, dtype;
+};
+hipError_t launch_sensitivity(const SensLaunch& a, hipStream_t s);
+
 }  // namespace rq

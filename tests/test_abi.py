@@ -225,3 +225,51 @@ def test_turbo_codebook_matches_oracle():
         assert np.all(np.isinf(tab[b - 1, 0, L - 1:]))
         np.testing.assert_allclose(tab[b - 1, 1, :L], c, rtol=2.0 ** -23)
         assert np.all(tab[b - 1, 1, L:] == 0)
+
+
+# ------------------------------------------------ sensitivity refinements
+def test_cap_weights_matches_oracle():
+    from oracle import sensitivity as osens
+    rng = np.random.default_rng(11)
+    for w in (rng.lognormal(0, 2.0, size=300), np.array([1.0] * 9 + [91.0]),
+              np.array([3.0])):
+        np.testing.assert_array_equal(rq.rq_cap_weights(w, 5.0),
+                                      osens.cap_weights(w, 5.0))
+    for bad in ([-1.0, 2.0], [np.nan, 1.0]):
+        with pytest.raises(rq.RQError) as e:
+            rq.rq_cap_weights(bad)
+        assert e.value.status == rq.RQ_EINVAL
+    with pytest.raises(rq.RQError):
+        rq.rq_cap_weights([1.0, 2.0], 0.0)
+
+
+def test_fallback_beta_matches_oracle():
+    from oracle import sensitivity as osens
+    rng = np.random.default_rng(12)
+    beta = rng.uniform(3.6, 5.3, size=500)
+    r2 = rng.uniform(0.9, 1.0, size=500)
+    np.testing.assert_array_equal(rq.rq_fallback_beta(beta, r2, 0.96),
+                                  osens.fallback_beta(beta, r2, 0.96))
+    with pytest.raises(rq.RQError):
+        rq.rq_fallback_beta([4.0, np.inf], [1.0, 1.0])
+
+
+def test_sensitivity_validates_before_launch():
+    # Every failure below is caught on the host: no device is needed.
+    L = rq.lib()
+    n = rq.rq_sensitivity_workspace(rq.RQ_F32, 16, 512, 512)
+    assert n == 8 * (16 * 512 * 2 + 512)        # 256 KiB slab: 2 chunks of 128 KiB
+    assert rq.rq_sensitivity_workspace(rq.RQ_BF16, 1, 1, 1) == 8 * 2
+    for args in ((7, 1, 1, 1), (rq.RQ_F32, 0, 1, 1), (rq.RQ_F32, 65536, 1, 1),
+                 (rq.RQ_F32, 1, 1, 0)):
+        with pytest.raises(rq.RQError):
+            rq.rq_sensitivity_workspace(*args)
+    w = np.empty(4)
+    wp = w.ctypes.data_as(C.POINTER(C.c_double))
+    fake = C.c_void_p(0x1000)
+    assert L.rq_sensitivity(rq.RQ_F32, None, 1, 4, 8, wp, fake, 1 << 20,
+                            None) == rq.RQ_EINVAL
+    assert L.rq_sensitivity(rq.RQ_F32, C.c_void_p(0x1004), 1, 4, 8, wp, fake,
+                            1 << 20, None) == rq.RQ_EINVAL      # misaligned
+    assert L.rq_sensitivity(rq.RQ_F32, fake, 1, 4, 8, wp, fake, 8,
+                            None) == rq.RQ_ESMALLWS
