@@ -48,42 +48,10 @@ __device__ __forceinline__ void pack_store(const uint32_t c[8], uint32_t* dst) {
   store_words<B>(dst, w);
 }
 
-__device__ __forceinline__ void pack_store_dyn(int bits, const uint32_t c[8], uint32_t* dst) {
-  switch (bits) {
-    case 1: pack_store<1>(c, dst); break;
-    case 2: pack_store<2>(c, dst); break;
-    case 3: pack_store<3>(c, dst); break;
-    case 4: pack_store<4>(c, dst); break;
-    case 5: pack_store<5>(c, dst); break;
-    case 6: pack_store<6>(c, dst); break;
-    case 7: pack_store<7>(c, dst); break;
-    default: pack_store<8>(c, dst); break;
-  }
-}
-
 struct Smem {
   uint32_t codes[kChunk * kD / 4];   // [32 tokens][128 channels] bytes
   uint16_t meta[256];                // one block's metadata (512 B)
 };
-
-// Write this block's packed V chunks: channel c -> b words over 32 tokens.
-__device__ __forceinline__ void pack_values_from_smem(const Smem& sm, int bits,
-                                      uint32_t* region_blk, int lane) {
-  const uint8_t* cb = reinterpret_cast<const uint8_t*>(sm.codes);
-#pragma unroll
-  for (int rep = 0; rep < 2; ++rep) {
-    const int c = lane + rep * kWave;
-    uint32_t w[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      w[i] = (uint32_t)cb[(4 * i + 0) * kD + c] |
-             ((uint32_t)cb[(4 * i + 1) * kD + c] << 8) |
-             ((uint32_t)cb[(4 * i + 2) * kD + c] << 16) |
-             ((uint32_t)cb[(4 * i + 3) * kD + c] << 24);
-    }
-    pack_store_dyn(bits, w, region_blk + (size_t)c * bits);
-  }
-}
 
 // ------------------------------------------------------------- KIVI (LDS)
 // Persistent kernel: every wave loops over blocks (block, kv-head, batch,
@@ -439,108 +407,145 @@ __device__ __forceinline__ float dpp_xor1(float v) {
                                       0xF, true));
 }
 
-template <int ROT>
-__device__ __forceinline__ void sym_block(const QuantLaunch& a, Smem& sm, int b, int h,
-                                          int kind, int blk, int lane) {
-  const int bits = a.tab.bits[h][kind];
-  const int off = 1 << (bits - 1);
-  const float qm = (float)(off - 1);
-  const int t0 = blk * kChunk;
-  const int t = lane >> 1, hb = lane & 1;
-  const uint16_t* src = token_src(a, b, h, kind, t0 + t);
-  // v[j] = x[32 hb + j], v[32 + j] = x[64 + 32 hb + j]
-  float v[64];
+__device__ __forceinline__ float dpp_xor2(float v) {
+  // quad_perm [2,3,0,1]: exchange with lane ^ 2
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x4E, 0xF,
+                                      0xF, true));
+}
+
+// One quarter of token t (channels 32 q .. 32 q + 31) into registers.
+__device__ __forceinline__ void load_quarter(const QuantLaunch& a, int b, int h,
+                                             int kind, int t, int q, u4 raw[4]) {
+  const RQ_GLOBAL u4* s = gptr(reinterpret_cast<const u4*>(
+      token_src(a, b, h, kind, t) + 32 * q));
 #pragma unroll
-  for (int part = 0; part < 2; ++part) {
-    const uint4* s4 = reinterpret_cast<const uint4*>(src + part * 64 + hb * 32);
+  for (int i = 0; i < 4; ++i) raw[i] = s[i];
+}
+
+// Write this block's packed V chunks from the staged code bytes: channel c
+// -> B words over the block's 32 tokens.
+template <int B>
+__device__ __forceinline__ void pack_values_b(const Smem& sm, uint32_t* region_blk,
+                                              int lane) {
+  const uint8_t* cb = reinterpret_cast<const uint8_t*>(sm.codes);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const uint4 w = s4[i];
-      const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        v[part * 32 + 8 * i + 2 * e] = widen(ww[e] & 0xffffu, a.is_bf16);
-        v[part * 32 + 8 * i + 2 * e + 1] = widen(ww[e] >> 16, a.is_bf16);
-      }
-    }
-  }
-  if constexpr (ROT) {
-    // butterflies h = 1..16 inside each 32-channel run
-#pragma unroll
-    for (int hh = 1; hh < 32; hh *= 2) {
-#pragma unroll
-      for (int base = 0; base < 64; base += 2 * hh) {
-#pragma unroll
-        for (int i = 0; i < hh; ++i) {
-          const float x = v[base + i], y = v[base + i + hh];
-          v[base + i] = x + y;
-          v[base + i + hh] = x - y;
-        }
-      }
-    }
-    // h = 32: partner lane holds channel + 32
-#pragma unroll
-    for (int i = 0; i < 64; ++i) {
-      const float o = dpp_xor1(v[i]);
-      v[i] = hb ? (o - v[i]) : (v[i] + o);
-    }
-    // h = 64: v[j] <-> v[32 + j] in this lane
-#pragma unroll
-    for (int i = 0; i < 32; ++i) {
-      const float x = v[i], y = v[32 + i];
-      v[i] = x + y;
-      v[32 + i] = x - y;
-    }
-    const float c = 0.08838834764831845f;  // fp32 nearest to 1/sqrt(128)
-#pragma unroll
-    for (int i = 0; i < 64; ++i) v[i] = v[i] * c;
-  }
-  float amax = 0.0f;
-#pragma unroll
-  for (int i = 0; i < 64; ++i) amax = __builtin_fmaxf(amax, __builtin_fabsf(v[i]));
-  amax = __builtin_fmaxf(amax, dpp_xor1(amax));
-  const uint16_t s16 = f16_sat(amax / qm);
-  const float sf = f16_to_f32(s16);
-  const float inv = (sf != 0.0f) ? 1.0f / sf : 0.0f;
-  uint32_t cw[2][8];
-#pragma unroll
-  for (int part = 0; part < 2; ++part) {
+  for (int rep = 0; rep < 2; ++rep) {
+    const int c = lane + rep * kWave;
+    uint32_t w[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      uint32_t acc = 0;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        float r = v[part * 32 + 4 * i + e] * inv;
-        r = __builtin_fminf(__builtin_fmaxf(r, -qm), qm);
-        acc |= (uint32_t)(rint_i(r) + off) << (8 * e);
-      }
-      cw[part][i] = acc;
+      w[i] = (uint32_t)cb[(4 * i + 0) * kD + c] |
+             ((uint32_t)cb[(4 * i + 1) * kD + c] << 8) |
+             ((uint32_t)cb[(4 * i + 2) * kD + c] << 16) |
+             ((uint32_t)cb[(4 * i + 3) * kD + c] << 24);
     }
-  }
-  if (hb == 0) sm.meta[pair_pos(t)] = s16;
-  uint32_t* region = reinterpret_cast<uint32_t*>(a.codes + a.tab.code_off[h][kind]);
-  if (kind == 0) {
-    // keys: chunks q = hb and 2 + hb of token t straight from registers
-    const size_t tok = (size_t)b * a.cap + t0 + t;
-    pack_store_dyn(bits, cw[0], region + (tok * 4 + hb) * bits);
-    pack_store_dyn(bits, cw[1], region + (tok * 4 + 2 + hb) * bits);
-    __syncthreads();
-  } else {
-    uint32_t* dst = sm.codes + (t * kD) / 4;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      dst[hb * 8 + i] = cw[0][i];
-      dst[16 + hb * 8 + i] = cw[1][i];
-    }
-    __syncthreads();
-    const int nblk_cap = a.cap / kChunk;
-    pack_values_from_smem(sm, bits,
-                          region + ((size_t)b * nblk_cap + blk) * kD * bits,
-                          lane);
+    pack_store<B>(w, region_blk + (size_t)c * B);
   }
 }
 
-template <int ROT>
+// A block in two passes of 16 tokens; the second pass is loaded before the
+// first is computed.  Lane -> token 16 p + lane / 4 and quarter q = lane % 4,
+// which is exactly packed chunk q of the token.  The rotation's butterflies
+// keep their order (stride 1 .. 16 inside the lane, 32 and 64 with the
+// quad's lanes q ^ 1 and q ^ 2, each as one fma with a +-1 factor: the same
+// single rounding of the same exact sum), so every value is the one the
+// definition computes.  A code is rounded by one fp32 add of 2^23 + 2^(B-1)
+// to the clamped quotient: half-to-even on the integer grid, and the even
+// offset keeps the parity of ties, so the low bits hold rint(quotient) +
+// 2^(B-1).
+template <int ROT, int BF16, int B>
+__device__ __forceinline__ void sym_block(const QuantLaunch& a, Smem& sm, int b, int h,
+                                          int kind, int blk, int lane) {
+  constexpr int off = 1 << (B - 1);
+  constexpr float qm = (float)(off - 1);
+  constexpr float magic = 8388608.0f + (float)off;
+  const int t0 = blk * kChunk;
+  const int tq = lane >> 2, q = lane & 3;
+  uint32_t* region = reinterpret_cast<uint32_t*>(a.codes + a.tab.code_off[h][kind]);
+  u4 raw[2][4];
+  load_quarter(a, b, h, kind, t0 + tq, q, raw[0]);
+  load_quarter(a, b, h, kind, t0 + 16 + tq, q, raw[1]);
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    const int t = 16 * p + tq;
+    float v[32];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t ww[4] = {raw[p][i].x, raw[p][i].y, raw[p][i].z, raw[p][i].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[8 * i + 2 * e] = widen_t<BF16>(ww[e] & 0xffffu);
+        v[8 * i + 2 * e + 1] = widen_t<BF16>(ww[e] >> 16);
+      }
+    }
+    if constexpr (ROT) {
+#pragma unroll
+      for (int hh = 1; hh < 32; hh *= 2)
+#pragma unroll
+        for (int i = 0; i < 32; ++i)
+          if ((i & hh) == 0) {
+            const float x = v[i], y = v[i + hh];
+            v[i] = x + y;
+            v[i + hh] = x - y;
+          }
+      // stride 32: lane q ^ 1 holds channel c ^ 32; the lower half (q even)
+      // takes v + o, the upper half o - v
+      const float sg1 = (q & 1) ? -1.0f : 1.0f;
+#pragma unroll
+      for (int i = 0; i < 32; ++i) v[i] = __builtin_fmaf(sg1, v[i], dpp_xor1(v[i]));
+      // stride 64: lane q ^ 2 holds channel c ^ 64
+      const float sg2 = (q & 2) ? -1.0f : 1.0f;
+#pragma unroll
+      for (int i = 0; i < 32; ++i) v[i] = __builtin_fmaf(sg2, v[i], dpp_xor2(v[i]));
+      const float c = 0.08838834764831845f;  // fp32 nearest to 1/sqrt(128)
+#pragma unroll
+      for (int i = 0; i < 32; ++i) v[i] = v[i] * c;
+    }
+    float amax = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 32; ++i) amax = __builtin_fmaxf(amax, __builtin_fabsf(v[i]));
+    amax = __builtin_fmaxf(amax, dpp_xor1(amax));
+    amax = __builtin_fmaxf(amax, dpp_xor2(amax));
+    const uint16_t s16 = f16_sat(amax / qm);
+    const float sf = f16_to_f32(s16);
+    const float inv = (sf != 0.0f) ? 1.0f / sf : 0.0f;
+    if (q == 0) sm.meta[pair_pos(t)] = s16;
+    if (kind == 0) {
+      // keys: this lane's chunk packed from registers
+      ChunkAcc<B> acc;
+      acc.init();
+#pragma unroll
+      for (int i = 0; i < 32; ++i) {
+        const float r = __builtin_amdgcn_fmed3f(v[i] * inv, -qm, qm);
+        acc.add(i, __float_as_uint(r + magic));
+      }
+      acc.finish();
+      const size_t tok = (size_t)b * a.cap + t0 + t;
+      store_chunk<B>(region + (tok * 4 + q) * B, acc.w);
+    } else {
+      // values: code bytes staged as [token][channel] for the transpose
+      uint32_t* dst = sm.codes + (t * kD) / 4 + 8 * q;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        uint32_t cb[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          cb[e] = __float_as_uint(
+              __builtin_amdgcn_fmed3f(v[4 * i + e] * inv, -qm, qm) + magic);
+        dst[i] = __builtin_amdgcn_perm(cb[1], cb[0], 0x0c0c0400u) |
+                 __builtin_amdgcn_perm(cb[3], cb[2], 0x04000c0cu);
+      }
+    }
+  }
+  __syncthreads();
+  if (kind == 1) {
+    const int nblk_cap = a.cap / kChunk;
+    pack_values_b<B>(sm, region + ((size_t)b * nblk_cap + blk) * kD * B, lane);
+  }
+}
+
+template <int ROT, int BF16>
 __global__ void __launch_bounds__(kWave)
 sym_quant_kernel(QuantLaunch a) {
   __shared__ Smem sm;
@@ -548,7 +553,15 @@ sym_quant_kernel(QuantLaunch a) {
   const int h = blockIdx.y;
   const int b = blockIdx.z >> 1, kind = blockIdx.z & 1;
   const int lane = threadIdx.x;
-  sym_block<ROT>(a, sm, b, h, kind, blk, lane);
+  switch (a.tab.bits[h][kind]) {
+    case 2: sym_block<ROT, BF16, 2>(a, sm, b, h, kind, blk, lane); break;
+    case 3: sym_block<ROT, BF16, 3>(a, sm, b, h, kind, blk, lane); break;
+    case 4: sym_block<ROT, BF16, 4>(a, sm, b, h, kind, blk, lane); break;
+    case 5: sym_block<ROT, BF16, 5>(a, sm, b, h, kind, blk, lane); break;
+    case 6: sym_block<ROT, BF16, 6>(a, sm, b, h, kind, blk, lane); break;
+    case 7: sym_block<ROT, BF16, 7>(a, sm, b, h, kind, blk, lane); break;
+    default: sym_block<ROT, BF16, 8>(a, sm, b, h, kind, blk, lane); break;
+  }
   __syncthreads();
   // metadata of this block
   const int nblk_cap = a.cap / kChunk;
@@ -600,10 +613,16 @@ hipError_t launch_quantize(const QuantLaunch& a, hipStream_t s) {
     }
   } else {
     dim3 grid(a.nblk, a.H, a.B * 2);
-    if (a.family == RQ_QUAROT)
-      hipLaunchKernelGGL(sym_quant_kernel<1>, grid, dim3(kWave), 0, s, a);
+    // bit-widths of the symmetric families are 2..8 (checked on the host)
+    const bool rot = a.family == RQ_QUAROT;
+    if (rot && a.is_bf16)
+      hipLaunchKernelGGL((sym_quant_kernel<1, 1>), grid, dim3(kWave), 0, s, a);
+    else if (rot)
+      hipLaunchKernelGGL((sym_quant_kernel<1, 0>), grid, dim3(kWave), 0, s, a);
+    else if (a.is_bf16)
+      hipLaunchKernelGGL((sym_quant_kernel<0, 1>), grid, dim3(kWave), 0, s, a);
     else
-      hipLaunchKernelGGL(sym_quant_kernel<0>, grid, dim3(kWave), 0, s, a);
+      hipLaunchKernelGGL((sym_quant_kernel<0, 0>), grid, dim3(kWave), 0, s, a);
   }
   return hipGetLastError();
 }
