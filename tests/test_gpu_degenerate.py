@@ -1,0 +1,84 @@
+"""GPU parity on the degenerate inputs the quantizers special-case, for every
+family: all-zero tokens and groups (scale or norm 0), constant rows (KIVI's
+min-max range 0), single-channel spikes, and bf16 values beyond the fp16
+range (the fp16 metadata saturates at 65504).  Codes, metadata and the
+window must match the oracle (TurboQuant codes by its near-threshold rule);
+attention is checked where the values stay in the fp16 operand range."""
+import numpy as np
+import pytest
+
+import paper_2605_06675_amd as rq
+import workloads
+from oracle import cache as ocache
+from tests import gpu_helpers as gh
+from tests import test_gpu_parity as gp
+from tests import test_gpu_turbo as gt
+
+pytestmark = pytest.mark.gpu
+
+H, G, T, R, BATCH = 4, 4, 224, 32, 2
+
+
+def _data(seed, scale=1.0):
+    """[B][H][T][128] float32: every 7th token zero, then constant rows,
+    single spikes, whole-zero 32-token blocks for one head, Gaussian rest."""
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((BATCH, H, T, 128))
+    t = np.arange(T)
+    x[:, :, t % 7 == 0] = 0.0
+    x[:, :, t % 7 == 1] = 0.5
+    spike = t % 7 == 2
+    x[:, :, spike] = 0.0
+    x[:, :, spike, 17] = 12.0
+    x[:, 1, 32:64] = 0.0                      # one block all zero (keys: s = 0)
+    x[:, 2, 64:96, :40] = -3.0                # constant channels over a block
+    return x * scale
+
+
+def _fill(family, dtype, bits, kf, vf, rotation=None):
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    ks = [workloads.bits16_from_f32(kf[b], dtype) for b in range(BATCH)]
+    vs = [workloads.bits16_from_f32(vf[b], dtype) for b in range(BATCH)]
+    kvc = rq.KVCache(family, dtype, 1, BATCH, H, H * G, T, R, bits,
+                     rotation=rotation)
+    K, V = gh.dev(np.stack(ks), dtype), gh.dev(np.stack(vs), dtype)
+    kvc.append(0, K[:, :, :150].contiguous(), V[:, :, :150].contiguous())
+    kvc.append(0, K[:, :, 150:].contiguous(), V[:, :, 150:].contiguous())
+    torch.cuda.synchronize()
+    return kvc, ks, vs
+
+
+@pytest.mark.parametrize("family,bits", [
+    (workloads.KIVI, [[1, 4], [2, 3], [3, 2], [8, 1]]),
+    (workloads.QUAROT, [[2, 4], [3, 3], [4, 2], [8, 5]]),
+    (workloads.RTN, [[2, 4], [3, 3], [4, 2], [8, 5]])],
+    ids=["kivi", "quarot", "rtn"])
+@pytest.mark.parametrize("dtype", [workloads.F16, workloads.BF16])
+def test_degenerate_affine_families(family, bits, dtype):
+    print(f"degenerate family {family} dtype {dtype}", flush=True)
+    bits = np.array([bits])
+    kvc, ks, vs = _fill(family, dtype, bits, _data(1), _data(2))
+    units = gp._check_cache(family, dtype, kvc, ks, vs, bits, R, BATCH, H, T)
+    gp._check_attention(kvc, units, dtype, BATCH, H, G)
+
+
+@pytest.mark.parametrize("family", [workloads.KIVI, workloads.QUAROT,
+                                    workloads.RTN], ids=["kivi", "quarot", "rtn"])
+def test_saturated_metadata_bf16(family):
+    # |x| up to ~1e7: scales and zero points saturate at the fp16 maximum
+    print(f"saturated metadata family {family}", flush=True)
+    bits = np.array([[[2, 3], [3, 2], [4, 4], [5, 6]]])
+    kvc, ks, vs = _fill(family, workloads.BF16, bits, _data(3, 2.0e5), _data(4, 2.0e5))
+    gp._check_cache(family, workloads.BF16, kvc, ks, vs, bits, R, BATCH, H, T)
+
+
+def test_degenerate_turbo():
+    print("degenerate turbo", flush=True)
+    dtype = workloads.BF16
+    bits = np.array([[[1, 4], [2, 3], [3, 2], [4, 4]]])
+    r16, rf = gt._rotations(1, H)
+    kvc, ks, vs = _fill(workloads.TURBO, dtype, bits, _data(5), _data(6),
+                        rotation=gh.dev(r16, workloads.BF16))
+    units = gt._check(dtype, kvc, ks, vs, rf[0], bits, R, BATCH, H)
+    gt._attention(kvc, units, dtype, BATCH, H, G)
