@@ -35,6 +35,18 @@ def test_version_and_error_text():
 
 
 @pytest.mark.parametrize("seed", workloads.SEEDS)
+def test_fit_recovers_planted_curves(seed):
+    # the single-layer workload's calibration: b = 1..4, beta ~ U(3.6, 5.3)
+    bits = [1, 2, 3, 4]
+    D, alpha, beta = workloads.planted_curves(16, bits, seed=seed)
+    assert np.all((beta > 3.6) & (beta < 5.3))
+    a, b, r2 = rq.rq_fit_distortion(D, bits)
+    np.testing.assert_allclose(a, alpha, rtol=1e-12)
+    np.testing.assert_allclose(b, beta, rtol=1e-12)
+    np.testing.assert_allclose(r2, 1.0, atol=1e-12)
+
+
+@pytest.mark.parametrize("seed", workloads.SEEDS)
 def test_fit_matches_oracle(seed):
     bits = [2, 3, 4, 5, 6]
     D, _, _ = workloads.planted_curves(300, bits, seed=seed, noise_sigma=0.05)
