@@ -13,6 +13,7 @@ hipError_t launch_attn_kivi_n4_b8(const AttnLaunch&, size_t, hipStream_t);
 hipError_t launch_attn_quarot_b4(const AttnLaunch&, size_t, hipStream_t);
 hipError_t launch_attn_quarot_b8(const AttnLaunch&, size_t, hipStream_t);
 hipError_t launch_attn_turbo_b4(const AttnLaunch&, size_t, hipStream_t);
+hipError_t launch_attn_turbo_b8(const AttnLaunch&, size_t, hipStream_t);
 
 size_t attention_area_bytes(int G, int wave_bytes, int family) {
   const size_t merge = (size_t)kWaves * G * (2 + kD) * sizeof(float);
@@ -29,7 +30,9 @@ size_t attention_area_bytes(int G, int wave_bytes, int family) {
 }
 
 size_t attention_tail_bytes(int G, int family) {
-  return (size_t)G * kD * sizeof(uint16_t) + (family == RQ_TURBO ? (size_t)G * kD * sizeof(float) : 0);
+  // TurboQuant: the rotated query rows and two fp16 centroid tables
+  return (size_t)G * kD * sizeof(uint16_t) +
+         (family == RQ_TURBO ? (size_t)G * kD * sizeof(float) + 2 * 256 * sizeof(uint16_t) : 0);
 }
 
 size_t attention_lds_bytes(int G, int wave_bytes, int family) {
@@ -44,7 +47,7 @@ hipError_t launch_attention(const AttnLaunch& a, hipStream_t s) {
   const bool wide = maxb > 4;
   hipError_t e;
   if (a.family == RQ_TURBO)
-    e = wide ? hipErrorInvalidValue : launch_attn_turbo_b4(a, lds, s);
+    e = (wide ? launch_attn_turbo_b8 : launch_attn_turbo_b4)(a, lds, s);
   else if (a.family == RQ_QUAROT || a.family == RQ_RTN)   // same kernel, no rotation
     e = (wide ? launch_attn_quarot_b8 : launch_attn_quarot_b4)(a, lds, s);
   else if (a.GP <= 4)

@@ -13,31 +13,39 @@
 // into the wave's LDS slot, from where each lane reads its MFMA operands.
 //
 // Per block (32 tokens) a wave runs QK^T and PV on v_mfma_f32_16x16x32_f16.
-// The VALU only turns packed fields into fp16 operands, and it does so in
-// one v_and_or_b32 per pair of codes: a field sitting at mantissa bit P of
-// the fp16 pattern 1024 (0x6400) reads as 1024 + u * 2^P.  The weight 2^P is
-// divided out of the other operand (the query for keys, the probability for
-// values) and the 1024 offset, the zero points and the symmetric offsets are
-// removed by a few more MFMAs against constant operands, so no per-element
-// subtraction or FMA is needed:
-//   KIVI keys    S = sum_c (q_c s_c 2^-P)(1024 + u 2^P)
-//                    + sum_c z_c q_c - 1024 sum_c (q_c s_c 2^-P)
-//   KIVI values  O = sum_t (p_t s_t 2^-P)(1024 + u 2^P)
-//                    + sum_t p_t z_t - 1024 sum_t (p_t s_t 2^-P)
-//   QuaRot       the same with per-token scales and codes u - 2^(b-1).
+// The VALU only turns packed fields into fp16 operands: a b-bit field masked
+// into mantissa bit P of a half-word whose exponent field is zero is the
+// exact subnormal u * 2^(P-24) (the matrix cores keep subnormal operands),
+// so one AND turns a pair of codes into a pair of operands.  The weight
+// 2^(P-24) is divided out of the other operand (the query for keys, the
+// probability for values) or out of the fp32 result:
+//   KIVI keys    S = 2^24 sum_c (q_c s_c 2^-P) (u 2^(P-24)) + sum_c z_c q_c
+//   KIVI values  O = 2^24 sum_t (p_t s_t 2^-P) (u 2^(P-24)) + sum_t p_t z_t
+//   QuaRot       per-token scales and codes u - 2^(b-1): the offset enters as
+//                the accumulator's start value (keys) or one more MFMA
+//                against constants (values).
 //   RTN          QuaRot's path with no rotation of the query or the output.
 //   TurboQuant   codes index the Lloyd-Max centroids, which are not affine
 //                in the code: each pair of codes is looked up in a table of
 //                fp16 centroids held in two to four registers (v_perm_b32,
-//                using the symmetry of the codebook for b >= 3), and the
-//                per-token norm scales the scores and probabilities.  The
-//                query is rotated by R on entry; the merge rotates the
-//                quantized part of the output back by R^T.
+//                using the symmetry of the codebook for b >= 3) or, above 4
+//                bits, in LDS; the per-token norm scales the scores and
+//                probabilities.  The query is rotated by R on entry; the
+//                merge rotates the quantized part of the output back by R^T.
 // With G query heads per kv-head the sixteen MFMA columns carry the G
 // queries 16/G times over; the KIVI value side uses the spare rows for the
 // four 32-channel groups of a token, so one A operand serves all of them.
 // Softmax runs in the log2 domain with a lazily moved maximum (it moves
 // only when a block exceeds it by 2^4), so probabilities stay <= 16.
+//
+// Range of the fp16 operands.  Each query row is scaled by a power of two
+// 2^-e so that its largest element lies in [1/2, 1); the scores are scaled
+// back in fp32.  With |q 2^-e| < 1 and every scale below 65504, a key
+// operand q s 2^-(P+e) stays finite.  On the value side a probability
+// (<= 16) times a scale (<= 65504) can exceed the fp16 range, so each wave
+// keeps a power-of-two exponent Ev (0 .. 4) by which the value operands are
+// divided: it grows, like the running maximum, only when a block holds a
+// scale above 4094 * 2^Ev, and the wave's value sums are rescaled then.
 //
 
 #pragma once
@@ -53,10 +61,12 @@ constexpr int kWave = 64;
 constexpr int kWaves = kAttnWaves;
 constexpr int kThreads = kWave * kWaves;
 constexpr float kInvSqrtD = 0.08838834764831845f;
-constexpr uint32_t kMagic = 0x64006400u;   // fp16 pair (1024, 1024)
-constexpr uint32_t kNeg1024 = 0xE400E400u; // fp16 pair (-1024, -1024)
 constexpr uint32_t kOnes = 0x3C003C00u;    // fp16 pair (1, 1)
 constexpr float kLazy = 4.0f;              // log2 headroom of the running max
+// Largest value-side scale (fp16 bits) that keeps 16 * scale * 2^-Ev below
+// the fp16 maximum at Ev = 0: 4094 (16 * 4094 = 65504).
+constexpr uint32_t kVScaleMax = 0x6BFFu;
+constexpr int kMaxEv = 4;                  // 65504 / 2^4 <= 4094
 
 // Streaming slots per merge group (two-level merge above this).
 constexpr int kGroup = kAttnGroup;
@@ -182,11 +192,6 @@ __device__ __forceinline__ void scale_inplace(f4& v, int i, float s) {
   v[i] = x;
 }
 
-// (x & mask) | c: with c opaque (the magic pattern) this is one
-// v_and_or_b32, the mask in an SGPR
-__device__ __forceinline__ uint32_t and_or(uint32_t x, uint32_t mask, uint32_t c) {
-  return (x & mask) | c;
-}
 // insert the bits of x under mask into c (one v_bfi_b32; used for the
 // lower planes of a code, whose bits are still zero in c)
 __device__ __forceinline__ uint32_t insert(uint32_t x, uint32_t mask, uint32_t c) {
@@ -207,13 +212,14 @@ __device__ __forceinline__ uint32_t pk_mul(uint32_t a, uint32_t b) {
   return as_u32(as_h2(a) * as_h2(b));
 }
 
-// fp16 pair (1024 + u_i 2^P, 1024 + u_{i+16} 2^P) of key pair i of a chunk
-// (its B words), P = kpos(B, i).
+// fp16 pair (u_i 2^(P-24), u_{i+16} 2^(P-24)) of key pair i of a chunk (its
+// B words), P = kpos(B, i): the fields masked into the mantissa of a zero
+// exponent, exact subnormals.
 template <int B>
-__device__ __forceinline__ uint32_t kpair(const uint32_t* wds, int i, uint32_t magic) {
+__device__ __forceinline__ uint32_t kpair(const uint32_t* wds, int i) {
   constexpr int w0 = plane_w(B, 0);
   const int P = kpos(B, i);
-  uint32_t acc = and_or(wds[i / (16 / w0)] >> kshift(B, i), pair_mask(w0) << P, magic);
+  uint32_t acc = (wds[i / (16 / w0)] >> kshift(B, i)) & (pair_mask(w0) << P);
 #pragma unroll
   for (int p = 1; p < plane_n(B); ++p) {
     const int w = plane_w(B, p), per = 16 / w, off = plane_off(B, p);
@@ -223,24 +229,23 @@ __device__ __forceinline__ uint32_t kpair(const uint32_t* wds, int i, uint32_t m
   return acc;
 }
 
-// fp16 pairs (1024 + u 2^P) of value slots i = 0..3 (codes 4r+i, 16+4r+i)
-// of one channel's chunk (its B words in LDS), P = vpos(B, i).
+// fp16 pairs (u 2^(P-24)) of value slots i = 0..3 (codes 4r+i, 16+4r+i) of
+// one channel's chunk (its B words in LDS), P = vpos(B, i).
 template <int B>
-__device__ __forceinline__ void vpairs(const uint32_t* ch, int r, uint32_t magic,
-                                       uint32_t out[4]) {
+__device__ __forceinline__ void vpairs(const uint32_t* ch, int r, uint32_t out[4]) {
   constexpr int w0 = plane_w(B, 0);
   if constexpr (w0 == 8) {
     const uint32_t x = ch[2 * r], y = ch[2 * r + 1];
-    out[0] = and_or(x, pair_mask(8), magic);
-    out[1] = and_or(x >> 8, pair_mask(8), magic);
-    out[2] = and_or(y, pair_mask(8), magic);
-    out[3] = and_or(y >> 8, pair_mask(8), magic);
+    out[0] = x & pair_mask(8);
+    out[1] = (x >> 8) & pair_mask(8);
+    out[2] = y & pair_mask(8);
+    out[3] = (y >> 8) & pair_mask(8);
   } else {
     constexpr int per = 16 / w0;
     const uint32_t x = ch[(4 * r) / per] >> (((4 * r) % per) * w0);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      out[i] = and_or(x >> vshift(B, i), pair_mask(w0) << vpos(B, i), magic);
+      out[i] = (x >> vshift(B, i)) & (pair_mask(w0) << vpos(B, i));
 #pragma unroll
     for (int p = 1; p < plane_n(B); ++p) {
       const int w = plane_w(B, p), pp = 16 / w, off = plane_off(B, p);
@@ -312,28 +317,67 @@ __device__ __forceinline__ void tq_make_lut(const float* cb, int b, uint32_t lut
   }
 }
 
+// Codes (i, i + 16) of a chunk times two, at bits 1 and 17: the byte offsets
+// of their entries in an fp16 table (widths 5..8).
+template <int B>
+__device__ __forceinline__ uint32_t tq_code2_pair(const uint32_t* wds, int i) {
+  uint32_t f = 0;
+#pragma unroll
+  for (int p = 0; p < plane_n(B); ++p) {
+    const int w = plane_w(B, p), per = 16 / w, off = plane_off(B, p);
+    f |= shr_signed(wds[off + i / per], (i % per) * w - off - 1) & (pair_mask(w) << (off + 1));
+  }
+  return f;
+}
+
+typedef __attribute__((address_space(3))) const _Float16 lds_h;
+
+// fp16 centroid pair of a doubled code pair f from an LDS table of 2^b fp16
+// centroids (widths 5..8; two 16-bit LDS reads straight into the halves)
+__device__ __forceinline__ uint32_t tq_lds(uint32_t f, lds_h* tab) {
+  typedef __attribute__((address_space(3))) const uint8_t lds_b;
+  h2 v;
+  v.x = *(lds_h*)((lds_b*)tab + (f & 0xffffu));
+  v.y = *(lds_h*)((lds_b*)tab + (f >> 16));
+  return as_u32(v);
+}
+
+// fp16 centroid pair of codes (i, i+16) of a chunk of width B
+template <int B>
+__device__ __forceinline__ uint32_t tq_pair(const uint32_t* wds, int i, const uint32_t* lut,
+                                            lds_h* tab) {
+  if constexpr (B <= 4) return tq_lut<B>(tq_code_pair<B>(wds, i), lut);
+  else return tq_lds(tq_code2_pair<B>(wds, i), tab);
+}
+
 // ------------------------------------------------------------ wave state
 template <int NA>
 struct WaveState {
-  f4 acc[8];        // PV accumulators, channel tiles 16nt..16nt+15
-  f4 corrA[NA];     // -1024 (and symmetric-offset) corrections per A operand
+  f4 acc[8];        // PV accumulators, channel tiles 16nt..16nt+15, scaled by
+                    // 2^-(24+Ev) (codes as subnormals) or 2^-Ev (TurboQuant)
+  f4 corrO;         // QuaRot/RTN: sum_t p s 2^-Ev (the symmetric offset term)
   f4 corrZ;         // KIVI: sum_t p z_{t,g} in column g, sum_t p in column 4;
-                    // QuaRot: sum_t p in every column
+                    // others: sum_t p in every column
   float m_run;      // running max of this lane's query (log2 domain)
+  int ev;           // value-side exponent Ev (the same in every lane)
+  uint32_t wv[4];   // fp16 pair 2^-(vpos(i) + Ev) of value slot i
+                    // (TurboQuant: 2^-Ev)
 };
 
 // Static per-lane operands built once per workgroup.
 struct LaneOps {
-  uint32_t qh[16];  // QK B operand: fp16 (q * 2^-kpos) per k-slot pair
-  uint32_t qz[16];  // KIVI: fp16 q per k-slot pair (zero-point term)
-  uint32_t wv[4];   // fp16 pair 2^-vpos of value slot i
-  uint32_t vq[4];   // QuaRot: fp16 pair -(1024 + 2^(b-1) 2^vpos) of slot i
-  f4 corrK;         // QuaRot: -sum_c qh (1024 + off 2^kpos) (same in all rows)
-  uint32_t magic;   // kMagic, kept in a VGPR so that "(x & m) | magic" is one
-                    // v_and_or_b32 with the mask in an SGPR (VOP3 takes no
-                    // literal operand on this target)
+  uint32_t qh[16];  // QK B operand: fp16 q' 2^-(kpos + e) per k-slot pair
+                    // (TurboQuant: q' 2^-e), q' the scaled (rotated) query
+  uint32_t qz[16];  // KIVI: fp16 q' 2^-e per k-slot pair (zero-point term)
+  uint32_t vq[4];   // QuaRot/RTN: fp16 pair 2^vpos(i) of value slot i
+  f4 corrK;         // QuaRot/RTN: -2^(b-1) sum_c 2^(kpos-24) qh (start value
+                    // of the score accumulators; the same in all rows)
+  float cK;         // 2^(24+e) (codes as subnormals) or 2^e (TurboQuant)
+  float eK;         // KIVI: 2^e (the zero-point sum)
   uint32_t lutk[4]; // TurboQuant: fp16 centroid tables of the K and V widths
-  uint32_t lutv[4];
+  uint32_t lutv[4]; //   (widths <= 4)
+  lds_h* tabk;      // TurboQuant: fp16 centroids of the K and V widths in LDS
+  lds_h* tabv;      //   (widths >= 5)
   int r, col, lane;
   int gsub;         // col / GP
   int GP;           // queries per replica (power of two >= G)
@@ -346,88 +390,123 @@ struct SlotPtrs {
   const u4* vm;        // V metadata
 };
 
-// K side of one block: S0 (tokens 4r+i), S1 (tokens 16+4r+i) relative to
-// m_ref, for this lane's query.  A operands: tile t (tokens 16t..16t+15,
-// row = col), k-slot pairs (kb, k') of chunk r, unpacked per K-step.
+// K side of one block: t0 (tokens 4r+i), t1 (tokens 16+4r+i), the log2
+// scores of this lane's query relative to m_ref.  A operands: tile t
+// (tokens 16t..16t+15, row = col), k-slot pairs (kb, k') of chunk r,
+// unpacked per K-step.
 template <int FAM, int BK>
 __device__ __forceinline__ void kpart(const SlotPtrs& sp, const LaneOps& lo, float m_ref,
-                                      f4& S0, f4& S1) {
+                                      f4& t0, f4& t1) {
   const int r = lo.r;
   uint32_t kw[2][BK];
 #pragma unroll
   for (int tile = 0; tile < 2; ++tile)
 #pragma unroll
     for (int i = 0; i < BK; ++i) kw[tile][i] = sp.kc[((16 * tile + lo.col) * 4 + r) * BK + i];
-  uint32_t Bq[16];
-  f4 X;
+  f4 S0, S1;
   if constexpr (FAM == RQ_KIVI) {
-    // per-channel scales folded into the query; zero points and the 1024
-    // offset enter through the X chain
-    const h8 neg = make_h8(kNeg1024, kNeg1024, kNeg1024, kNeg1024);
-    X = (f4){-m_ref, -m_ref, -m_ref, -m_ref};
+    // per-channel scales folded into the query; the zero points enter
+    // through their own chain X = sum_c z_c q'_c 2^-e, the same in all rows
+    f4 X = {0.f, 0.f, 0.f, 0.f};
+    S0 = X;
+    S1 = X;
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       const u4 s4 = sp.km[r * 8 + kb], z4 = sp.km[r * 8 + 4 + kb];
-      Bq[4 * kb + 0] = pk_mul(lo.qh[4 * kb + 0], s4.x);
-      Bq[4 * kb + 1] = pk_mul(lo.qh[4 * kb + 1], s4.y);
-      Bq[4 * kb + 2] = pk_mul(lo.qh[4 * kb + 2], s4.z);
-      Bq[4 * kb + 3] = pk_mul(lo.qh[4 * kb + 3], s4.w);
+      const h8 Bk = make_h8(pk_mul(lo.qh[4 * kb + 0], s4.x), pk_mul(lo.qh[4 * kb + 1], s4.y),
+                            pk_mul(lo.qh[4 * kb + 2], s4.z), pk_mul(lo.qh[4 * kb + 3], s4.w));
       X = mfma(u4_h8(z4), make_h8(lo.qz[4 * kb], lo.qz[4 * kb + 1], lo.qz[4 * kb + 2],
                                   lo.qz[4 * kb + 3]), X);
-    }
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
-      X = mfma(neg, make_h8(Bq[4 * kb], Bq[4 * kb + 1], Bq[4 * kb + 2], Bq[4 * kb + 3]), X);
-  } else {
-#pragma unroll
-    for (int i = 0; i < 16; ++i) Bq[i] = lo.qh[i];
-    X = lo.corrK;
-  }
-  // KIVI: the score chains start from zero and take the (block-constant)
-  // X chain at the end, so the two run side by side on the matrix cores
-  S0 = FAM == RQ_KIVI ? (f4){0.f, 0.f, 0.f, 0.f} : X;
-  S1 = S0;
-#pragma unroll
-  for (int kb = 0; kb < 4; ++kb) {
-    const h8 Bk = make_h8(Bq[4 * kb], Bq[4 * kb + 1], Bq[4 * kb + 2], Bq[4 * kb + 3]);
-    if constexpr (FAM == RQ_TURBO) {
-      S0 = mfma(make_h8(tq_lut<BK>(tq_code_pair<BK>(kw[0], 4 * kb), lo.lutk),
-                        tq_lut<BK>(tq_code_pair<BK>(kw[0], 4 * kb + 1), lo.lutk),
-                        tq_lut<BK>(tq_code_pair<BK>(kw[0], 4 * kb + 2), lo.lutk),
-                        tq_lut<BK>(tq_code_pair<BK>(kw[0], 4 * kb + 3), lo.lutk)),
+      S0 = mfma(make_h8(kpair<BK>(kw[0], 4 * kb), kpair<BK>(kw[0], 4 * kb + 1),
+                        kpair<BK>(kw[0], 4 * kb + 2), kpair<BK>(kw[0], 4 * kb + 3)),
                 Bk, S0);
-      S1 = mfma(make_h8(tq_lut<BK>(tq_code_pair<BK>(kw[1], 4 * kb), lo.lutk),
-                        tq_lut<BK>(tq_code_pair<BK>(kw[1], 4 * kb + 1), lo.lutk),
-                        tq_lut<BK>(tq_code_pair<BK>(kw[1], 4 * kb + 2), lo.lutk),
-                        tq_lut<BK>(tq_code_pair<BK>(kw[1], 4 * kb + 3), lo.lutk)),
-                Bk, S1);
-    } else {
-      S0 = mfma(make_h8(kpair<BK>(kw[0], 4 * kb, lo.magic), kpair<BK>(kw[0], 4 * kb + 1, lo.magic),
-                        kpair<BK>(kw[0], 4 * kb + 2, lo.magic), kpair<BK>(kw[0], 4 * kb + 3, lo.magic)),
-                Bk, S0);
-      S1 = mfma(make_h8(kpair<BK>(kw[1], 4 * kb, lo.magic), kpair<BK>(kw[1], 4 * kb + 1, lo.magic),
-                        kpair<BK>(kw[1], 4 * kb + 2, lo.magic), kpair<BK>(kw[1], 4 * kb + 3, lo.magic)),
+      S1 = mfma(make_h8(kpair<BK>(kw[1], 4 * kb), kpair<BK>(kw[1], 4 * kb + 1),
+                        kpair<BK>(kw[1], 4 * kb + 2), kpair<BK>(kw[1], 4 * kb + 3)),
                 Bk, S1);
     }
-  }
-  if constexpr (FAM == RQ_KIVI) {
+    const float xx = __builtin_fmaf(X[0], lo.eK, -m_ref);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      S0[i] += X[i];
-      S1[i] += X[i];
+      t0[i] = __builtin_fmaf(S0[i], lo.cK, xx);
+      t1[i] = __builtin_fmaf(S1[i], lo.cK, xx);
     }
   } else {
-    // per-token scales: dword 4r+i of the pair-ordered scales holds tokens
-    // (4r+i, 16+4r+i)
+    S0 = FAM == RQ_TURBO ? (f4){0.f, 0.f, 0.f, 0.f} : lo.corrK;
+    S1 = S0;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      const h8 Bk = make_h8(lo.qh[4 * kb], lo.qh[4 * kb + 1], lo.qh[4 * kb + 2],
+                            lo.qh[4 * kb + 3]);
+      if constexpr (FAM == RQ_TURBO) {
+        S0 = mfma(make_h8(tq_pair<BK>(kw[0], 4 * kb, lo.lutk, lo.tabk),
+                          tq_pair<BK>(kw[0], 4 * kb + 1, lo.lutk, lo.tabk),
+                          tq_pair<BK>(kw[0], 4 * kb + 2, lo.lutk, lo.tabk),
+                          tq_pair<BK>(kw[0], 4 * kb + 3, lo.lutk, lo.tabk)),
+                  Bk, S0);
+        S1 = mfma(make_h8(tq_pair<BK>(kw[1], 4 * kb, lo.lutk, lo.tabk),
+                          tq_pair<BK>(kw[1], 4 * kb + 1, lo.lutk, lo.tabk),
+                          tq_pair<BK>(kw[1], 4 * kb + 2, lo.lutk, lo.tabk),
+                          tq_pair<BK>(kw[1], 4 * kb + 3, lo.lutk, lo.tabk)),
+                  Bk, S1);
+      } else {
+        S0 = mfma(make_h8(kpair<BK>(kw[0], 4 * kb), kpair<BK>(kw[0], 4 * kb + 1),
+                          kpair<BK>(kw[0], 4 * kb + 2), kpair<BK>(kw[0], 4 * kb + 3)),
+                  Bk, S0);
+        S1 = mfma(make_h8(kpair<BK>(kw[1], 4 * kb), kpair<BK>(kw[1], 4 * kb + 1),
+                          kpair<BK>(kw[1], 4 * kb + 2), kpair<BK>(kw[1], 4 * kb + 3)),
+                  Bk, S1);
+      }
+    }
+    // per-token scales (TurboQuant: norms): dword 4r+i of the pair-ordered
+    // scales holds tokens (4r+i, 16+4r+i)
     const u4 sv = sp.km[r];
     const uint32_t ss[4] = {sv.x, sv.y, sv.z, sv.w};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const h2 sc = as_h2(ss[i]);
-      S0[i] = __builtin_fmaf(S0[i], (float)sc.x, -m_ref);
-      S1[i] = __builtin_fmaf(S1[i], (float)sc.y, -m_ref);
+      t0[i] = __builtin_fmaf(S0[i] * lo.cK, (float)sc.x, -m_ref);
+      t1[i] = __builtin_fmaf(S1[i] * lo.cK, (float)sc.y, -m_ref);
     }
   }
+}
+
+// The value-side scales this lane multiplies into its A operands (KIVI: the
+// groups of its A operands; others: the per-token scales or norms), as
+// fp16 pairs.
+template <int FAM, int NA>
+struct VScales {
+  u4 s[FAM == RQ_KIVI ? NA : 1];
+};
+
+template <int FAM, int NA>
+__device__ __forceinline__ VScales<FAM, NA> load_vscales(const SlotPtrs& sp, const LaneOps& lo) {
+  VScales<FAM, NA> v;
+  if constexpr (FAM == RQ_KIVI) {
+    constexpr int GPA = 4 / NA;   // value groups per A operand
+#pragma unroll
+    for (int a = 0; a < NA; ++a) v.s[a] = sp.vm[(a * GPA + lo.gsub % GPA) * 8 + lo.r];
+  } else {
+    v.s[0] = sp.vm[lo.r];
+  }
+  return v;
+}
+
+typedef uint16_t us2 __attribute__((ext_vector_type(2)));
+
+// Largest of the lane's value-side scales as an fp16 pair (both halves are
+// candidates; the scales are >= 0, so their bit patterns order like them).
+template <int FAM, int NA>
+__device__ __forceinline__ us2 vscale_max(const VScales<FAM, NA>& v) {
+  constexpr int n = FAM == RQ_KIVI ? NA : 1;
+  us2 m = __builtin_bit_cast(us2, v.s[0].x);
+#pragma unroll
+  for (int a = 0; a < n; ++a) {
+    if (a > 0) m = __builtin_elementwise_max(m, __builtin_bit_cast(us2, v.s[a].x));
+    m = __builtin_elementwise_max(m, __builtin_bit_cast(us2, v.s[a].y));
+    m = __builtin_elementwise_max(m, __builtin_bit_cast(us2, v.s[a].z));
+    m = __builtin_elementwise_max(m, __builtin_bit_cast(us2, v.s[a].w));
+  }
+  return m;
 }
 
 // V side of one block: probabilities P (fp16 pairs of tokens 4r+i and
@@ -435,37 +514,21 @@ __device__ __forceinline__ void kpart(const SlotPtrs& sp, const LaneOps& lo, flo
 // tile nt (channels 16nt..16nt+15, column = col), token slots of quarter r.
 template <int FAM, int NA, int BV>
 __device__ __forceinline__ void vpart(const SlotPtrs& sp, const LaneOps& lo,
-                                      const uint32_t (&P)[4], const uint32_t* cst,
-                                      WaveState<NA>& ws) {
+                                      const uint32_t (&P)[4], const VScales<FAM, NA>& vs,
+                                      const uint32_t* cst, WaveState<NA>& ws) {
   constexpr int GPA = 4 / NA;   // value groups per A operand (KIVI)
   const int r = lo.r, col = lo.col;
   uint32_t P2[4];
-  if constexpr (FAM == RQ_TURBO) {
-    // the centroid scale n / sqrt(128): 1/sqrt(128) here, n below
-    const h2 c = {(_Float16)kInvSqrtD, (_Float16)kInvSqrtD};
 #pragma unroll
-    for (int i = 0; i < 4; ++i) P2[i] = pk_mul(P[i], as_u32(c));
-  } else {
+  for (int i = 0; i < 4; ++i) P2[i] = pk_mul(P[i], ws.wv[FAM == RQ_TURBO ? 0 : i]);
+  constexpr int nA = FAM == RQ_KIVI ? NA : 1;
+  uint32_t A[nA][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) P2[i] = pk_mul(P[i], h_pair(h_pow2_neg(vpos(BV, i))));
-  }
-  uint32_t A[NA][4];
-  if constexpr (FAM == RQ_KIVI) {
-#pragma unroll
-    for (int a = 0; a < NA; ++a) {
-      const int g = a * GPA + lo.gsub % GPA;
-      const u4 s4 = sp.vm[g * 8 + r];
-      A[a][0] = pk_mul(P2[0], s4.x);
-      A[a][1] = pk_mul(P2[1], s4.y);
-      A[a][2] = pk_mul(P2[2], s4.z);
-      A[a][3] = pk_mul(P2[3], s4.w);
-    }
-  } else {
-    const u4 s4 = sp.vm[r];
-    A[0][0] = pk_mul(P2[0], s4.x);
-    A[0][1] = pk_mul(P2[1], s4.y);
-    A[0][2] = pk_mul(P2[2], s4.z);
-    A[0][3] = pk_mul(P2[3], s4.w);
+  for (int a = 0; a < nA; ++a) {
+    A[a][0] = pk_mul(P2[0], vs.s[a].x);
+    A[a][1] = pk_mul(P2[1], vs.s[a].y);
+    A[a][2] = pk_mul(P2[2], vs.s[a].z);
+    A[a][3] = pk_mul(P2[3], vs.s[a].w);
   }
 #pragma unroll
   for (int nt = 0; nt < 8; ++nt) {
@@ -474,39 +537,81 @@ __device__ __forceinline__ void vpart(const SlotPtrs& sp, const LaneOps& lo,
     if constexpr (FAM == RQ_TURBO) {
       const uint32_t* ch = sp.vc + (16 * nt + col) * BV;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) pr[i] = tq_lut<BV>(tq_code_pair<BV>(ch, 4 * r + i), lo.lutv);
+      for (int i = 0; i < 4; ++i) pr[i] = tq_pair<BV>(ch, 4 * r + i, lo.lutv, lo.tabv);
     } else {
-      vpairs<BV>(sp.vc + (16 * nt + col) * BV, r, lo.magic, pr);
+      vpairs<BV>(sp.vc + (16 * nt + col) * BV, r, pr);
     }
     ws.acc[nt] = mfma(make_h8(A[a][0], A[a][1], A[a][2], A[a][3]),
                       make_h8(pr[0], pr[1], pr[2], pr[3]), ws.acc[nt]);
   }
   const h8 Ph = make_h8(P[0], P[1], P[2], P[3]);
   if constexpr (FAM == RQ_KIVI) {
-    const h8 neg = make_h8(kNeg1024, kNeg1024, kNeg1024, kNeg1024);
-#pragma unroll
-    for (int a = 0; a < NA; ++a)
-      ws.corrA[a] = mfma(make_h8(A[a][0], A[a][1], A[a][2], A[a][3]), neg, ws.corrA[a]);
     // column g < 4: zero points of group g; column 4: ones; others: zeros
     const u4 bz = (col < 4) ? sp.vm[col * 8 + 4 + r]
                             : reinterpret_cast<const u4*>(cst)[col == 4 ? 0 : 1];
     ws.corrZ = mfma(Ph, u4_h8(bz), ws.corrZ);
-  } else if constexpr (FAM == RQ_TURBO) {
-    ws.corrZ = mfma(Ph, make_h8(kOnes, kOnes, kOnes, kOnes), ws.corrZ);
   } else {
-    uint32_t c[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      // -(1024 + 2^(b-1) 2^vpos) of slot i, exact in fp16
-      const _Float16 v = (_Float16)(-(1024.0f + (float)(1 << (BV - 1)) *
-                                                    (float)(1 << vpos(BV, i))));
-      const h2 vv = {v, v};
-      c[i] = as_u32(vv);
-    }
-    ws.corrA[0] = mfma(make_h8(A[0][0], A[0][1], A[0][2], A[0][3]),
-                       make_h8(c[0], c[1], c[2], c[3]), ws.corrA[0]);
+    if constexpr (FAM != RQ_TURBO)
+      ws.corrO = mfma(make_h8(A[0][0], A[0][1], A[0][2], A[0][3]),
+                      make_h8(lo.vq[0], lo.vq[1], lo.vq[2], lo.vq[3]), ws.corrO);
     ws.corrZ = mfma(Ph, make_h8(kOnes, kOnes, kOnes, kOnes), ws.corrZ);
   }
+}
+
+// fp16 pairs 2^-(vpos(i) + ev) of the value slots (TurboQuant: 2^-ev)
+template <int FAM, int BV>
+__device__ __forceinline__ void set_wv(int ev, uint32_t wv[4]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int e = (FAM == RQ_TURBO ? 0 : vpos(BV, i)) + ev;
+    wv[i] = h_pair((uint32_t)(15 - e) << 10);
+  }
+}
+
+// The rarely taken part of a block: move the running maximum of the lane's
+// query to the block's, and/or raise the value exponent Ev until every
+// value-side scale of the block is at most 4094 * 2^Ev; rescale the wave's
+// sums accordingly.
+template <int FAM, int NA, int BV>
+__device__ __forceinline__ void block_rescale(const LaneOps& lo, float m_ref, float mx,
+                                              us2 smax, f4& t0, f4& t1, WaveState<NA>& ws) {
+  mx = __builtin_fmaxf(mx, xor_shfl(mx, 16));
+  mx = __builtin_fmaxf(mx, xor_shfl(mx, 32));
+  const float mnew = __builtin_fmaxf(ws.m_run, m_ref + mx);
+  const float alpha = __builtin_amdgcn_exp2f(ws.m_run - mnew);
+  const float delta = m_ref - mnew;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    t0[i] += delta;
+    t1[i] += delta;
+  }
+  ws.m_run = mnew;
+  // exponent this lane's scales need, then the wave's
+  const int sb = smax.x > smax.y ? smax.x : smax.y;
+  int need = sb > (int)kVScaleMax ? (sb - (int)kVScaleMax + 1023) >> 10 : 0;
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) {
+    const int o = __shfl_xor(need, d, kWave);
+    need = o > need ? o : need;
+  }
+  const int ev_new = need > ws.ev ? need : ws.ev;
+  const float fv = __builtin_ldexpf(1.0f, ws.ev - ev_new);
+  if (ev_new != ws.ev) {
+    ws.ev = ev_new;
+    set_wv<FAM, BV>(ev_new, ws.wv);
+  }
+  xdl_wait();
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    // accumulator row 4r+i belongs to query (4r+i) mod GP
+    const float ar = __shfl(alpha, (4 * lo.r + i) & (lo.GP - 1), kWave);
+    const float av = ar * fv;
+#pragma unroll
+    for (int nt = 0; nt < 8; ++nt) scale_inplace(ws.acc[nt], i, av);
+    if constexpr (FAM == RQ_QUAROT) scale_inplace(ws.corrO, i, av);
+    scale_inplace(ws.corrZ, i, ar);
+  }
+  xdl_wait();
 }
 
 // One block from the LDS slot: QK^T, online softmax, PV.
@@ -520,49 +625,31 @@ __device__ __forceinline__ void block_step(const uint8_t* slot, const LaneOps& l
   sp.km = reinterpret_cast<const u4*>(slot + 512 * (BK + BV));
   sp.vm = reinterpret_cast<const u4*>(slot + 512 * (BK + BV) + MB);
   const float m_ref = ws.m_run == -INFINITY ? 0.0f : ws.m_run;
-  f4 S0, S1;
-  kpart<FAM, BK>(sp, lo, m_ref, S0, S1);
+  f4 t0, t1;
+  kpart<FAM, BK>(sp, lo, m_ref, t0, t1);
+  const VScales<FAM, NA> vs = load_vscales<FAM, NA>(sp, lo);
   // keep the phases apart: hoisting all LDS reads of the block to its top
-  // needs more registers than two waves per SIMD allow
+  // needs more registers than the waves per SIMD allow
   __builtin_amdgcn_sched_barrier(0);
-  float mx = max3(S0[0], S1[0], S0[1]);
-  mx = max3(mx, S1[1], S0[2]);
-  mx = max3(mx, S1[2], S0[3]);
-  mx = max3(mx, S1[3], S1[3]);
-  if (__builtin_amdgcn_ballot_w64(!(mx <= kLazy) || ws.m_run == -INFINITY)) {
-    mx = __builtin_fmaxf(mx, xor_shfl(mx, 16));
-    mx = __builtin_fmaxf(mx, xor_shfl(mx, 32));
-    const float mnew = __builtin_fmaxf(ws.m_run, m_ref + mx);
-    const float alpha = __builtin_amdgcn_exp2f(ws.m_run - mnew);
-    const float delta = m_ref - mnew;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      S0[i] += delta;
-      S1[i] += delta;
-    }
-    ws.m_run = mnew;
-    xdl_wait();
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      // accumulator row 4r+i belongs to query (4r+i) mod GP
-      const float ar = __shfl(alpha, (4 * lo.r + i) & (lo.GP - 1), kWave);
-#pragma unroll
-      for (int nt = 0; nt < 8; ++nt) scale_inplace(ws.acc[nt], i, ar);
-#pragma unroll
-      for (int a = 0; a < NA; ++a) scale_inplace(ws.corrA[a], i, ar);
-      scale_inplace(ws.corrZ, i, ar);
-    }
-    xdl_wait();
-  }
+  float mx = max3(t0[0], t1[0], t0[1]);
+  mx = max3(mx, t1[1], t0[2]);
+  mx = max3(mx, t1[2], t0[3]);
+  mx = max3(mx, t1[3], t1[3]);
+  const us2 smax = vscale_max<FAM, NA>(vs);
+  const uint32_t thr = (kVScaleMax + ((uint32_t)ws.ev << 10)) * 0x00010001u;
+  const bool big = __builtin_bit_cast(uint32_t, __builtin_elementwise_max(
+                       smax, __builtin_bit_cast(us2, thr))) != thr;
+  if (__builtin_amdgcn_ballot_w64(!(mx <= kLazy) || ws.m_run == -INFINITY || big))
+    block_rescale<FAM, NA, BV>(lo, m_ref, mx, smax, t0, t1, ws);
   uint32_t P[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const h2 pv = {(_Float16)__builtin_amdgcn_exp2f(S0[i]),
-                   (_Float16)__builtin_amdgcn_exp2f(S1[i])};
+    const h2 pv = {(_Float16)__builtin_amdgcn_exp2f(t0[i]),
+                   (_Float16)__builtin_amdgcn_exp2f(t1[i])};
     P[i] = as_u32(pv);
   }
   __builtin_amdgcn_sched_barrier(0);
-  vpart<FAM, NA, BV>(sp, lo, P, cst, ws);
+  vpart<FAM, NA, BV>(sp, lo, P, vs, cst, ws);
 }
 
 // A block's data is four contiguous byte ranges: K codes (512*BK), V codes
@@ -1081,17 +1168,29 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
   __syncthreads();
   LaneOps lo;
   lo.lane = lane;
-  lo.magic = opaque_magic();
   lo.r = lane >> 4;
   lo.col = lane & 15;
   lo.GP = a.GP;
   lo.gsub = lo.col / a.GP;
+  lo.tabk = lo.tabv = nullptr;
   {
     // this lane's query row j = col mod GP, channels 32 r .. 32 r + 31
     // (the rotated row for QuaRot and TurboQuant), scaled
     const int j = lo.col & (a.GP - 1);
     float qv[32];
     if (FAM == RQ_TURBO) {
+      if (MAXB > 4) {
+        // fp16 centroid tables of the unit's K and V widths (above 4 bits
+        // they are looked up in LDS); rotate_queries ends with a barrier
+        _Float16* tab = reinterpret_cast<_Float16*>(reinterpret_cast<uint8_t*>(qs) +
+                                                    (size_t)G * kD * sizeof(float));
+        for (int e = tid; e < 512; e += kThreads) {
+          const int side = e >> 8, k = e & 255, bb = side ? bv : bk;
+          if (k < (1 << bb)) tab[e] = (_Float16)a.cb[(bb - 1) * 512 + 256 + k];
+        }
+        lo.tabk = (lds_h*)tab;
+        lo.tabv = (lds_h*)(tab + 256);
+      }
       rotate_queries(a, h, qraw, qs);
 #pragma unroll
       for (int i = 0; i < 32; ++i) qv[i] = j < G ? qs[j][32 * lo.r + i] : 0.0f;
@@ -1137,6 +1236,16 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
 #pragma unroll
       for (int i = 0; i < 32; ++i) qv[i] *= f;
     }
+    // row exponent e: the row's largest |q'| is below 2^e (frexp), so every
+    // q' 2^-e lies in (-1, 1); 0 for a zero row
+    float amax = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 32; ++i) amax = __builtin_fmaxf(amax, __builtin_fabsf(qv[i]));
+    amax = __builtin_fmaxf(amax, xor_shfl(amax, 16));
+    amax = __builtin_fmaxf(amax, xor_shfl(amax, 32));
+    const int e = amax > 0.0f ? __builtin_amdgcn_frexp_expf(amax) : 0;
+    lo.cK = __builtin_ldexpf(1.0f, FAM == RQ_TURBO ? e : 24 + e);
+    lo.eK = __builtin_ldexpf(1.0f, e);
     // static QK operands: k-slot pair (kb, k') = channels 32r + 4kb + k'
     // and 32r + 16 + 4kb + k'
     const int8_t* kp = kFieldPos.k[bk];
@@ -1146,36 +1255,28 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
         const float q0 = qv[4 * kb + kk], q1 = qv[16 + 4 * kb + kk];
-        const float wgt = FAM == RQ_TURBO ? 1.0f : __builtin_ldexpf(1.0f, -kp[4 * kb + kk]);
-        const h2 vh = {(_Float16)(q0 * wgt), (_Float16)(q1 * wgt)};
-        const h2 vz = {(_Float16)q0, (_Float16)q1};
+        const int sh = FAM == RQ_TURBO ? -e : -e - kp[4 * kb + kk];
+        const h2 vh = {(_Float16)__builtin_ldexpf(q0, sh), (_Float16)__builtin_ldexpf(q1, sh)};
+        const h2 vz = {(_Float16)__builtin_ldexpf(q0, -e), (_Float16)__builtin_ldexpf(q1, -e)};
         lo.qh[4 * kb + kk] = as_u32(vh);
         lo.qz[4 * kb + kk] = as_u32(vz);
       }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int e = vp[i];
-      lo.wv[i] = h_pair((uint32_t)(15 - e) << 10);
-      const _Float16 v = (_Float16)(-(1024.0f + (float)(1 << (bv - 1)) * __builtin_ldexpf(1.0f, e)));
-      const h2 vv = {v, v};
-      lo.vq[i] = as_u32(vv);
-    }
+    for (int i = 0; i < 4; ++i) lo.vq[i] = h_pair((uint32_t)(15 + vp[i]) << 10);
     lo.corrK = (f4){0.f, 0.f, 0.f, 0.f};
     if (FAM == RQ_TURBO) {
       tq_make_lut(a.cb, bk, lo.lutk);
       tq_make_lut(a.cb, bv, lo.lutv);
     }
     if (FAM == RQ_QUAROT) {
-      const float off = (float)(1 << (bk - 1));
+      // the symmetric offset of the key codes, -2^(b-1) at the codes'
+      // weights 2^(kpos-24) (exact subnormals), against the query operands
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) {
         uint32_t c[4];
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-          const _Float16 v = (_Float16)(-(1024.0f + off * __builtin_ldexpf(1.0f, kp[4 * kb + kk])));
-          const h2 vv = {v, v};
-          c[kk] = as_u32(vv);
-        }
+        for (int kk = 0; kk < 4; ++kk)
+          c[kk] = h_pair(0x8000u | (1u << (bk - 1 + kp[4 * kb + kk])));
         lo.corrK = mfma(make_h8(c[0], c[1], c[2], c[3]),
                         make_h8(lo.qh[4 * kb], lo.qh[4 * kb + 1], lo.qh[4 * kb + 2],
                                 lo.qh[4 * kb + 3]),
@@ -1187,10 +1288,17 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
   WaveState<NA> ws;
 #pragma unroll
   for (int nt = 0; nt < 8; ++nt) ws.acc[nt] = (f4){0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int i = 0; i < NA; ++i) ws.corrA[i] = (f4){0.f, 0.f, 0.f, 0.f};
+  ws.corrO = (f4){0.f, 0.f, 0.f, 0.f};
   ws.corrZ = (f4){0.f, 0.f, 0.f, 0.f};
   ws.m_run = -INFINITY;
+  ws.ev = 0;
+  {
+    // value slots' 2^-vpos (TurboQuant: 1), the exponent Ev = 0
+    const int8_t* vp = kFieldPos.v[bv];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      ws.wv[i] = h_pair((uint32_t)(15 - (FAM == RQ_TURBO ? 0 : vp[i])) << 10);
+  }
 
   // blocks at normal priority; what comes before and after at raised
   // priority (see attn_kernel)
@@ -1212,6 +1320,12 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
   float mrow[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) mrow[i] = __shfl(ws.m_run, (4 * r + i) & (GP - 1), kWave);
+  // scale of the value sums: 2^(24+Ev) for codes as subnormals (QuaRot and
+  // RTN: 2^Ev times 2^24 acc minus the offset 2^(b-1) corrO), 2^Ev / sqrt(128)
+  // for TurboQuant
+  const float cv = FAM == RQ_TURBO ? __builtin_ldexpf(kInvSqrtD, ws.ev)
+                                   : __builtin_ldexpf(1.0f, FAM == RQ_QUAROT ? ws.ev : 24 + ws.ev);
+  const float voff = (float)(1 << (bv - 1));
   __syncthreads();   // every wave is done with its slot
   float* mw = merge + (size_t)wave * G * (2 + kD);
 #pragma unroll
@@ -1221,10 +1335,9 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
       if (FAM == RQ_KIVI) {
 #pragma unroll
         for (int nt = 0; nt < 8; ++nt) {
-          const int gt = nt / 2, at = gt / GPA;
+          const int gt = nt / 2;
           if (gs == gt % GPA)
-            mw[jj * (2 + kD) + 2 + 16 * nt + col] =
-                ws.acc[nt][i] + ws.corrA[at][i] + zt[gt][i];
+            mw[jj * (2 + kD) + 2 + 16 * nt + col] = __builtin_fmaf(ws.acc[nt][i], cv, zt[gt][i]);
         }
         if (gs == 0 && col == 0) {
           mw[jj * (2 + kD)] = mrow[i];
@@ -1232,8 +1345,14 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
         }
       } else if (gs == 0) {
 #pragma unroll
-        for (int nt = 0; nt < 8; ++nt)
-          mw[jj * (2 + kD) + 2 + 16 * nt + col] = ws.acc[nt][i] + ws.corrA[0][i];
+        for (int nt = 0; nt < 8; ++nt) {
+          float v;
+          if (FAM == RQ_QUAROT)
+            v = __builtin_fmaf(ws.acc[nt][i], 16777216.0f, -voff * ws.corrO[i]) * cv;
+          else
+            v = ws.acc[nt][i] * cv;
+          mw[jj * (2 + kD) + 2 + 16 * nt + col] = v;
+        }
         if (col == 0) {
           mw[jj * (2 + kD)] = mrow[i];
           mw[jj * (2 + kD) + 1] = lrow[i];

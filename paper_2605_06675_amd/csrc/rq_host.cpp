@@ -372,16 +372,6 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
     return fail(RQ_EINVAL, "NULL device pointer");
   if (!std::isfinite(scale)) return fail(RQ_EINVAL, "scale is not finite");
   const rq::LayerTable tab = layer_table(c, layer);
-  int maxb = 1;
-  for (int h = 0; h < c->n_kv_heads; ++h) {
-    const int kb = tab.bits[h][0], vb = tab.bits[h][1];
-    maxb = kb > maxb ? kb : maxb;
-    maxb = vb > maxb ? vb : maxb;
-  }
-  if (c->family == RQ_TURBO && maxb > 4)
-    return fail(RQ_EUNSUPPORTED,
-                "TurboQuant decode attention handles widths up to 4 bits (layer %d has %d)",
-                layer, maxb);
   int max_blk = 0;
   for (int h = 0; h < c->n_kv_heads; ++h) {
     const int bb = 512 * (tab.bits[h][0] + tab.bits[h][1]) + 2 * meta_per_block(c);

@@ -1,9 +1,10 @@
 """GPU parity on the degenerate inputs the quantizers special-case, for every
 family: all-zero tokens and groups (scale or norm 0), constant rows (KIVI's
 min-max range 0), single-channel spikes, and bf16 values beyond the fp16
-range (the fp16 metadata saturates at 65504).  Codes, metadata and the
-window must match the oracle (TurboQuant codes by its near-threshold rule);
-attention is checked where the values stay in the fp16 operand range."""
+range (the fp16 metadata saturates at 65504), and queries far above and
+below unit scale.  Codes, metadata and the window must match the oracle
+(TurboQuant codes by its near-threshold rule); attention must match it
+everywhere, to 1e-2 at unit scale and in proportion beyond."""
 import numpy as np
 import pytest
 
@@ -70,7 +71,25 @@ def test_saturated_metadata_bf16(family):
     print(f"saturated metadata family {family}", flush=True)
     bits = np.array([[[2, 3], [3, 2], [4, 4], [5, 6]]])
     kvc, ks, vs = _fill(family, workloads.BF16, bits, _data(3, 2.0e5), _data(4, 2.0e5))
-    gp._check_cache(family, workloads.BF16, kvc, ks, vs, bits, R, BATCH, H, T)
+    units = gp._check_cache(family, workloads.BF16, kvc, ks, vs, bits, R, BATCH, H, T)
+    gp._check_attention(kvc, units, workloads.BF16, BATCH, H, G)
+
+
+@pytest.mark.parametrize("q_mult", [1.0e6, 1.0e-6], ids=["q1e6", "q1e-6"])
+@pytest.mark.parametrize("family", [workloads.KIVI, workloads.QUAROT,
+                                    workloads.RTN], ids=["kivi", "quarot", "rtn"])
+def test_large_values_and_queries(family, q_mult):
+    # value scales near the fp16 maximum (probability x scale beyond the
+    # fp16 range) and queries whose scaled elements leave it (q1e6) or
+    # underflow it (q1e-6)
+    print(f"large values family {family} q x {q_mult:g}", flush=True)
+    bits = np.array([[[2, 2], [3, 2], [4, 3], [8, 5]]])
+    rng = np.random.default_rng(11)
+    kf = rng.standard_normal((BATCH, H, T, 128))
+    vf = rng.standard_normal((BATCH, H, T, 128)) * 3.0e4
+    kvc, ks, vs = _fill(family, workloads.BF16, bits, kf, vf)
+    units = gp._check_cache(family, workloads.BF16, kvc, ks, vs, bits, R, BATCH, H, T)
+    gp._check_attention(kvc, units, workloads.BF16, BATCH, H, G, q_mult=q_mult)
 
 
 def test_degenerate_turbo():
@@ -82,3 +101,20 @@ def test_degenerate_turbo():
                         rotation=gh.dev(r16, workloads.BF16))
     units = gt._check(dtype, kvc, ks, vs, rf[0], bits, R, BATCH, H)
     gt._attention(kvc, units, dtype, BATCH, H, G)
+
+
+@pytest.mark.parametrize("q_mult", [1.0e6, 1.0e-6], ids=["q1e6", "q1e-6"])
+def test_large_values_and_queries_turbo(q_mult):
+    # norms near the fp16 maximum (probability x norm / sqrt(128) beyond
+    # the fp16 range) and queries far from unit scale; widths 1..8
+    print(f"large values turbo q x {q_mult:g}", flush=True)
+    dtype = workloads.BF16
+    bits = np.array([[[1, 6], [3, 8], [5, 2], [7, 4]]])
+    rng = np.random.default_rng(12)
+    kf = rng.standard_normal((BATCH, H, T, 128))
+    vf = rng.standard_normal((BATCH, H, T, 128)) * 5.0e3
+    r16, rf = gt._rotations(1, H)
+    kvc, ks, vs = _fill(workloads.TURBO, dtype, bits, kf, vf,
+                        rotation=gh.dev(r16, workloads.BF16))
+    units = gt._check(dtype, kvc, ks, vs, rf[0], bits, R, BATCH, H)
+    gt._attention(kvc, units, dtype, BATCH, H, G, q_mult=q_mult)

@@ -73,21 +73,30 @@ def _check_cache(family, dtype, kvc, ks, vs, bits, R, batch, H, T):
     return units
 
 
-def _check_attention(kvc, units, dtype, batch, H, G, seed=7):
+def attention_tol(v_hat):
+    """Attention tolerance of one unit: 1e-2 max-abs for values of the
+    workloads' unit scale, growing in proportion to the values beyond it
+    (fp16 operands carry 11 significant bits whatever the magnitude)."""
+    return ATOL * max(1.0, float(np.max(np.abs(v_hat))) / 8.0)
+
+
+def _check_attention(kvc, units, dtype, batch, H, G, seed=7, q_mult=1.0):
     torch = _torch()
-    q16 = np.random.default_rng(seed).standard_normal((batch, H * G, 128))
+    q16 = np.random.default_rng(seed).standard_normal((batch, H * G, 128)) * q_mult
     q16 = workloads.bits16_from_f32(q16, dtype)
     out = kvc.attention(0, gh.dev(q16, dtype))
     torch.cuda.synchronize()
     out = out.cpu().numpy()
+    assert np.all(np.isfinite(out))
     worst = 0.0
     for (b, h), u in units.items():
         q = workloads.u16_to_f32(q16[b, h * G:(h + 1) * G], dtype)
-        want = oatt.decode_attention(q, u.keys(), u.values())
+        v_hat = u.values()
+        want = oatt.decode_attention(q, u.keys(), v_hat)
         err = np.max(np.abs(out[b, h * G:(h + 1) * G] - want))
-        worst = max(worst, err)
-    print(f"attention max-abs error {worst:.3e}")
-    assert worst < ATOL
+        assert err < attention_tol(v_hat), (b, h, err, attention_tol(v_hat))
+        worst = max(worst, err / attention_tol(v_hat) * ATOL)
+    print(f"attention max-abs error {worst:.3e} (at unit scale)")
     return worst
 
 
