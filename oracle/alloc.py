@@ -19,16 +19,20 @@ the average bit-width and the component count).
 * ``waterfill_iterative``: the paper's own bound-handling loop (Appendix
   "Proof of Theorem 1", "Iterative waterfilling"): solve with all free, clip
   violators to their bound and fix them, update the budget, repeat.
-* ``greedy``: Stage 3 of Alg. 1 with the max-heap of Alg. 2 -- start every
-  component at bmin and hand out the remaining R = B - n*bmin bits one at a
-  time to the largest marginal gain w_i [D_i(b_i) - D_i(b_i+1)]
-  = w_i alpha_i beta_i^-b_i (1 - 1/beta_i), among components below bmax.
-  The heap key is the logarithm of that gain, evaluated in IEEE double as
-  log(w) + log(alpha) - b*log(beta) + log1p(-1/beta) (left to right).  Equal
-  keys go to the lowest index (the paper does not say).
+* ``greedy``: the integer allocation of Stage 3 of Alg. 1 / Alg. 2, written
+  from its definition rather than its listing.  Raising component i from b
+  to b+1 lowers J by the marginal gain w_i [D_i(b) - D_i(b+1)]
+  = w_i alpha_i beta_i^-b (1 - 1/beta_i) (Sec. 3.3; Proposition 3), a
+  strictly decreasing function of b when beta_i > 1.  Starting every
+  component at bmin, the greedy rule spends the remaining R = B - n*bmin
+  bits on the R largest gains; because each component's gains fall with b,
+  that is the same as ranking all n (bmax - bmin) increments (i, b) at once
+  and keeping the top R.  Gains are compared through their logarithm,
+  evaluated in IEEE double as log(w) + log(alpha) - b*log(beta) +
+  log1p(-1/beta) (left to right); equal keys go to the lower index, then the
+  lower b (the paper does not say).
 * ``brute_force``: exhaustive search of the integer problem (tiny n).
 """
-import heapq
 import itertools
 import math
 
@@ -127,22 +131,19 @@ def gain_key(w, alpha, beta, b):
 
 
 def greedy(w, alpha, beta, B, bmin, bmax):
-    """Integer allocation (Alg. 1 Stage 3 / Alg. 2).  Returns int32 array."""
+    """Integer allocation (Alg. 1 Stage 3 / Alg. 2; Proposition 3): every
+    component at bmin plus one bit for each of the R = B - n*bmin largest
+    marginal gains among all increments (i, b), bmin <= b < bmax.  Returns
+    an int32 array."""
     w, alpha, beta = _check(w, alpha, beta, B, bmin, bmax)
     n = w.size
-    b = np.full(n, bmin, dtype=np.int64)
     R = B - n * bmin
-    heap = []
-    if bmin < bmax:
-        heap = [(-gain_key(w[i], alpha[i], beta[i], bmin), i) for i in range(n)]
-        heapq.heapify(heap)
-    while R > 0:
-        _, i = heapq.heappop(heap)
-        b[i] += 1
-        R -= 1
-        if b[i] < bmax:
-            heapq.heappush(heap, (-gain_key(w[i], alpha[i], beta[i], b[i]), i))
-    return b.astype(np.int32)
+    steps = sorted((-gain_key(w[i], alpha[i], beta[i], b), i, b)
+                   for i in range(n) for b in range(bmin, bmax))
+    bits = np.full(n, bmin, dtype=np.int64)
+    for _, i, _ in steps[:R]:
+        bits[i] += 1
+    return bits.astype(np.int32)
 
 
 def brute_force(w, alpha, beta, B, bmin, bmax):
