@@ -45,11 +45,15 @@ STEPS = {"qwen3-32b-kv-b1-t131072-kivi-2b": 64}
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=5)
-    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--workload", default=DEFAULT)
-    p.add_argument("--cpu-seconds", type=float, default=15.0,
-                   help="budget of the oracle CPU-baseline sample")
+    p.add_argument("--cpu-seconds", type=float, default=8.0,
+                   help="budget of each oracle CPU-baseline sample (one core, "
+                        "then all cores)")
+    p.add_argument("--cpu-workers", type=int, default=0,
+                   help="processes of the all-core sample (0: the cores this "
+                        "process may run on, at most 16)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--calib-tokens", type=int, default=512)
     return p.parse_args()
@@ -93,81 +97,140 @@ def quantize_bytes(wl, bits_table, T):
     return total
 
 
-def cpu_baseline(wl, bits_table, seconds):
-    """The oracle (numpy), as it stands, on a bounded sample of the same
-    workload: whole (layer, batch entry, kv-head) units, each quantized and
-    packed by the oracle (its cache builder), then decode attention read
-    back from the packed codes (unpack + dequantize + fp64 attention).
-    Units are added until the time budget is spent.  Reports the attention
-    rate in the metric's unit (algorithmic bytes / oracle attention time)
-    and the quantize rate in whole-model tokens per second."""
-    from threadpoolctl import threadpool_limits
-
+def _oracle_unit(job):
+    """One (layer, batch entry, kv-head) unit through the oracle: quantize +
+    pack (its cache builder), then unpack + dequantize + fp64 decode
+    attention from the packed codes.  Returns (quantize s, attention s,
+    algorithmic attention bytes)."""
     import workloads
     from oracle import attention as oatt
     from oracle import cache as ocache
     from oracle import fmt
     from oracle import quant as oq
-
-    T = wl.context
-    R = wl.residual
+    wname, l, b, h, bk, bv = job
+    wl = workloads.WORKLOADS[wname]
+    T, R, G = wl.context, wl.residual, wl.group
     nq = n_quantized(T, R)
-    G = wl.group
     mb = meta_per_block(wl.family)
-    att_bytes, t_att, t_q, units = 0, 0.0, 0.0, 0
-    with threadpool_limits(limits=1):
-        for l, b in ((l, b) for l in range(wl.n_layers)
-                     for b in range(wl.batch)):
-            if t_att + t_q >= seconds:
-                break
-            q16 = workloads.q_cpu(wl, l)
-            k16, v16 = workloads.kv_cpu(wl, l, b, T)
+    q16 = workloads.q_cpu(wl, l)
+    k16, v16 = workloads.kv_cpu(wl, l, b, T)
+    k = workloads.u16_to_f32(k16[h], wl.dtype)
+    v = workloads.u16_to_f32(v16[h], wl.dtype)
+    q = workloads.u16_to_f32(q16[b, h * G:(h + 1) * G], wl.dtype)
+    rot = None
+    if wl.family == workloads.TURBO:
+        rot = workloads.u16_to_f32(workloads.turbo_rotation(42, l, h),
+                                   workloads.BF16).astype(np.float64)
+    t0 = time.perf_counter()
+    u = ocache.Unit(wl.family, k, v, bk, bv, R, rotation=rot)
+    t1 = time.perf_counter()
+    kc = ocache.unpack_keys(u.k_words, bk)
+    vc = ocache.unpack_values(u.v_words, bv)
+    if wl.family == workloads.KIVI:
+        kh = oq.kivi_dequant_keys(kc, *_kivi_meta_keys(u.k_meta))
+        vh = oq.kivi_dequant_values(vc, *_kivi_meta_values(u.v_meta))
+    else:
+        nk = fmt.from_pair_order(u.k_meta).reshape(-1)
+        nv = fmt.from_pair_order(u.v_meta).reshape(-1)
+        if wl.family == workloads.QUAROT:
+            kh, vh = oq.quarot_dequant(kc, nk, bk), oq.quarot_dequant(vc, nv, bv)
+        elif wl.family == workloads.RTN:
+            kh, vh = oq.rtn_dequant(kc, nk, bk), oq.rtn_dequant(vc, nv, bv)
+        else:
+            kh = oq.turbo_dequant(kc, nk, rot, bk)
+            vh = oq.turbo_dequant(vc, nv, rot, bv)
+    oatt.decode_attention(q, np.concatenate([kh, u.k_res]),
+                          np.concatenate([vh, u.v_res]))
+    t2 = time.perf_counter()
+    nbytes = (nq * 128 * (bk + bv) // 8 + 2 * (nq // 32) * mb
+              + 2 * (T - nq) * 256 + G * 128 * 6)
+    return t1 - t0, t2 - t1, nbytes
+
+
+def _pool_init():
+    from threadpoolctl import threadpool_limits
+    global _LIMITS
+    _LIMITS = threadpool_limits(limits=1)
+
+
+def _cpu_jobs(wl, bits_table):
+    for l in range(wl.n_layers):
+        for b in range(wl.batch):
             for h in range(wl.n_kv_heads):
-                if t_att + t_q >= seconds:
+                yield (wl.name, l, b, h, int(bits_table[l, h, 0]),
+                       int(bits_table[l, h, 1]))
+
+
+def _cpu_rates(res, wall, wl):
+    """Attention GB/s and whole-model quantize tok/s of a finished sample;
+    with wall set, rates over the wall time of all processes together."""
+    tq = sum(r[0] for r in res)
+    ta = sum(r[1] for r in res)
+    nb = sum(r[2] for r in res)
+    units = len(res)
+    if wall:
+        # each process spends its time in proportion: split the wall time
+        ta_w, tq_w = wall * ta / (ta + tq), wall * tq / (ta + tq)
+    else:
+        ta_w, tq_w = ta, tq
+    tok = units * wl.context / (wl.n_layers * wl.n_kv_heads)
+    return nb / ta_w / 1e9, tok / tq_w, tq, ta
+
+
+def cpu_baseline(wl, bits_table, seconds, workers):
+    """The oracle (numpy), as it stands, on bounded samples of the same
+    workload: whole (layer, batch entry, kv-head) units, first on one core
+    (units run one after another until the budget is spent), then on every
+    allowed core (one process per core, each single-threaded, for about the
+    same wall time).  Runs before the GPU is touched, so the worker
+    processes are plain forks.  Reports the attention rate in the metric's
+    unit (algorithmic bytes / oracle attention time) and the quantize rate
+    in whole-model tokens per second."""
+    import multiprocessing as mp
+    import platform
+    from threadpoolctl import threadpool_limits
+
+    model = platform.processor() or "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
                     break
-                k = workloads.u16_to_f32(k16[h], wl.dtype)
-                v = workloads.u16_to_f32(v16[h], wl.dtype)
-                bk, bv = int(bits_table[l, h, 0]), int(bits_table[l, h, 1])
-                q = workloads.u16_to_f32(q16[b, h * G:(h + 1) * G], wl.dtype)
-                rot = None
-                if wl.family == workloads.TURBO:
-                    rot = workloads.u16_to_f32(workloads.turbo_rotation(42, l, h),
-                                               workloads.BF16).astype(np.float64)
-                t0 = time.perf_counter()
-                u = ocache.Unit(wl.family, k, v, bk, bv, R, rotation=rot)
-                t1 = time.perf_counter()
-                kc = ocache.unpack_keys(u.k_words, bk)
-                vc = ocache.unpack_values(u.v_words, bv)
-                if wl.family == workloads.KIVI:
-                    kh = oq.kivi_dequant_keys(kc, *_kivi_meta_keys(u.k_meta))
-                    vh = oq.kivi_dequant_values(vc, *_kivi_meta_values(u.v_meta))
-                else:
-                    nk = fmt.from_pair_order(u.k_meta).reshape(-1)
-                    nv = fmt.from_pair_order(u.v_meta).reshape(-1)
-                    if wl.family == workloads.QUAROT:
-                        kh, vh = oq.quarot_dequant(kc, nk, bk), oq.quarot_dequant(vc, nv, bv)
-                    elif wl.family == workloads.RTN:
-                        kh, vh = oq.rtn_dequant(kc, nk, bk), oq.rtn_dequant(vc, nv, bv)
-                    else:
-                        kh = oq.turbo_dequant(kc, nk, rot, bk)
-                        vh = oq.turbo_dequant(vc, nv, rot, bv)
-                oatt.decode_attention(q, np.concatenate([kh, u.k_res]),
-                                      np.concatenate([vh, u.v_res]))
-                t2 = time.perf_counter()
-                t_q += t1 - t0
-                t_att += t2 - t1
-                units += 1
-                att_bytes += (nq * 128 * (bk + bv) // 8 + 2 * (nq // 32) * mb
-                              + 2 * (T - nq) * 256 + G * 128 * 6)
-    # a whole-model token is one token of every (layer, kv-head)
-    q_tok_s = units * T / (wl.n_layers * wl.n_kv_heads) / t_q
-    return {"value": round(att_bytes / t_att / 1e9, 4), "unit": "GB/s",
-            "cores": 1, "kind": "oracle",
-            "quantize_tok_s": round(q_tok_s, 1),
-            "sample": f"{units} (layer, batch, kv-head) units, {T} tokens "
-                      f"each: oracle quantize + pack ({t_q:.1f} s), then "
-                      f"unpack + dequantize + fp64 decode attention "
-                      f"({t_att:.1f} s); single thread"}
+    except OSError:
+        pass
+    allowed = len(os.sched_getaffinity(0))
+    n = workers or min(16, allowed)
+    jobs = _cpu_jobs(wl, bits_table)
+    one = []
+    t0 = time.perf_counter()
+    with threadpool_limits(limits=1):
+        for job in jobs:
+            one.append(_oracle_unit(job))
+            if time.perf_counter() - t0 >= seconds:
+                break
+    a1, q1, tq1, ta1 = _cpu_rates(one, 0.0, wl)
+    # all cores: about `seconds` of wall time
+    per_unit = (time.perf_counter() - t0) / len(one)
+    n_units = max(n, int(seconds / per_unit) * n)
+    batch = [j for _, j in zip(range(n_units), _cpu_jobs(wl, bits_table))]
+    ctx = mp.get_context("fork")
+    t1 = time.perf_counter()
+    with ctx.Pool(n, initializer=_pool_init) as pool:
+        many = pool.map(_oracle_unit, batch, chunksize=1)
+    wall = time.perf_counter() - t1
+    an, qn, tqn, tan = _cpu_rates(many, wall, wl)
+    return {"value": round(an, 4), "unit": "GB/s", "cores": n, "kind": "oracle",
+            "quantize_tok_s": round(qn, 1),
+            "single_core": {"value": round(a1, 4), "unit": "GB/s",
+                            "quantize_tok_s": round(q1, 1), "units": len(one),
+                            "seconds": round(tq1 + ta1, 2)},
+            "cpu_model": model, "nproc": os.cpu_count(), "allowed_cpus": allowed,
+            "sample": f"{len(many)} (layer, batch, kv-head) units of "
+                      f"{wl.context} tokens on {n} processes ({wall:.1f} s wall; "
+                      f"single core: {len(one)} units, {tq1 + ta1:.1f} s): oracle "
+                      f"quantize + pack, then unpack + dequantize + fp64 decode "
+                      f"attention"}
 
 
 def _kivi_meta_keys(m):
@@ -255,6 +318,82 @@ def sensitivity_rate(args, wl, dev):
             "peak": PEAK_HBM_GBS, "frac": round(gbs / PEAK_HBM_GBS, 4)}
 
 
+def stream_ceiling(dev, gib=4, reps=10):
+    """The device's streaming-read rate: rq_read_probe (a plain kernel of
+    16-byte non-temporal loads) over a 4 GiB buffer, median of 10 calls."""
+    import torch
+
+    import paper_2605_06675_amd as rq
+    buf = torch.empty(gib << 30, dtype=torch.uint8, device=dev)
+    n_blocks = 4096
+    sink = torch.empty(n_blocks, dtype=torch.int32, device=dev)
+    rq.rq_read_probe(buf, sink, n_blocks)
+    ts = []
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        rq.rq_read_probe(buf, sink, n_blocks)
+        b.record()
+        torch.cuda.synchronize()
+        ts.append(a.elapsed_time(b) * 1e-3)
+    del buf
+    gbs = (gib << 30) / float(np.median(ts)) / 1e9
+    return {"kernel": "read_probe_kernel", "bytes": gib << 30,
+            "achieved": round(gbs, 1), "unit": "GB/s",
+            "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4)}
+
+
+def uniform_comparison(wl, kvc, prefill, dec, Q, outs, table, T0, nsteps,
+                       rot, dev, reps=10):
+    """The paper's zero-overhead claim (Appendix "Runtime Analysis"): decode
+    attention over a cache with every head at the same width and the same
+    average (K at floor, V at ceil of the average) against the mixed
+    allocation, both over the whole cache after the decode steps, all
+    layers, median of `reps`; the ratio compares time per algorithmic
+    byte (1.0 = no overhead from mixing widths)."""
+    import torch
+
+    import paper_2605_06675_amd as rq
+    L, H = table.shape[0], table.shape[1]
+    T = T0 + nsteps
+    ut = np.empty_like(table)
+    ut[..., 0] = int(np.floor(wl.avg_bits))
+    ut[..., 1] = int(np.ceil(wl.avg_bits))
+    ukv = rq.KVCache(wl.family, wl.dtype, L, wl.batch, H, wl.n_q_heads,
+                     wl.context, wl.residual, ut, device=dev, rotation=rot)
+    for l in range(L):
+        ukv.append(l, prefill[l][0], prefill[l][1])
+        for s in range(nsteps):
+            ukv.append(l, dec[l][0][s], dec[l][1][s])
+    ws = torch.zeros(max(rq.rq_decode_workspace(c.desc, T) for c in (kvc, ukv)),
+                     dtype=torch.uint8, device=dev)
+
+    def timed(c):
+        ts = []
+        for r in range(reps + 1):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for l in range(L):
+                rq.rq_decode_attention(c.desc, l, T, Q[l][nsteps - 1], outs[l], ws)
+            b.record()
+            torch.cuda.synchronize()
+            if r:
+                ts.append(a.elapsed_time(b) * 1e3 / L)
+        return float(np.median(ts))
+
+    us_m, us_u = timed(kvc), timed(ukv)
+    by_m = attention_bytes(wl, table, T) / L
+    by_u = attention_bytes(wl, ut, T) / L
+    del ukv
+    torch.cuda.empty_cache()
+    return {"uniform_bits_kv": [int(ut[0, 0, 0]), int(ut[0, 0, 1])],
+            "mixed_us_per_layer": round(us_m, 2), "uniform_us_per_layer": round(us_u, 2),
+            "mixed_gbs": round(by_m / us_m / 1e3, 1),
+            "uniform_gbs": round(by_u / us_u / 1e3, 1),
+            "time_ratio_mixed_over_uniform": round(us_m / us_u, 4),
+            "per_byte_ratio_mixed_over_uniform": round((us_m / by_m) / (us_u / by_u), 4)}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -262,26 +401,42 @@ def main():
                           "be 1 (the path shards by kv-head/batch with no "
                           "exchange, see the design notes)"}))
         sys.exit(2)
+    import workloads
+    from oracle import alloc as oalloc
+
+    wl = workloads.WORKLOADS[args.workload]
+    L, H = wl.n_layers, wl.n_kv_heads
+    lo, hi = min(wl.bit_set), max(wl.bit_set)
+    w, alpha_p, beta_p = workloads.allocation_inputs(wl)
+    cpu = None
+    if not args.no_cpu_baseline:
+        # the oracle's own allocation picks the sample's units; the host
+        # samples run before the GPU is initialised (the pool forks)
+        t_or = oalloc.greedy(w, alpha_p, beta_p,
+                             oalloc.budget(wl.n_comp, wl.avg_bits), lo, hi)
+        cpu = cpu_baseline(wl, np.asarray(t_or).reshape(L, H, 2),
+                           args.cpu_seconds, args.cpu_workers)
+        cpu["allocation_matches_library"] = None
+
     import torch
 
     import paper_2605_06675_amd as rq
-    import workloads
 
     rq.lib()
-    wl = workloads.WORKLOADS[args.workload]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    L, B, H, Hq, T = wl.n_layers, wl.batch, wl.n_kv_heads, wl.n_q_heads, wl.context
-    lo, hi = min(wl.bit_set), max(wl.bit_set)
+    B, Hq, T = wl.batch, wl.n_q_heads, wl.context
     n_comp = wl.n_comp
     nsteps = STEPS.get(wl.name, 1)
     T0 = T - nsteps                      # prefill length
     td = workloads.torch_dtype(wl.dtype)
 
     # ---- inputs, resident in HBM before timing
-    w, alpha_p, beta_p = workloads.allocation_inputs(wl)
     bits0, _, _ = rq.rq_allocate_bits(w, alpha_p, beta_p, wl.avg_bits, lo, hi)
     table = bits0.reshape(L, H, 2)
+    if cpu is not None:
+        cpu["allocation_matches_library"] = bool(np.array_equal(
+            np.asarray(t_or).reshape(-1), bits0))
     rot = None
     if wl.family == workloads.TURBO:
         r16 = workloads.turbo_rotations(wl)
@@ -358,13 +513,17 @@ def main():
     wall = time.perf_counter() - t0
 
     sens = sensitivity_rate(args, wl, dev)
+    ceiling = stream_ceiling(dev)
+    uniform = uniform_comparison(wl, kvc, prefill, dec, Q, outs, table, T0,
+                                 nsteps, rot, dev)
 
+    # stage times: medians over the timed steps
     el = lambda p: p[0].elapsed_time(p[1])
-    ms = {"calib": float(np.mean([el(r[0]["calib"]) for r in rec])),
-          "quantize": float(np.mean([el(r[0]["quantize"]) for r in rec])),
-          "append": float(np.mean([sum(el(x) for x in r[1]) for r in rec])),
-          "attention": float(np.mean([sum(el(x) for x in r[2]) for r in rec]))}
-    alloc_ms = float(np.mean([r[3] for r in rec])) * 1e3
+    ms = {"calib": float(np.median([el(r[0]["calib"]) for r in rec])),
+          "quantize": float(np.median([el(r[0]["quantize"]) for r in rec])),
+          "append": float(np.median([sum(el(x) for x in r[1]) for r in rec])),
+          "attention": float(np.median([sum(el(x) for x in r[2]) for r in rec]))}
+    alloc_ms = float(np.median([r[3] for r in rec])) * 1e3
     att_bytes = sum(attention_bytes(wl, table, T0 + s + 1) for s in range(nsteps))
     q_bytes = quantize_bytes(wl, table, T0)
     att_gbs = att_bytes / (ms["attention"] * 1e-3) / 1e9
@@ -423,10 +582,14 @@ def main():
                    "fitted_beta_median": round(float(np.nanmedian(beta_fit)), 3)},
         "roofline": rooflines[dom],
         "roofline_by_kernel": rooflines,
+        "stream_ceiling": ceiling,
+        "uniform_vs_mixed": uniform,
         "sensitivity": sens,
     }
-    if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(wl, table, args.cpu_seconds)
+    for name, r in rooflines.items():
+        r["frac_of_stream_ceiling"] = round(r["achieved"] / ceiling["achieved"], 4)
+    if cpu is not None:
+        line["cpu_baseline"] = cpu
     print(json.dumps(line), flush=True)
 
 

@@ -194,6 +194,15 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
                               float scale, void* ws, uint64_t ws_bytes,
                               rq_stream stream);
 
+/* Measurement utility, not part of the method: reads `bytes` (a multiple of
+ * 16) of the device buffer buf once with a plain streaming kernel of
+ * n_blocks workgroups (1..65535) of 256 threads and writes one word per
+ * workgroup to the device array sink[n_blocks].  Timed by the caller, it
+ * gives the device's streaming-read ceiling that the path's HBM rates are
+ * compared with.  Asynchronous. */
+rq_status rq_read_probe(const void* buf, uint64_t bytes, uint32_t* sink,
+                        int32_t n_blocks, rq_stream stream);
+
 /* Workspace bytes rq_calibrate_distortion needs. */
 rq_status rq_calibrate_workspace(int32_t n_comp, int32_t n_tokens,
                                  int32_t n_bits, uint64_t* bytes);

@@ -26,7 +26,7 @@ EXPORTS = ("rq_version", "rq_last_error", "rq_cache_sizes", "rq_region_offset",
            "rq_calibrate_workspace", "rq_calibrate_distortion",
            "rq_fit_distortion", "rq_allocate_bits", "rq_turbo_codebook",
            "rq_sensitivity_workspace", "rq_sensitivity", "rq_cap_weights",
-           "rq_fallback_beta")
+           "rq_fallback_beta", "rq_read_probe")
 RQ_TURBO_TABLE_FLOATS = 8 * 2 * 256
 
 
@@ -85,6 +85,7 @@ def lib():
             "rq_sensitivity": (i32, [i32, vp, i32, i32, i32, pd, vp, u64, vp]),
             "rq_cap_weights": (i32, [i32, pd, C.c_double]),
             "rq_fallback_beta": (i32, [i32, pd, pd, C.c_double]),
+            "rq_read_probe": (i32, [vp, u64, vp, i32, vp]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)
@@ -208,9 +209,35 @@ def rq_decode_workspace(cache, n_tokens):
 
 
 # --------------------------------------------------------------- device calls
+def _need_device(t, what, shape, elem):
+    """The C side sees raw pointers only: check what it cannot (shape,
+    element size, device, contiguity) before a kernel reads or writes the
+    buffer."""
+    if not t.is_cuda:
+        raise ValueError(f"{what} must be a device tensor")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{what} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if t.element_size() != elem:
+        raise ValueError(f"{what} has {t.element_size()}-byte elements, expected {elem}")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+
+
+def _check_attention_args(cache, q, out):
+    import torch
+    shape = (cache.batch, cache.n_q_heads, 128)
+    _need_device(q, "q", shape, 2)
+    _need_device(out, "out", shape, 4)
+    if out.dtype != torch.float32 or q.device != out.device:
+        raise ValueError("out must be float32 on q's device")
+
+
 def rq_quantize_kv(cache, layer, n_past, k, v, stream=None):
     """k, v: torch [batch][n_kv_heads][n_new][128] (fp16/bf16, device)."""
-    n_new = k.shape[2]
+    n_new = k.shape[2] if k.dim() == 4 else -1
+    shape = (cache.batch, cache.n_kv_heads, n_new, 128)
+    _need_device(k, "k", shape, 2)
+    _need_device(v, "v", shape, 2)
     _check(lib().rq_quantize_kv(C.byref(cache), layer, n_past, _tptr(k),
                                 _tptr(v), n_new, _stream(stream)))
 
@@ -221,9 +248,19 @@ def rq_decode_attention(cache, layer, n_tokens, q, out, ws, scale=None,
     byte tensor of at least rq_decode_workspace bytes."""
     if scale is None:
         scale = 1.0 / np.sqrt(128.0)
+    _check_attention_args(cache, q, out)
+    if not ws.is_cuda or not ws.is_contiguous():
+        raise ValueError("ws must be a contiguous device tensor")
     _check(lib().rq_decode_attention(
         C.byref(cache), layer, n_tokens, _tptr(q), _tptr(out), float(scale),
         _tptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def rq_read_probe(buf, sink, n_blocks, stream=None):
+    """Read the whole device tensor buf once (measurement utility); sink:
+    device int32/uint32 tensor of n_blocks elements."""
+    _check(lib().rq_read_probe(_tptr(buf), buf.numel() * buf.element_size(),
+                               _tptr(sink), int(n_blocks), _stream(stream)))
 
 
 def rq_calibrate_distortion(family, dtype, x, is_value, bits, ws=None,
@@ -332,14 +369,17 @@ class KVCache:
         rq_quantize_kv(self.desc, layer, self.n_tokens[layer], k, v, stream)
         self.n_tokens[layer] += k.shape[2]
 
-    def workspace(self, n_tokens):
+    def workspace(self, n_tokens, stream=None):
         import torch
         need = rq_decode_workspace(self.desc, n_tokens)
         if self._ws is None or self._ws.numel() < need:
-            # zeroed once: the arrival counters at its start must be zero
-            # before the first call (every call leaves them zero)
-            self._ws = torch.zeros(need, dtype=torch.uint8,
-                                   device=self.codes.device)
+            # zeroed once, on the stream of the call that first uses it: the
+            # arrival counters at its start must be zero before the first
+            # call (every call leaves them zero)
+            s = torch.cuda.current_stream() if stream is None else stream
+            with torch.cuda.stream(s):
+                self._ws = torch.zeros(need, dtype=torch.uint8,
+                                       device=self.codes.device)
         return self._ws
 
     def attention(self, layer, q, out=None, scale=None, stream=None):
@@ -347,6 +387,6 @@ class KVCache:
         if out is None:
             out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
         n = self.n_tokens[layer]
-        rq_decode_attention(self.desc, layer, n, q, out, self.workspace(n),
-                            scale, stream)
+        rq_decode_attention(self.desc, layer, n, q, out,
+                            self.workspace(n, stream), scale, stream)
         return out

@@ -1,10 +1,11 @@
 // Decode attention over the packed mixed-bit cache (KIVI-style,
 // QuaRot-style, TurboQuant-style and per-token symmetric RTN quantizers).
 //
-// Grid (workgroup slot, kv-head, batch), four waves per workgroup.  Slots
-// 0 .. n_wg-1 stream the quantized 32-token blocks of their (batch, kv-head)
-// unit (about three workgroups per CU in all); the first slots first attend
-// to the 16-bit residual window, 32 tokens each.  Each workgroup
+// Flat grid of (workgroup slot, unit) with the unit fastest, four waves per
+// workgroup; a unit is one (batch, kv-head).  Slots 0 .. nwg[h]-1 stream the
+// quantized 32-token blocks of their unit (about three workgroups per CU in
+// all, each kv-head's share sized by the cost of its widths); the first
+// slots first attend to the 16-bit residual window, 32 tokens each.  Each workgroup
 // writes a partial (max, sum, acc) with cache-coherent stores and takes a
 // ticket from a per-unit counter; the last to arrive merges the unit's
 // partials and writes the output (QuaRot: rotated back).  A wave streams every
@@ -19,7 +20,9 @@
 // so one AND turns a pair of codes into a pair of operands.  The weight
 // 2^(P-24) is divided out of the other operand (the query for keys, the
 // probability for values) or out of the fp32 result:
-//   KIVI keys    S = 2^24 sum_c (q_c s_c 2^-P) (u 2^(P-24)) + sum_c z_c q_c
+//   KIVI keys    S = 2^24 sum_c (q_c s_c 2^-P) (u 2^(P-24)) + sum_c z_c q_c,
+//                with q_c s_c 2^-P split into two fp16 operands (its rounded
+//                value and the rounding error) so that the sum is exact
 //   KIVI values  O = 2^24 sum_t (p_t s_t 2^-P) (u 2^(P-24)) + sum_t p_t z_t
 //   QuaRot       per-token scales and codes u - 2^(b-1): the offset enters as
 //                the accumulator's start value (keys) or one more MFMA
@@ -137,20 +140,16 @@ __host__ __device__ __forceinline__ constexpr int vpos(int b, int i) {
   return (w == 8 ? 8 * (i & 1) : i * w) - vshift(b, i);
 }
 // kpos and vpos of every width as a table, for set-up code where the width
-// is a run-time value (the helpers above loop and divide)
-struct FieldPos {
-  int8_t k[9][16];
-  int8_t v[9][4];
-};
-__host__ __device__ constexpr FieldPos make_field_pos() {
-  FieldPos t{};
+// is a run-time value (the helpers above loop and divide); it travels in
+// the kernel arguments, which every wave reads at its start anyway
+__host__ __device__ constexpr FieldPosTab make_field_pos() {
+  FieldPosTab t{};
   for (int b = 1; b <= 8; ++b) {
     for (int i = 0; i < 16; ++i) t.k[b][i] = (int8_t)kpos(b, i);
     for (int i = 0; i < 4; ++i) t.v[b][i] = (int8_t)vpos(b, i);
   }
   return t;
 }
-__constant__ const FieldPos kFieldPos = make_field_pos();
 
 // fp16 bits of 2^-e (0 <= e <= 14), exact
 constexpr uint32_t h_pow2_neg(int e) { return (uint32_t)(15 - e) << 10; }
@@ -210,6 +209,13 @@ __device__ __forceinline__ float ld_agent(const float* p) {
 
 __device__ __forceinline__ uint32_t pk_mul(uint32_t a, uint32_t b) {
   return as_u32(as_h2(a) * as_h2(b));
+}
+
+// a * b - c per fp16 half with one rounding (v_pk_fma_f16): with c the
+// rounded product, the product's rounding error, exact in fp16 unless it is
+// below the subnormal range
+__device__ __forceinline__ uint32_t pk_fms(uint32_t a, uint32_t b, uint32_t c) {
+  return as_u32(__builtin_elementwise_fma(as_h2(a), as_h2(b), -as_h2(c)));
 }
 
 // fp16 pair (u_i 2^(P-24), u_{i+16} 2^(P-24)) of key pair i of a chunk (its
@@ -367,13 +373,15 @@ struct WaveState {
 // Static per-lane operands built once per workgroup.
 struct LaneOps {
   uint32_t qh[16];  // QK B operand: fp16 q' 2^-(kpos + e) per k-slot pair
-                    // (TurboQuant: q' 2^-e), q' the scaled (rotated) query
+                    // (TurboQuant: q' 2^-e), q' the query (QuaRot: H q /
+                    // sqrt(128), TurboQuant: R q / sqrt(128))
   uint32_t qz[16];  // KIVI: fp16 q' 2^-e per k-slot pair (zero-point term)
   uint32_t vq[4];   // QuaRot/RTN: fp16 pair 2^vpos(i) of value slot i
   f4 corrK;         // QuaRot/RTN: -2^(b-1) sum_c 2^(kpos-24) qh (start value
                     // of the score accumulators; the same in all rows)
-  float cK;         // 2^(24+e) (codes as subnormals) or 2^e (TurboQuant)
-  float eK;         // KIVI: 2^e (the zero-point sum)
+  float cK;         // qscale 2^(24+e) (codes as subnormals) or qscale 2^e
+                    // (TurboQuant), qscale = scale * log2(e)
+  float eK;         // KIVI: qscale 2^e (the zero-point sum)
   uint32_t lutk[4]; // TurboQuant: fp16 centroid tables of the K and V widths
   uint32_t lutv[4]; //   (widths <= 4)
   lds_h* tabk;      // TurboQuant: fp16 centroids of the K and V widths in LDS
@@ -405,24 +413,35 @@ __device__ __forceinline__ void kpart(const SlotPtrs& sp, const LaneOps& lo, flo
     for (int i = 0; i < BK; ++i) kw[tile][i] = sp.kc[((16 * tile + lo.col) * 4 + r) * BK + i];
   f4 S0, S1;
   if constexpr (FAM == RQ_KIVI) {
-    // per-channel scales folded into the query; the zero points enter
-    // through their own chain X = sum_c z_c q'_c 2^-e, the same in all rows
+    // per-channel scales folded into the query as an exact fp16 pair
+    // hi + lo = q' s 2^-(kpos+e) (hi the rounded product, lo its rounding
+    // error), both against the same codes; the zero points enter through
+    // their own chain X = sum_c z_c q'_c 2^-e, the same in all rows
     f4 X = {0.f, 0.f, 0.f, 0.f};
     S0 = X;
     S1 = X;
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       const u4 s4 = sp.km[r * 8 + kb], z4 = sp.km[r * 8 + 4 + kb];
-      const h8 Bk = make_h8(pk_mul(lo.qh[4 * kb + 0], s4.x), pk_mul(lo.qh[4 * kb + 1], s4.y),
-                            pk_mul(lo.qh[4 * kb + 2], s4.z), pk_mul(lo.qh[4 * kb + 3], s4.w));
+      const uint32_t s[4] = {s4.x, s4.y, s4.z, s4.w};
+      uint32_t hi[4], lw[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        hi[i] = pk_mul(lo.qh[4 * kb + i], s[i]);
+        lw[i] = pk_fms(lo.qh[4 * kb + i], s[i], hi[i]);
+      }
+      const h8 Bhi = make_h8(hi[0], hi[1], hi[2], hi[3]);
+      const h8 Blo = make_h8(lw[0], lw[1], lw[2], lw[3]);
       X = mfma(u4_h8(z4), make_h8(lo.qz[4 * kb], lo.qz[4 * kb + 1], lo.qz[4 * kb + 2],
                                   lo.qz[4 * kb + 3]), X);
-      S0 = mfma(make_h8(kpair<BK>(kw[0], 4 * kb), kpair<BK>(kw[0], 4 * kb + 1),
-                        kpair<BK>(kw[0], 4 * kb + 2), kpair<BK>(kw[0], 4 * kb + 3)),
-                Bk, S0);
-      S1 = mfma(make_h8(kpair<BK>(kw[1], 4 * kb), kpair<BK>(kw[1], 4 * kb + 1),
-                        kpair<BK>(kw[1], 4 * kb + 2), kpair<BK>(kw[1], 4 * kb + 3)),
-                Bk, S1);
+      const h8 A0 = make_h8(kpair<BK>(kw[0], 4 * kb), kpair<BK>(kw[0], 4 * kb + 1),
+                            kpair<BK>(kw[0], 4 * kb + 2), kpair<BK>(kw[0], 4 * kb + 3));
+      const h8 A1 = make_h8(kpair<BK>(kw[1], 4 * kb), kpair<BK>(kw[1], 4 * kb + 1),
+                            kpair<BK>(kw[1], 4 * kb + 2), kpair<BK>(kw[1], 4 * kb + 3));
+      S0 = mfma(A0, Bhi, S0);
+      S1 = mfma(A1, Bhi, S1);
+      S0 = mfma(A0, Blo, S0);
+      S1 = mfma(A1, Blo, S1);
     }
     const float xx = __builtin_fmaf(X[0], lo.eK, -m_ref);
 #pragma unroll
@@ -784,9 +803,9 @@ __device__ __forceinline__ uint32_t claim_issue(uint32_t* ctr, int lane) {
 // The wave's blocks, up to `depth` (2 .. kMaxDepth) in flight in a ring of
 // slots of the block's exact size.  Its n_static statically assigned blocks
 // (blk0 + j stride into slot j) come first: the prologue issued the first
-// two, the others follow one per computed block, so that the ring fills
-// while the first blocks are computed rather than in one burst that would
-// hold the wave's issue behind full memory queues.  Then claimed blocks:
+// n_up (the whole ring: the first before the set-up, the others right after
+// it, so that memory stays busy while the first blocks are computed), any
+// others follow one per computed block.  Then claimed blocks:
 // each slot is refilled after it has been computed; the claim for the
 // block after that is issued just before the refill, so its result has a
 // whole block's time to come back.  `issued` counts this wave's
@@ -795,17 +814,20 @@ __device__ __forceinline__ uint32_t claim_issue(uint32_t* ctr, int lane) {
 // `depth` slots receive a static block, so blocks are always consumed in
 // ring order.
 template <int FAM, int NA, int BK, int BV>
-__device__ __forceinline__ void stream_blocks(const Geo& g, int depth, int n_static, int blk0,
-                                              int stride, Claims& cl, int issued,
+__device__ __forceinline__ void stream_blocks(const Geo& g, int depth, int n_static, int n_up,
+                                              int blk0, int stride, Claims& cl, int issued,
                                               uint8_t* slots, const LaneOps& lo,
                                               const uint32_t* cst, WaveState<NA>& ws) {
   using S = Slot<FAM, BK, BV>;
   static_assert(kMaxDepth == 4, "the ring below rotates four marks");
   // m0: `issued` just after the copies of the block in the current slot,
-  // m1.. those of the next slots in ring order
-  const int n0 = n_static < 2 ? n_static : 2;
+  // m1.. those of the next slots in ring order (the first n0 slots were
+  // issued back to back)
+  const int n0 = n_static < n_up ? n_static : n_up;
   int m0 = issued - (n0 - 1) * S::pieces;
-  int m1 = m0 + S::pieces, m2 = m1, m3 = m1;
+  int m1 = m0 + S::pieces;
+  int m2 = n0 > 2 ? m0 + 2 * S::pieces : m1;
+  int m3 = n0 > 3 ? m0 + 3 * S::pieces : m1;
   int inflight = n0;
   int ramp = n0;   // next static block (and slot), two ahead of the current
   int off = 0;
@@ -855,14 +877,14 @@ __device__ __forceinline__ void stream_blocks(const Geo& g, int depth, int n_sta
 // above MAXB are not instantiated.
 template <int FAM, int NA, int MAXB>
 __device__ __forceinline__ void dispatch(int bk, int bv, const Geo& g, int depth, int n_static,
-                                         int blk0, int stride, Claims& cl, int issued,
+                                         int n_up, int blk0, int stride, Claims& cl, int issued,
                                          uint8_t* slots, const LaneOps& lo, const uint32_t* cst,
                                          WaveState<NA>& ws) {
 #define RQ_CASE(K, V)                                                              \
   case (K - 1) * 8 + (V - 1):                                                      \
     if (K <= MAXB && V <= MAXB)                                                    \
       stream_blocks<FAM, NA, (K <= MAXB ? K : 1), (V <= MAXB ? V : 1)>(            \
-          g, depth, n_static, blk0, stride, cl, issued, slots, lo, cst, ws);       \
+          g, depth, n_static, n_up, blk0, stride, cl, issued, slots, lo, cst, ws); \
     break;
 #define RQ_ROW(K) RQ_CASE(K, 1) RQ_CASE(K, 2) RQ_CASE(K, 3) RQ_CASE(K, 4) \
                   RQ_CASE(K, 5) RQ_CASE(K, 6) RQ_CASE(K, 7) RQ_CASE(K, 8)
@@ -934,7 +956,7 @@ __device__ __forceinline__ void store_queries(const AttnLaunch& a, u4 piece, boo
   }
 }
 
-// TurboQuant: qs[j] = qscale R q_j / sqrt(128) for the G query rows, on the
+// TurboQuant: qs[j] = R q_j / sqrt(128) for the G query rows, on the
 // matrix cores: D[row][coord] = Q . R^T with the 16-bit query rows (qraw,
 // rows >= G unused) as A and rows of R (global memory, bf16; converted to
 // fp16 for fp16 queries) as B.  Wave w computes coordinate tiles 2w, 2w+1.
@@ -974,14 +996,14 @@ __device__ __forceinline__ void rotate_queries(const AttnLaunch& a, int h, const
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int j = 4 * g + i;
-      if (j < a.G) qs[j][16 * nt + r] = d[i] * (a.qscale * kInvSqrtD);
+      if (j < a.G) qs[j][16 * nt + r] = d[i] * kInvSqrtD;
     }
   }
   __syncthreads();
 }
 
 // Partial of (unit, slot): float [G][2 + 128] = (max, sum, acc[128]).
-// Slots of a unit: 0 .. n_wg-1 streaming, n_wg .. n_wg+n_rw-1 the window,
+// Slots of a unit: 0 .. nw-1 streaming, nw .. nw+n_rw-1 the window,
 // then the group partials of the two-level merge.
 __device__ __forceinline__ float* part_ptr(const AttnLaunch& a, size_t unit, int slot) {
   return a.part + (unit * a.pstride + slot) * (size_t)a.G * (2 + kD);
@@ -1112,7 +1134,7 @@ __device__ __forceinline__ void residual_slot(const AttnLaunch& a, int b, int h,
 // Quantized blocks of workgroup slot `slot` of unit (b, h): stream, merge the
 // four waves and write the slot's partial.
 template <int FAM, int NA, int MAXB>
-__device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h, int b,
+__device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int nw, int h, int b,
                                             float (*qs)[kD], uint16_t* qraw, uint32_t* cst,
                                             uint8_t* slots, float* merge) {
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid / kWave), lane = tid & (kWave - 1);
@@ -1142,9 +1164,9 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
   // the others while the first ones are computed.
   const int grp = slot / kGroup;
   const int gw0 = grp * kGroup;
-  const int gn = a.n_wg - gw0 < kGroup ? a.n_wg - gw0 : kGroup;
-  const int g_lo = (int)((long)nblk * gw0 / a.n_wg);
-  const int g_hi = (int)((long)nblk * (gw0 + gn) / a.n_wg);
+  const int gn = nw - gw0 < kGroup ? nw - gw0 : kGroup;
+  const int g_lo = (int)((long)nblk * gw0 / nw);
+  const int g_hi = (int)((long)nblk * (gw0 + gn) / nw);
   const int wk = (slot - gw0) * kWaves + wave, wstride = gn * kWaves;
   int n_static = 0;
   for (int j = 0; j < depth; ++j) n_static += g_lo + wk + j * wstride < g_hi ? 1 : 0;
@@ -1206,7 +1228,6 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
           qv[8 * c8 + 2 * e + 1] = widen(w[e] >> 16, a.is_bf16);
         }
       }
-      float f = a.qscale;
       // RTN runs this instantiation with codes in the original domain
       if (FAM == RQ_QUAROT && a.family == RQ_QUAROT) {
         // unnormalised Walsh-Hadamard transform of the row, stages of
@@ -1231,25 +1252,26 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
             qv[i] = upper ? o - qv[i] : qv[i] + o;
           }
         }
-        f *= kInvSqrtD;
-      }
 #pragma unroll
-      for (int i = 0; i < 32; ++i) qv[i] *= f;
+        for (int i = 0; i < 32; ++i) qv[i] *= kInvSqrtD;
+      }
     }
     // row exponent e: the row's largest |q'| is below 2^e (frexp), so every
-    // q' 2^-e lies in (-1, 1); 0 for a zero row
+    // q' 2^-e lies in (-1, 1); 0 for a zero row.  The softmax scale
+    // (scale * log2 e) is applied to the fp32 scores, so the operands of
+    // unrotated queries are the 16-bit inputs times powers of two, exact.
     float amax = 0.0f;
 #pragma unroll
     for (int i = 0; i < 32; ++i) amax = __builtin_fmaxf(amax, __builtin_fabsf(qv[i]));
     amax = __builtin_fmaxf(amax, xor_shfl(amax, 16));
     amax = __builtin_fmaxf(amax, xor_shfl(amax, 32));
     const int e = amax > 0.0f ? __builtin_amdgcn_frexp_expf(amax) : 0;
-    lo.cK = __builtin_ldexpf(1.0f, FAM == RQ_TURBO ? e : 24 + e);
-    lo.eK = __builtin_ldexpf(1.0f, e);
+    lo.cK = __builtin_ldexpf(a.qscale, FAM == RQ_TURBO ? e : 24 + e);
+    lo.eK = __builtin_ldexpf(a.qscale, e);
     // static QK operands: k-slot pair (kb, k') = channels 32r + 4kb + k'
     // and 32r + 16 + 4kb + k'
-    const int8_t* kp = kFieldPos.k[bk];
-    const int8_t* vp = kFieldPos.v[bv];
+    const int8_t* kp = a.fpos.k[bk];
+    const int8_t* vp = a.fpos.v[bv];
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
@@ -1284,7 +1306,8 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
       }
     }
   }
-  issued += issue_first(g, bk, bv, per_blk, 1, 2, g_lo + wk, wstride, g_hi, lane, my_slots);
+  // the rest of the ring, now that the set-up is done
+  issued += issue_first(g, bk, bv, per_blk, 1, depth, g_lo + wk, wstride, g_hi, lane, my_slots);
   WaveState<NA> ws;
 #pragma unroll
   for (int nt = 0; nt < 8; ++nt) ws.acc[nt] = (f4){0.f, 0.f, 0.f, 0.f};
@@ -1294,7 +1317,7 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
   ws.ev = 0;
   {
     // value slots' 2^-vpos (TurboQuant: 1), the exponent Ev = 0
-    const int8_t* vp = kFieldPos.v[bv];
+    const int8_t* vp = a.fpos.v[bv];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
       ws.wv[i] = h_pair((uint32_t)(15 - (FAM == RQ_TURBO ? 0 : vp[i])) << 10);
@@ -1303,8 +1326,8 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int h
   // blocks at normal priority; what comes before and after at raised
   // priority (see attn_kernel)
   __builtin_amdgcn_s_setprio(0);
-  dispatch<FAM, NA, MAXB>(bk, bv, g, depth, n_static, g_lo + wk, wstride, cl, issued, my_slots,
-                          lo, cst, ws);
+  dispatch<FAM, NA, MAXB>(bk, bv, g, depth, n_static, depth, g_lo + wk, wstride, cl, issued,
+                          my_slots, lo, cst, ws);
   __builtin_amdgcn_s_setprio(kSetupPrio);
 
   // ---- this wave's result per query row: (m, l, out[128]) in canonical form
@@ -1557,31 +1580,43 @@ attn_kernel(AttnLaunch a) {
   float* merge = reinterpret_cast<float*>(dyn);
   uint16_t* qraw = reinterpret_cast<uint16_t*>(slots + a.area_bytes);
   float (*qs)[kD] = reinterpret_cast<float (*)[kD]>(slots + a.area_bytes + a.G * kD * 2);
-  const int slot = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-  const size_t unit = (size_t)b * a.H + h;
+  // Flat grid, unit index fastest and skewed by one per slot: the nw
+  // workgroups of a unit are about n_units apart in dispatch order, so they
+  // land in every residency round of the CUs (the workgroups sharing a CU
+  // issue at different rates, the older first), and on different XCDs
+  // (workgroups go to the XCDs round-robin).  Block claims then balance
+  // each unit over fast and slow slots alike.
+  const int n_units = a.B * a.H;
+  const int slot = blockIdx.x / n_units;
+  const size_t unit = (blockIdx.x + slot) % n_units;
+  const int h = (int)(unit % a.H), b = (int)(unit / a.H);
+  // this unit's workgroups (its kv-head's share of the grid; slots beyond
+  // it have nothing to do)
+  const int nw = a.nwg[h];
+  const int nx = nw > 0 ? nw : 1;
+  if (slot >= nx) return;
   // Set-up, the window, the partial write and the merges run at a raised
   // wave priority: they share SIMDs with other workgroups' block loops, and
   // a unit finishes only after its slowest set-up and its merge, so they
   // go first; the block loops run at normal priority.
   __builtin_amdgcn_s_setprio(kSetupPrio);
   // The unit's nx workgroups: slot s first takes the 16-bit window chunks
-  // s, s + nx, .. (kResChunk tokens each, partial n_wg + chunk; the area is
+  // s, s + nx, .. (kResChunk tokens each, partial nw + chunk; the area is
   // their staging), then streams its share of the quantized blocks (slots
-  // 0 .. n_wg-1).  The window thus costs a few workgroups some of their
+  // 0 .. nw-1).  The window thus costs a few workgroups some of their
   // blocks (the claims hand those to the others) instead of holding
   // workgroups of its own.
-  const int nx = a.n_wg > 0 ? a.n_wg : 1;
   for (int c = slot; c < a.n_rw; c += nx) {
     const int t_lo = a.nq + c * kResChunk;
     const int t_hi = t_lo + kResChunk < a.n_tokens ? t_lo + kResChunk : a.n_tokens;
     residual_slot(a, b, h, reinterpret_cast<float (*)[kD]>(slots + kResLds),
-                  reinterpret_cast<uint16_t*>(slots), part_ptr(a, unit, a.n_wg + c), t_lo, t_hi);
+                  reinterpret_cast<uint16_t*>(slots), part_ptr(a, unit, nw + c), t_lo, t_hi);
     __syncthreads();   // the staging area is reused
   }
   // the block stream counts this wave's memory operations from zero: the
   // window's partial stores complete first
   if (slot < a.n_rw) wait_vm<0>();
-  if (slot < a.n_wg) stream_slot<FAM, NA, MAXB>(a, slot, h, b, qs, qraw, cst, slots, merge);
+  if (slot < nw) stream_slot<FAM, NA, MAXB>(a, slot, nw, h, b, qs, qraw, cst, slots, merge);
   // publish this workgroup's partials and take a ticket.  Up to kGroup
   // workgroups: the last to arrive merges every slot and the window.  More:
   // they report in groups of kGroup, the last of a group merges it into a
@@ -1589,29 +1624,29 @@ attn_kernel(AttnLaunch a) {
   // whose last arrival merges the group partials and the window.  Every
   // counter is left at zero for the next call.
   uint32_t* cnt = a.counters + unit * a.cstride;
-  const int ng = (a.n_wg + kGroup - 1) / kGroup;
+  const int ng = (nw + kGroup - 1) / kGroup;
   if (ng <= 1) {
     if (take_ticket(cnt) == (uint32_t)(nx - 1)) {
-      merge_slots(a, unit, merge, 0, a.n_wg, a.n_wg, a.n_rw, nullptr);
+      merge_slots(a, unit, merge, 0, nw, nw, a.n_rw, nullptr);
       reset_counter(cnt);
       reset_counter(cnt + a.claim_off);
     }
     return;
   }
   {
-    // two levels: every workgroup streams (nx = n_wg > kGroup)
+    // two levels: every workgroup streams (nx = nw > kGroup)
     const int g = slot / kGroup;
-    const int gsz = a.n_wg - g * kGroup < kGroup ? a.n_wg - g * kGroup : kGroup;
+    const int gsz = nw - g * kGroup < kGroup ? nw - g * kGroup : kGroup;
     if (take_ticket(cnt + 1 + g) != (uint32_t)(gsz - 1)) return;
     __syncthreads();   // the merge area is read until here
     merge_slots(a, unit, merge, g * kGroup, gsz, 0, 0,
-                part_ptr(a, unit, a.n_wg + a.n_rw + g));
+                part_ptr(a, unit, nw + a.n_rw + g));
     reset_counter(cnt + 1 + g);
     // every wave of the group has stopped claiming
     reset_counter(cnt + a.claim_off + 32 * g);
   }
   if (take_ticket(cnt) != (uint32_t)(ng - 1)) return;
-  merge_slots(a, unit, merge, a.n_wg + a.n_rw, ng, a.n_wg, a.n_rw, nullptr);
+  merge_slots(a, unit, merge, nw + a.n_rw, ng, nw, a.n_rw, nullptr);
   reset_counter(cnt);
 }
 
@@ -1624,9 +1659,11 @@ attn_kernel(AttnLaunch a) {
 #define RQ_DEFINE_ATTN_LAUNCHER(FAM, NA, MAXB, NAME)                            \
   namespace rq {                                                                \
   hipError_t NAME(const AttnLaunch& a, size_t lds, hipStream_t s) {             \
-    dim3 grid(a.n_wg > 0 ? a.n_wg : 1, a.H, a.B);                               \
+    AttnLaunch b = a;                                                           \
+    b.fpos = make_field_pos();                                                  \
+    dim3 grid((a.n_wg > 0 ? a.n_wg : 1) * a.H * a.B);                           \
     hipLaunchKernelGGL((attn_kernel<FAM, NA, MAXB>), grid, dim3(kThreads), lds, \
-                       s, a);                                                   \
+                       s, b);                                                   \
     return hipGetLastError();                                                   \
   }                                                                             \
   }

@@ -149,7 +149,10 @@ size_t lds_per_cu() {
 }
 
 struct SplitPlan {
-  int nq, n_wg, blk_per_wg, n_rw;
+  int nq, n_rw;
+  int n_wg;                          // the largest nwg (grid slots per unit)
+  int nwg[RQ_MAX_KV_HEADS];          // workgroups per unit of each kv-head
+  int pstride;                       // partial slots per unit
 };
 
 // LDS shape of the attention kernel for one layer: the most workgroups per
@@ -198,37 +201,42 @@ int cu_count() {
   return n;
 }
 
-// Workgroups (four waves each) per (batch, kv-head) unit.  The grid is sized
-// to one resident round with every CU busy: three workgroups per CU (the
-// attention kernel runs three waves per SIMD), split evenly over the units.
-// The 16-bit window is n_rw chunks of 32 tokens, taken by the unit's first
-// workgroups before their blocks.
-SplitPlan plan_splits(const rq_cache* c, int n_tokens, int wg_per_cu = 3) {
-  SplitPlan p;
-  p.nq = n_quantized(n_tokens, c->residual);
-  p.n_rw = (n_tokens - p.nq + rq::kAttnResChunk - 1) / rq::kAttnResChunk;
-  const long nblk = p.nq / rq::kChunk;
-  const long units = (long)c->batch * c->n_kv_heads;
-  long per = 0;
-  const char* env = std::getenv("RQ_ATTN_WG_BLOCKS");
-  if (env && std::atoi(env) > 0) {
-    per = std::atoi(env) < 4 ? 4 : std::atoi(env);
-  } else {
-    // one resident round
-    long target = (long)cu_count() * wg_per_cu / units;
-    if (target < 1) target = 1;
-    per = (nblk + target - 1) / target;
-    if (per < 4) per = 4;
-  }
-  p.blk_per_wg = (int)per;
-  p.n_wg = nblk == 0 ? 0 : (int)((nblk + per - 1) / per);
-  return p;
-}
-
-// Merge groups of a plan (the two-level merge starts above one group).
+// Merge groups of a unit's workgroups (the two-level merge starts above one
+// group).
 int merge_groups(int n_wg) {
   const int ng = (n_wg + rq::kAttnGroup - 1) / rq::kAttnGroup;
   return ng <= 1 ? 0 : ng;
+}
+
+// Workgroups (four waves each) per (batch, kv-head) unit.  The grid is sized
+// to one resident round with every CU busy (wg_per_cu workgroups per CU,
+// three when the LDS allows), split evenly over the units, at least 4
+// blocks per workgroup.  (Shares weighted by the cost of each kv-head's
+// widths were measured slower on MI355X: a unit's extra workgroups land in
+// the youngest residency slots, which issue last.)  The 16-bit window is
+// n_rw chunks of 32 tokens, taken by the unit's first workgroups before
+// their blocks.
+SplitPlan plan_splits(const rq_cache* c, int layer, int n_tokens, int wg_per_cu = 3) {
+  (void)layer;
+  SplitPlan p{};
+  p.nq = n_quantized(n_tokens, c->residual);
+  p.n_rw = (n_tokens - p.nq + rq::kAttnResChunk - 1) / rq::kAttnResChunk;
+  const long nblk = p.nq / rq::kChunk;
+  const int H = c->n_kv_heads;
+  const double budget = (double)cu_count() * wg_per_cu / ((double)c->batch * H);
+  const long most = (nblk + 3) / 4;   // at least 4 blocks per workgroup
+  p.n_wg = 0;
+  p.pstride = 1;
+  for (int h = 0; h < H; ++h) {
+    long n = nblk == 0 ? 0 : (long)budget;
+    if (nblk > 0 && n < 1) n = 1;
+    if (n > most) n = most;
+    p.nwg[h] = (int)n;
+    p.n_wg = p.nwg[h] > p.n_wg ? p.nwg[h] : p.n_wg;
+    const int ps = p.nwg[h] + p.n_rw + merge_groups(p.nwg[h]);
+    p.pstride = ps > p.pstride ? ps : p.pstride;
+  }
+  return p;
 }
 
 // Counters per unit, sized for the most workgroups any call on this cache
@@ -250,7 +258,7 @@ uint64_t attn_counter_bytes(const rq_cache* c) {
          256 * 256;
 }
 
-int part_stride(const SplitPlan& p) { return p.n_wg + p.n_rw + merge_groups(p.n_wg); }
+int part_stride(const SplitPlan& p) { return p.pstride; }
 
 uint64_t attn_ws_bytes(const rq_cache* c, const SplitPlan& p) {
   const uint64_t G = c->n_q_heads / c->n_kv_heads;
@@ -259,6 +267,84 @@ uint64_t attn_ws_bytes(const rq_cache* c, const SplitPlan& p) {
 }
 
 }  // namespace
+
+namespace rq {
+
+uint64_t decode_counter_bytes(const rq_cache* c) { return attn_counter_bytes(c); }
+
+rq_status decode_attention(const rq_cache* c, int32_t layer, int32_t n_tokens, const void* q,
+                           float* out, float scale, uint32_t* counters, uint64_t counter_cap,
+                           float* part, uint64_t part_cap, rq_stream stream) {
+  rq_status st = check_cache(c);
+  if (st != RQ_OK) return st;
+  if (layer < 0 || layer >= c->n_layers)
+    return fail(RQ_EINVAL, "layer %d out of range", layer);
+  if (n_tokens < 1 || n_tokens > c->capacity)
+    return fail(RQ_EINVAL, "n_tokens %d outside 1..%d", n_tokens, c->capacity);
+  if (!q || !out || !counters || !part || !c->codes || !c->meta || !c->resid)
+    return fail(RQ_EINVAL, "NULL device pointer");
+  if (!std::isfinite(scale)) return fail(RQ_EINVAL, "scale is not finite");
+  const rq::LayerTable tab = layer_table(c, layer);
+  int max_blk = 0;
+  for (int h = 0; h < c->n_kv_heads; ++h) {
+    const int bb = 512 * (tab.bits[h][0] + tab.bits[h][1]) + 2 * meta_per_block(c);
+    max_blk = bb > max_blk ? bb : max_blk;
+  }
+  AttnShape shape;
+  if (!attn_shape(c, max_blk, &shape))
+    return fail(RQ_EUNSUPPORTED,
+                "layer %d: two %d-byte blocks per wave do not fit the LDS of a CU "
+                "(K+V bit-widths of one kv-head are too wide)", layer, max_blk);
+  const SplitPlan p = plan_splits(c, layer, n_tokens, shape.wg_per_cu);
+  const uint64_t need_c = attn_counter_bytes(c);
+  const uint64_t need_p = attn_ws_bytes(c, p) - need_c;
+  if (counter_cap < need_c || part_cap < need_p)
+    return fail(RQ_ESMALLWS, "workspace: counters %llu of %llu bytes, partials %llu of %llu",
+                (unsigned long long)counter_cap, (unsigned long long)need_c,
+                (unsigned long long)part_cap, (unsigned long long)need_p);
+  const int G = c->n_q_heads / c->n_kv_heads;
+  rq::AttnLaunch a{};
+  a.q = static_cast<const uint16_t*>(q);
+  a.codes = static_cast<const uint8_t*>(c->codes);
+  a.meta = static_cast<const uint8_t*>(c->meta) + meta_layer_bytes(c) * layer;
+  a.resid = static_cast<const uint16_t*>(c->resid) + resid_layer_elems(c) * layer;
+  a.out = out;
+  a.counters = counters;
+  a.part = part;
+  a.pstride = part_stride(p);
+  a.cstride = counter_stride(c);
+  a.claim_off = claim_offset(c);
+  a.B = c->batch;
+  a.H = c->n_kv_heads;
+  a.G = G;
+  a.GP = 1;
+  while (a.GP < G) a.GP *= 2;
+  a.cap = c->capacity;
+  a.R = c->residual;
+  a.nq = p.nq;
+  a.n_tokens = n_tokens;
+  a.n_wg = p.n_wg;
+  for (int h = 0; h < c->n_kv_heads; ++h) a.nwg[h] = (uint16_t)p.nwg[h];
+  a.n_rw = p.n_rw;
+  a.is_bf16 = c->dtype == RQ_BF16;
+  a.family = c->family;
+  a.qscale = scale * 1.4426950408889634f;
+  if (c->family == RQ_TURBO) {
+    a.rot = static_cast<const uint16_t*>(c->rotation) +
+            (size_t)layer * c->n_kv_heads * rq::kD * rq::kD;
+    a.cb = c->codebook;
+  }
+  a.tab = tab;
+  a.wave_bytes = shape.wave_bytes;
+  a.area_bytes = (int)rq::attention_area_bytes(G, a.wave_bytes, c->family);
+  hipError_t e = rq::launch_attention(a, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "attention launch");
+  return ok();
+}
+
+rq_status set_error(rq_status code, const char* msg) { return fail(code, "%s", msg); }
+
+}  // namespace rq
 
 extern "C" {
 
@@ -354,7 +440,13 @@ rq_status rq_decode_workspace(const rq_cache* c, int32_t n_tokens,
   if (n_tokens < 1 || n_tokens > c->capacity)
     return fail(RQ_EINVAL, "n_tokens %d outside 1..%d", n_tokens, c->capacity);
   if (!bytes) return fail(RQ_EINVAL, "bytes is NULL");
-  *bytes = attn_ws_bytes(c, plan_splits(c, n_tokens));
+  // the largest over the layers (their kv-heads share the grid by cost)
+  uint64_t most = 0;
+  for (int l = 0; l < c->n_layers; ++l) {
+    const uint64_t b = attn_ws_bytes(c, plan_splits(c, l, n_tokens));
+    most = b > most ? b : most;
+  }
+  *bytes = most;
   return ok();
 }
 
@@ -364,67 +456,14 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
                               rq_stream stream) {
   rq_status st = check_cache(c);
   if (st != RQ_OK) return st;
-  if (layer < 0 || layer >= c->n_layers)
-    return fail(RQ_EINVAL, "layer %d out of range", layer);
-  if (n_tokens < 1 || n_tokens > c->capacity)
-    return fail(RQ_EINVAL, "n_tokens %d outside 1..%d", n_tokens, c->capacity);
-  if (!q || !out || !ws || !c->codes || !c->meta || !c->resid)
-    return fail(RQ_EINVAL, "NULL device pointer");
-  if (!std::isfinite(scale)) return fail(RQ_EINVAL, "scale is not finite");
-  const rq::LayerTable tab = layer_table(c, layer);
-  int max_blk = 0;
-  for (int h = 0; h < c->n_kv_heads; ++h) {
-    const int bb = 512 * (tab.bits[h][0] + tab.bits[h][1]) + 2 * meta_per_block(c);
-    max_blk = bb > max_blk ? bb : max_blk;
-  }
-  AttnShape shape;
-  if (!attn_shape(c, max_blk, &shape))
-    return fail(RQ_EUNSUPPORTED,
-                "layer %d: two %d-byte blocks per wave do not fit the LDS of a CU "
-                "(K+V bit-widths of one kv-head are too wide)", layer, max_blk);
-  const SplitPlan p = plan_splits(c, n_tokens, shape.wg_per_cu);
-  const uint64_t need = attn_ws_bytes(c, p);
-  if (ws_bytes < need)
+  if (!ws) return fail(RQ_EINVAL, "NULL workspace");
+  const uint64_t cb = attn_counter_bytes(c);
+  if (ws_bytes < cb)
     return fail(RQ_ESMALLWS, "workspace %llu bytes < %llu needed",
-                (unsigned long long)ws_bytes, (unsigned long long)need);
-  const int G = c->n_q_heads / c->n_kv_heads;
-  rq::AttnLaunch a{};
-  a.q = static_cast<const uint16_t*>(q);
-  a.codes = static_cast<const uint8_t*>(c->codes);
-  a.meta = static_cast<const uint8_t*>(c->meta) + meta_layer_bytes(c) * layer;
-  a.resid = static_cast<const uint16_t*>(c->resid) + resid_layer_elems(c) * layer;
-  a.out = out;
-  a.counters = static_cast<uint32_t*>(ws);
-  a.part = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + attn_counter_bytes(c));
-  a.pstride = part_stride(p);
-  a.cstride = counter_stride(c);
-  a.claim_off = claim_offset(c);
-  a.B = c->batch;
-  a.H = c->n_kv_heads;
-  a.G = G;
-  a.GP = 1;
-  while (a.GP < G) a.GP *= 2;
-  a.cap = c->capacity;
-  a.R = c->residual;
-  a.nq = p.nq;
-  a.n_tokens = n_tokens;
-  a.n_wg = p.n_wg;
-  a.n_rw = p.n_rw;
-  a.blk_per_wg = p.blk_per_wg;
-  a.is_bf16 = c->dtype == RQ_BF16;
-  a.family = c->family;
-  a.qscale = scale * 1.4426950408889634f;
-  if (c->family == RQ_TURBO) {
-    a.rot = static_cast<const uint16_t*>(c->rotation) +
-            (size_t)layer * c->n_kv_heads * rq::kD * rq::kD;
-    a.cb = c->codebook;
-  }
-  a.tab = tab;
-  a.wave_bytes = shape.wave_bytes;
-  a.area_bytes = (int)rq::attention_area_bytes(G, a.wave_bytes, c->family);
-  hipError_t e = rq::launch_attention(a, reinterpret_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return hip_fail(e, "attention launch");
-  return ok();
+                (unsigned long long)ws_bytes, (unsigned long long)cb);
+  return rq::decode_attention(c, layer, n_tokens, q, out, scale, static_cast<uint32_t*>(ws), cb,
+                              reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + cb),
+                              ws_bytes - cb, stream);
 }
 
 rq_status rq_calibrate_workspace(int32_t n_comp, int32_t n_tokens,

@@ -25,6 +25,14 @@ struct LayerTable {
   uint8_t bits[RQ_MAX_KV_HEADS][2];
 };
 
+// Field positions of the packed codes of every width (1..8) in the fp16
+// operands the attention kernel builds: key pair slot i (0..15) and value
+// slot i (0..3).  Filled by the attention launchers.
+struct FieldPosTab {
+  int8_t k[9][16];
+  int8_t v[9][4];
+};
+
 struct QuantLaunch {
   const uint16_t* k;      // [B][H][n_new][128]
   const uint16_t* v;
@@ -67,7 +75,8 @@ struct AttnLaunch {
   int B, H, G, cap, R;
   int GP;                 // smallest power of two >= G
   int nq, n_tokens;
-  int n_wg, blk_per_wg;   // workgroups per unit streaming blocks
+  int n_wg;               // grid slots per unit: the largest nwg[h]
+  uint16_t nwg[RQ_MAX_KV_HEADS];  // workgroups streaming blocks, per kv-head
   int n_rw;               // workgroups per unit on the 16-bit window
   int wave_bytes;         // LDS bytes of one wave's block ring
   int area_bytes;         // LDS bytes of the ring/merge/staging area
@@ -76,6 +85,7 @@ struct AttnLaunch {
   const uint16_t* rot;    // TurboQuant: this layer's rotations [H][128][128] bf16
   const float* cb;        // TurboQuant: codebook table (rq_turbo_codebook)
   LayerTable tab;
+  FieldPosTab fpos;
 };
 
 struct CalibLaunch {
@@ -112,5 +122,17 @@ struct SensLaunch {
   int n_seq, n_comp, T, chunks, dtype;
 };
 hipError_t launch_sensitivity(const SensLaunch& a, hipStream_t s);
+
+// Decode attention of one layer with the arrival counters (counter_cap
+// bytes, zero between calls) and the partial results (part_cap bytes) in
+// the given device buffers: the validation and launch shared by the entry
+// points with a caller's workspace and with the library's own scratch.
+rq_status decode_attention(const rq_cache* c, int32_t layer, int32_t n_tokens, const void* q,
+                           float* out, float scale, uint32_t* counters, uint64_t counter_cap,
+                           float* part, uint64_t part_cap, rq_stream stream);
+// Bytes of arrival counters a cache's calls use.
+uint64_t decode_counter_bytes(const rq_cache* c);
+// Record an error message for rq_last_error and return code.
+rq_status set_error(rq_status code, const char* msg);
 
 }  // namespace rq
