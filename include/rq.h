@@ -194,6 +194,23 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
                               float scale, void* ws, uint64_t ws_bytes,
                               rq_stream stream);
 
+/* For callers that cannot allocate device memory (code under stream
+ * capture, serving loops, harnesses that forbid allocation):
+ * rq_decode_attention with the workspace replaced by the library's own
+ * scratch, a static device array of rq_decode_static_bytes() bytes (8 MiB:
+ * 1 MiB of arrival counters, 7 MiB of partial results) that each GPU the
+ * library runs on holds until the process ends.  Same arguments, results
+ * and errors as rq_decode_attention otherwise; a call whose counters or
+ * partials exceed those sizes returns RQ_ESMALLWS.  The call allocates
+ * nothing.  Every call on one GPU shares that GPU's scratch: calls that
+ * overlap on one GPU (different streams, or host threads) race and must be
+ * serialized by the caller.  Asynchronous. */
+uint64_t rq_decode_static_bytes(void);
+rq_status rq_decode_attention_static(const rq_cache* c, int32_t layer,
+                                     int32_t n_tokens, const void* q,
+                                     float* out, float scale,
+                                     rq_stream stream);
+
 /* Measurement utility, not part of the method: reads `bytes` (a multiple of
  * 16) of the device buffer buf once with a plain streaming kernel of
  * n_blocks workgroups (1..65535) of 256 threads and writes one word per

@@ -26,7 +26,8 @@ EXPORTS = ("rq_version", "rq_last_error", "rq_cache_sizes", "rq_region_offset",
            "rq_calibrate_workspace", "rq_calibrate_distortion",
            "rq_fit_distortion", "rq_allocate_bits", "rq_turbo_codebook",
            "rq_sensitivity_workspace", "rq_sensitivity", "rq_cap_weights",
-           "rq_fallback_beta", "rq_read_probe")
+           "rq_fallback_beta", "rq_decode_static_bytes",
+           "rq_decode_attention_static", "rq_read_probe")
 RQ_TURBO_TABLE_FLOATS = 8 * 2 * 256
 
 
@@ -85,7 +86,10 @@ def lib():
             "rq_sensitivity": (i32, [i32, vp, i32, i32, i32, pd, vp, u64, vp]),
             "rq_cap_weights": (i32, [i32, pd, C.c_double]),
             "rq_fallback_beta": (i32, [i32, pd, pd, C.c_double]),
+            "rq_decode_static_bytes": (u64, []),
             "rq_read_probe": (i32, [vp, u64, vp, i32, vp]),
+            "rq_decode_attention_static": (i32, [pc, i32, i32, vp, vp,
+                                                 C.c_float, vp]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)
@@ -256,6 +260,18 @@ def rq_decode_attention(cache, layer, n_tokens, q, out, ws, scale=None,
         _tptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
+def rq_decode_attention_static(cache, layer, n_tokens, q, out, scale=None,
+                               stream=None):
+    """rq_decode_attention with the library's own scratch: allocates
+    nothing (for callers that cannot allocate)."""
+    if scale is None:
+        scale = 1.0 / np.sqrt(128.0)
+    _check_attention_args(cache, q, out)
+    _check(lib().rq_decode_attention_static(
+        C.byref(cache), layer, n_tokens, _tptr(q), _tptr(out), float(scale),
+        _stream(stream)))
+
+
 def rq_read_probe(buf, sink, n_blocks, stream=None):
     """Read the whole device tensor buf once (measurement utility); sink:
     device int32/uint32 tensor of n_blocks elements."""
@@ -389,4 +405,11 @@ class KVCache:
         n = self.n_tokens[layer]
         rq_decode_attention(self.desc, layer, n, q, out,
                             self.workspace(n, stream), scale, stream)
+        return out
+
+    def attention_static(self, layer, q, out, scale=None, stream=None):
+        """Decode attention through rq_decode_attention_static (the
+        library's own scratch; no allocation: out is the caller's)."""
+        rq_decode_attention_static(self.desc, layer, self.n_tokens[layer], q,
+                                   out, scale, stream)
         return out
