@@ -19,7 +19,8 @@
  *    a call that returns an error has written nothing.  rq_last_error()
  *    then describes the problem (thread-local, valid until the next call
  *    on the same thread).
- *  - head_dim is 128.  Bit-widths are 1..8 (QuaRot and RTN need >= 2).
+ *  - head_dim is 128.  Bit-widths are 1..8 (QuaRot and RTN need >= 2, and
+ *    so do the values of KIVI_RTN).
  *
  * Numeric formats (bit-exact contract shared with the test oracle)
  *  - K/V inputs are fp16 or bf16 (rq_dtype).  Metadata (scale, zero) is
@@ -37,6 +38,9 @@
  *      RTN    the QuaRot step on y = x itself (per-token symmetric
  *             round-to-nearest, no rotation; Appendix "RTN Base
  *             Quantizer").
+ *      KIVI_RTN  keys by KIVI, values by RTN: each side its own base
+ *             quantizer (the per-side treatment of Sec. 3.4, "K/V
+ *             separation").
  *      Turbo  n = fp16(fp32(|x|)) (sum of squares and root in fp64);
  *             y = R x, t = y * (sqrt(128) / n) (0 when n == 0); code =
  *             number of thresholds of the b-bit codebook below t.  y is
@@ -59,12 +63,15 @@
  *           K: [batch][token][chunk q: channels 32q..32q+31][b words]
  *           V: [batch][block of 32 tokens][channel][b words]  (a chunk is
  *              the 32 tokens of the block)
- *  meta   KIVI:   [l][h][kind][batch][block][4][s(32), z(32)] fp16, pair
- *                 order; K: group index = chunk q, entries = channels;
+ *  meta   [l][h][kind][batch][block][one block's metadata], a block of
+ *         kind K taking mK bytes and of kind V mV bytes:
+ *         KIVI-style (512 bytes): [4][s(32), z(32)] fp16, pair order;
+ *                 K: group index = chunk q, entries = channels;
  *                 V: group index = channel group cg, entries = tokens.
- *         QuaRot, RTN: [l][h][kind][batch][block][s(32 tokens)] fp16,
- *                 pair order.
- *         Turbo:  [l][h][kind][batch][block][n(32 tokens)] fp16, pair order.
+ *         per-token (64 bytes): [s(32 tokens)] fp16, pair order (QuaRot
+ *                 and RTN scales, Turbo norms).
+ *         KIVI: both sides KIVI-style; KIVI_RTN: K KIVI-style, V per-token;
+ *         QuaRot, RTN, Turbo: both sides per-token.
  *  resid  [l][batch][h][kind][R + 32][128] in the input dtype; token t of
  *         the 16-bit window lives in slot t mod (R + 32).
  *  Residual rule: with T tokens cached the quantized prefix is
@@ -92,6 +99,7 @@ typedef int32_t rq_status;
 #define RQ_QUAROT 1
 #define RQ_TURBO 2
 #define RQ_RTN 3
+#define RQ_KIVI_RTN 4         /* KIVI keys, RTN values (mixed families)     */
 
 #define RQ_F16 0
 #define RQ_BF16 1
@@ -110,7 +118,8 @@ typedef void* rq_stream;
  * "static lookup table", Appendix "Runtime Analysis"): host int8
  * [n_layers][n_kv_heads][2], K then V. */
 typedef struct rq_cache {
-  int32_t family;        /* RQ_KIVI, RQ_QUAROT, RQ_TURBO or RQ_RTN        */
+  int32_t family;        /* RQ_KIVI, RQ_QUAROT, RQ_TURBO, RQ_RTN or
+                            RQ_KIVI_RTN                                    */
   int32_t dtype;         /* RQ_F16 or RQ_BF16: K/V/q input type           */
   int32_t n_layers;
   int32_t batch;

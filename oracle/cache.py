@@ -19,12 +19,15 @@ see ``fmt`` for chunks and pair order):
            V: [channel group cg][s(32 tokens, pair order), z(...)]  fp16
   QuaRot meta, per block: [32 tokens, pair order] fp16 scale
   TurboQuant meta, per block: [32 tokens, pair order] fp16 norm
+  KIVI_RTN (the "mixed" family: KIVI's per-channel asymmetric keys with
+  RTN's per-token symmetric values, each side its own quantizer as the
+  paper's K/V separation allows, Sec. 3.4): K meta as KIVI, V meta as RTN
 """
 import numpy as np
 
 from . import fmt, quant
 
-KIVI, QUAROT, TURBO, RTN = 0, 1, 2, 3
+KIVI, QUAROT, TURBO, RTN, KIVI_RTN = 0, 1, 2, 3, 4
 
 
 def n_quantized(T, R):
@@ -112,6 +115,13 @@ class Unit:
             self.k_hat = quant.rtn_dequant(uk, sk, bk)
             self.v_hat = quant.rtn_dequant(uv, sv, bv)
             self.k_meta = token_meta(sk)
+            self.v_meta = token_meta(sv)
+        elif family == KIVI_RTN:
+            uk, sk, zk = quant.kivi_quant_keys(kq, bk)
+            uv, sv = quant.rtn_quant(vq, bv)
+            self.k_hat = quant.kivi_dequant_keys(uk, sk, zk)
+            self.v_hat = quant.rtn_dequant(uv, sv, bv)
+            self.k_meta = kivi_meta_keys(sk, zk)
             self.v_meta = token_meta(sv)
         elif family == TURBO:
             uk, nk, self.k_t = quant.turbo_quant(kq, rotation, bk)

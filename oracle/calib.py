@@ -12,10 +12,13 @@ import numpy as np
 
 from . import quant
 
-KIVI, QUAROT, TURBO, RTN = 0, 1, 2, 3
+KIVI, QUAROT, TURBO, RTN, KIVI_RTN = 0, 1, 2, 3, 4
 
 
 def roundtrip(family, x, b, is_value, rotation=None):
+    if family == KIVI_RTN:
+        # the mixed family: KIVI keys, RTN values
+        family = RTN if is_value else KIVI
     if family == KIVI:
         if is_value:
             u, s, z = quant.kivi_quant_values(x, b)

@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(HERE, "librq.so")
 
 RQ_OK, RQ_EINVAL, RQ_EINFEASIBLE, RQ_EUNSUPPORTED, RQ_EDEVICE, RQ_ESMALLWS = (
     0, -1, -2, -3, -4, -5)
-RQ_KIVI, RQ_QUAROT, RQ_TURBO, RQ_RTN = 0, 1, 2, 3
+RQ_KIVI, RQ_QUAROT, RQ_TURBO, RQ_RTN, RQ_KIVI_RTN = 0, 1, 2, 3, 4
 RQ_F16, RQ_BF16, RQ_F32 = 0, 1, 2
 RQ_MAX_KV_HEADS = 32
 

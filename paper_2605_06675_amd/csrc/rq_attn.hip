@@ -14,6 +14,8 @@ hipError_t launch_attn_quarot_b4(const AttnLaunch&, size_t, hipStream_t);
 hipError_t launch_attn_quarot_b8(const AttnLaunch&, size_t, hipStream_t);
 hipError_t launch_attn_turbo_b4(const AttnLaunch&, size_t, hipStream_t);
 hipError_t launch_attn_turbo_b8(const AttnLaunch&, size_t, hipStream_t);
+hipError_t launch_attn_kivirtn_b4(const AttnLaunch&, size_t, hipStream_t);
+hipError_t launch_attn_kivirtn_b8(const AttnLaunch&, size_t, hipStream_t);
 
 size_t attention_area_bytes(int G, int wave_bytes, int family) {
   const size_t merge = (size_t)kWaves * G * (2 + kD) * sizeof(float);
@@ -50,6 +52,8 @@ hipError_t launch_attention(const AttnLaunch& a, hipStream_t s) {
     e = (wide ? launch_attn_turbo_b8 : launch_attn_turbo_b4)(a, lds, s);
   else if (a.family == RQ_QUAROT || a.family == RQ_RTN)   // same kernel, no rotation
     e = (wide ? launch_attn_quarot_b8 : launch_attn_quarot_b4)(a, lds, s);
+  else if (a.family == RQ_KIVI_RTN)
+    e = (wide ? launch_attn_kivirtn_b8 : launch_attn_kivirtn_b4)(a, lds, s);
   else if (a.GP <= 4)
     e = (wide ? launch_attn_kivi_n1_b8 : launch_attn_kivi_n1_b4)(a, lds, s);
   else if (a.GP == 8)

@@ -356,6 +356,12 @@ __device__ __forceinline__ uint32_t tq_pair(const uint32_t* wds, int i, const ui
   else return tq_lds(tq_code2_pair<B>(wds, i), tab);
 }
 
+// Key-side and value-side paths of a family.  The mixed family (KIVI keys,
+// RTN values) takes the KIVI path for its keys and the per-token symmetric
+// path (the QuaRot instantiation, queries left unrotated) for its values.
+__host__ __device__ constexpr int key_fam(int f) { return f == RQ_KIVI_RTN ? RQ_KIVI : f; }
+__host__ __device__ constexpr int val_fam(int f) { return f == RQ_KIVI_RTN ? RQ_QUAROT : f; }
+
 // ------------------------------------------------------------ wave state
 template <int NA>
 struct WaveState {
@@ -637,16 +643,17 @@ __device__ __forceinline__ void block_rescale(const LaneOps& lo, float m_ref, fl
 template <int FAM, int NA, int BK, int BV>
 __device__ __forceinline__ void block_step(const uint8_t* slot, const LaneOps& lo,
                                            const uint32_t* cst, WaveState<NA>& ws) {
-  constexpr int MB = FAM == RQ_KIVI ? kMetaBlockKivi : kMetaBlockTok;
+  constexpr int KF = key_fam(FAM), VF = val_fam(FAM);
+  constexpr int MBK = meta_block_bytes(FAM, 0);
   SlotPtrs sp;
   sp.kc = reinterpret_cast<const uint32_t*>(slot);
   sp.vc = reinterpret_cast<const uint32_t*>(slot + 512 * BK);
   sp.km = reinterpret_cast<const u4*>(slot + 512 * (BK + BV));
-  sp.vm = reinterpret_cast<const u4*>(slot + 512 * (BK + BV) + MB);
+  sp.vm = reinterpret_cast<const u4*>(slot + 512 * (BK + BV) + MBK);
   const float m_ref = ws.m_run == -INFINITY ? 0.0f : ws.m_run;
   f4 t0, t1;
-  kpart<FAM, BK>(sp, lo, m_ref, t0, t1);
-  const VScales<FAM, NA> vs = load_vscales<FAM, NA>(sp, lo);
+  kpart<KF, BK>(sp, lo, m_ref, t0, t1);
+  const VScales<VF, NA> vs = load_vscales<VF, NA>(sp, lo);
   // keep the phases apart: hoisting all LDS reads of the block to its top
   // needs more registers than the waves per SIMD allow
   __builtin_amdgcn_sched_barrier(0);
@@ -654,12 +661,12 @@ __device__ __forceinline__ void block_step(const uint8_t* slot, const LaneOps& l
   mx = max3(mx, t1[1], t0[2]);
   mx = max3(mx, t1[2], t0[3]);
   mx = max3(mx, t1[3], t1[3]);
-  const us2 smax = vscale_max<FAM, NA>(vs);
+  const us2 smax = vscale_max<VF, NA>(vs);
   const uint32_t thr = (kVScaleMax + ((uint32_t)ws.ev << 10)) * 0x00010001u;
   const bool big = __builtin_bit_cast(uint32_t, __builtin_elementwise_max(
                        smax, __builtin_bit_cast(us2, thr))) != thr;
   if (__builtin_amdgcn_ballot_w64(!(mx <= kLazy) || ws.m_run == -INFINITY || big))
-    block_rescale<FAM, NA, BV>(lo, m_ref, mx, smax, t0, t1, ws);
+    block_rescale<VF, NA, BV>(lo, m_ref, mx, smax, t0, t1, ws);
   uint32_t P[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -668,11 +675,12 @@ __device__ __forceinline__ void block_step(const uint8_t* slot, const LaneOps& l
     P[i] = as_u32(pv);
   }
   __builtin_amdgcn_sched_barrier(0);
-  vpart<FAM, NA, BV>(sp, lo, P, vs, cst, ws);
+  vpart<VF, NA, BV>(sp, lo, P, vs, cst, ws);
 }
 
 // A block's data is four contiguous byte ranges: K codes (512*BK), V codes
-// (512*BV), K metadata and V metadata (MB bytes each).  A wave copies it
+// (512*BV), K metadata and V metadata (the family's metadata bytes of a
+// block of each kind).  A wave copies it
 // straight from global memory into one of its LDS slots with
 // global_load_lds_dwordx4: piece k of lane l covers bytes [16 l + 1024 k,
 // +16) of the concatenation, so every instruction moves 1 KB of contiguous
@@ -680,8 +688,9 @@ __device__ __forceinline__ void block_step(const uint8_t* slot, const LaneOps& l
 template <int FAM, int BK, int BV> struct Slot {
   static constexpr int kb = 512 * BK;
   static constexpr int vb = 512 * BV;
-  static constexpr int mb = FAM == RQ_KIVI ? kMetaBlockKivi : kMetaBlockTok;
-  static constexpr int bytes = kb + vb + 2 * mb;
+  static constexpr int kmb = meta_block_bytes(FAM, 0);
+  static constexpr int vmb = meta_block_bytes(FAM, 1);
+  static constexpr int bytes = kb + vb + kmb + vmb;
   static constexpr int pieces = (bytes + 1023) / 1024;
 };
 
@@ -709,8 +718,8 @@ __device__ __forceinline__ void issue_block(const Geo& g, int blk, int lane, uin
       const uint8_t* src;
       if (o < S::kb) src = g.kreg + (size_t)blk * S::kb + o;
       else if (o < S::kb + S::vb) src = g.vreg + (size_t)blk * S::vb + (o - S::kb);
-      else if (o < S::kb + S::vb + S::mb) src = g.kmeta + (size_t)blk * S::mb + (o - S::kb - S::vb);
-      else src = g.vmeta + (size_t)blk * S::mb + (o - S::kb - S::vb - S::mb);
+      else if (o < S::kb + S::vb + S::kmb) src = g.kmeta + (size_t)blk * S::kmb + (o - S::kb - S::vb);
+      else src = g.vmeta + (size_t)blk * S::vmb + (o - S::kb - S::vb - S::kmb);
       __builtin_amdgcn_global_load_lds(src, (lds_void*)(slot + 1024 * k), 16, 0, kStreamPolicy);
     }
   }
@@ -730,10 +739,10 @@ __device__ __forceinline__ void wait_vm() {
 // Static blocks j0 .. j1-1 of a wave's ring (block blk0 + j stride, below
 // nblk, into slot j at j * bytes; bytes and pieces as in Slot<>, at run
 // time).  Returns the copy instructions issued.
-__device__ __forceinline__ int issue_first(const Geo& g, int bk, int bv, int mb, int j0, int j1,
-                                           int blk0, int stride, int nblk, int lane,
+__device__ __forceinline__ int issue_first(const Geo& g, int bk, int bv, int mk, int mv, int j0,
+                                           int j1, int blk0, int stride, int nblk, int lane,
                                            uint8_t* slots) {
-  const int kb = 512 * bk, vb = 512 * bv, bytes = kb + vb + 2 * mb;
+  const int kb = 512 * bk, vb = 512 * bv, bytes = kb + vb + mk + mv;
   const int pieces = (bytes + 1023) / 1024;
   int issued = 0;
   for (int j = j0; j < j1; ++j) {
@@ -747,8 +756,8 @@ __device__ __forceinline__ int issue_first(const Geo& g, int bk, int bv, int mb,
         const uint8_t* src;
         if (o < kb) src = g.kreg + (size_t)blk * kb + o;
         else if (o < kb + vb) src = g.vreg + (size_t)blk * vb + (o - kb);
-        else if (o < kb + vb + mb) src = g.kmeta + (size_t)blk * mb + (o - kb - vb);
-        else src = g.vmeta + (size_t)blk * mb + (o - kb - vb - mb);
+        else if (o < kb + vb + mk) src = g.kmeta + (size_t)blk * mk + (o - kb - vb);
+        else src = g.vmeta + (size_t)blk * mv + (o - kb - vb - mk);
         __builtin_amdgcn_global_load_lds(src, (lds_void*)(slot + 1024 * k), 16, 0, kStreamPolicy);
       }
     }
@@ -1142,15 +1151,15 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int n
   const int G = a.G;
   const int bk = a.tab.bits[h][0], bv = a.tab.bits[h][1];
   const int nblk_cap = a.cap / kChunk;
-  const int per_blk = FAM == RQ_KIVI ? kMetaBlockKivi : kMetaBlockTok;
+  constexpr int mk = meta_block_bytes(FAM, 0), mv = meta_block_bytes(FAM, 1);
   Geo g;
   g.kreg = a.codes + a.tab.code_off[h][0] + (size_t)b * a.cap * 16 * bk;
   g.vreg = a.codes + a.tab.code_off[h][1] + (size_t)b * a.cap * 16 * bv;
-  g.kmeta = a.meta + (((size_t)h * 2 + 0) * a.B + b) * nblk_cap * per_blk;
-  g.vmeta = a.meta + (((size_t)h * 2 + 1) * a.B + b) * nblk_cap * per_blk;
+  g.kmeta = a.meta + meta_unit_offset(FAM, h, 0, b, a.B, nblk_cap);
+  g.vmeta = a.meta + meta_unit_offset(FAM, h, 1, b, a.B, nblk_cap);
   const int nblk = a.nq / kChunk;
   // this unit's ring: as many whole blocks as the wave's region holds
-  const int blk_bytes = 512 * (bk + bv) + 2 * per_blk;
+  const int blk_bytes = 512 * (bk + bv) + mk + mv;
   int depth = a.wave_bytes / blk_bytes;
   depth = depth < kMaxDepth ? depth : kMaxDepth;
   uint8_t* my_slots = slots + (size_t)wave * a.wave_bytes;
@@ -1182,7 +1191,7 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int n
     cl.pending = claim_issue(cl.ctr, lane);
     issued += 1;
   }
-  const int nb_ops = issue_first(g, bk, bv, per_blk, 0, 1, g_lo + wk, wstride, g_hi, lane,
+  const int nb_ops = issue_first(g, bk, bv, mk, mv, 0, 1, g_lo + wk, wstride, g_hi, lane,
                                  my_slots);
   if (nq_ops) wait_vm_rt(issued + nb_ops);
   issued += nb_ops;
@@ -1290,7 +1299,7 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int n
       tq_make_lut(a.cb, bk, lo.lutk);
       tq_make_lut(a.cb, bv, lo.lutv);
     }
-    if (FAM == RQ_QUAROT) {
+    if (key_fam(FAM) == RQ_QUAROT) {
       // the symmetric offset of the key codes, -2^(b-1) at the codes'
       // weights 2^(kpos-24) (exact subnormals), against the query operands
 #pragma unroll
@@ -1307,7 +1316,7 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int n
     }
   }
   // the rest of the ring, now that the set-up is done
-  issued += issue_first(g, bk, bv, per_blk, 1, depth, g_lo + wk, wstride, g_hi, lane, my_slots);
+  issued += issue_first(g, bk, bv, mk, mv, 1, depth, g_lo + wk, wstride, g_hi, lane, my_slots);
   WaveState<NA> ws;
 #pragma unroll
   for (int nt = 0; nt < 8; ++nt) ws.acc[nt] = (f4){0.f, 0.f, 0.f, 0.f};
@@ -1338,7 +1347,7 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int n
   for (int i = 0; i < 4; ++i) {
 #pragma unroll
     for (int gg = 0; gg < 4; ++gg) zt[gg][i] = __shfl(ws.corrZ[i], r * 16 + gg, kWave);
-    lrow[i] = __shfl(ws.corrZ[i], r * 16 + (FAM == RQ_KIVI ? 4 : 0), kWave);
+    lrow[i] = __shfl(ws.corrZ[i], r * 16 + (val_fam(FAM) == RQ_KIVI ? 4 : 0), kWave);
   }
   float mrow[4];
 #pragma unroll
@@ -1346,8 +1355,9 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int n
   // scale of the value sums: 2^(24+Ev) for codes as subnormals (QuaRot and
   // RTN: 2^Ev times 2^24 acc minus the offset 2^(b-1) corrO), 2^Ev / sqrt(128)
   // for TurboQuant
-  const float cv = FAM == RQ_TURBO ? __builtin_ldexpf(kInvSqrtD, ws.ev)
-                                   : __builtin_ldexpf(1.0f, FAM == RQ_QUAROT ? ws.ev : 24 + ws.ev);
+  constexpr int VF = val_fam(FAM);
+  const float cv = VF == RQ_TURBO ? __builtin_ldexpf(kInvSqrtD, ws.ev)
+                                  : __builtin_ldexpf(1.0f, VF == RQ_QUAROT ? ws.ev : 24 + ws.ev);
   const float voff = (float)(1 << (bv - 1));
   __syncthreads();   // every wave is done with its slot
   float* mw = merge + (size_t)wave * G * (2 + kD);
@@ -1355,7 +1365,7 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int n
   for (int i = 0; i < 4; ++i) {
     const int row = 4 * r + i, jj = row & (GP - 1), gs = row / GP;
     if (jj < G) {
-      if (FAM == RQ_KIVI) {
+      if (VF == RQ_KIVI) {
 #pragma unroll
         for (int nt = 0; nt < 8; ++nt) {
           const int gt = nt / 2;
@@ -1370,7 +1380,7 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int n
 #pragma unroll
         for (int nt = 0; nt < 8; ++nt) {
           float v;
-          if (FAM == RQ_QUAROT)
+          if (VF == RQ_QUAROT)
             v = __builtin_fmaf(ws.acc[nt][i], 16777216.0f, -voff * ws.corrO[i]) * cv;
           else
             v = ws.acc[nt][i] * cv;
@@ -1480,7 +1490,7 @@ __device__ __forceinline__ void merge_rows(const AttnLaunch& a, size_t unit, flo
   }
   float* out = a.out + unit * G * kD + (size_t)j * kD + c0;   // (b, h) -> rows h*G..
   const float inv = own ? 1.0f / den : 0.0f;
-  if (a.family == RQ_KIVI || a.family == RQ_RTN) {
+  if (a.family == RQ_KIVI || a.family == RQ_RTN || a.family == RQ_KIVI_RTN) {
     if (own)
 #pragma unroll
       for (int k = 0; k < E; ++k) out[k] = (num[k] + tail[k]) * inv;

@@ -37,14 +37,15 @@ int n_quantized(int T, int R) {
   return x <= 0 ? 0 : (x / rq::kChunk) * rq::kChunk;
 }
 
-int meta_per_block(const rq_cache* c) {
-  return c->family == RQ_KIVI ? rq::kMetaBlockKivi : rq::kMetaBlockTok;
+// metadata bytes of one block of K plus one of V
+int meta_pair_bytes(const rq_cache* c) {
+  return rq::meta_block_bytes(c->family, 0) + rq::meta_block_bytes(c->family, 1);
 }
 
 rq_status check_cache(const rq_cache* c) {
   if (!c) return fail(RQ_EINVAL, "cache descriptor is NULL");
   if (c->family != RQ_KIVI && c->family != RQ_QUAROT && c->family != RQ_TURBO &&
-      c->family != RQ_RTN)
+      c->family != RQ_RTN && c->family != RQ_KIVI_RTN)
     return fail(RQ_EINVAL, "unknown family %d", c->family);
   if (c->family == RQ_TURBO && (!c->rotation || !c->codebook))
     return fail(RQ_EINVAL, "TurboQuant needs the rotation and codebook pointers");
@@ -67,9 +68,13 @@ rq_status check_cache(const rq_cache* c) {
                 c->capacity);
   if (c->residual < 0) return fail(RQ_EINVAL, "residual window must be >= 0");
   if (!c->bits) return fail(RQ_EINVAL, "bit table is NULL");
-  const int lo = (c->family == RQ_QUAROT || c->family == RQ_RTN) ? 2 : 1;
   for (int i = 0; i < c->n_layers * c->n_kv_heads * 2; ++i) {
     const int b = c->bits[i];
+    // symmetric quantizers need two bits or more: QuaRot and RTN on both
+    // sides, the values (odd entries) of KIVI_RTN
+    const bool sym = c->family == RQ_QUAROT || c->family == RQ_RTN ||
+                     (c->family == RQ_KIVI_RTN && (i & 1));
+    const int lo = sym ? 2 : 1;
     if (b < lo || b > 8)
       return fail(RQ_EINVAL, "bit table entry %d is %d (allowed %d..8)", i, b, lo);
   }
@@ -92,8 +97,8 @@ uint64_t region_offset(const rq_cache* c, int layer, int head, int kind) {
 }
 
 uint64_t meta_layer_bytes(const rq_cache* c) {
-  return (uint64_t)c->n_kv_heads * 2 * c->batch * (c->capacity / rq::kChunk) *
-         meta_per_block(c);
+  return (uint64_t)c->n_kv_heads * c->batch * (c->capacity / rq::kChunk) *
+         meta_pair_bytes(c);
 }
 
 uint64_t resid_layer_elems(const rq_cache* c) {
@@ -287,7 +292,7 @@ rq_status decode_attention(const rq_cache* c, int32_t layer, int32_t n_tokens, c
   const rq::LayerTable tab = layer_table(c, layer);
   int max_blk = 0;
   for (int h = 0; h < c->n_kv_heads; ++h) {
-    const int bb = 512 * (tab.bits[h][0] + tab.bits[h][1]) + 2 * meta_per_block(c);
+    const int bb = 512 * (tab.bits[h][0] + tab.bits[h][1]) + meta_pair_bytes(c);
     max_blk = bb > max_blk ? bb : max_blk;
   }
   AttnShape shape;
@@ -485,8 +490,10 @@ rq_status rq_calibrate_distortion(int32_t family, int32_t dtype, const void* x,
                                   double* beta, double* r2, void* ws,
                                   uint64_t ws_bytes, rq_stream stream) {
   if (family != RQ_KIVI && family != RQ_QUAROT && family != RQ_TURBO &&
-      family != RQ_RTN)
+      family != RQ_RTN && family != RQ_KIVI_RTN)
     return fail(RQ_EINVAL, "unknown family %d", family);
+  // the mixed family sweeps its keys as KIVI and its values as RTN
+  if (family == RQ_KIVI_RTN) family = is_value ? RQ_RTN : RQ_KIVI;
   if (family == RQ_TURBO && (!rotation || !codebook))
     return fail(RQ_EINVAL, "TurboQuant needs the rotation and codebook pointers");
   if (dtype != RQ_F16 && dtype != RQ_BF16)

@@ -12,6 +12,21 @@ constexpr int kD = 128;          // head_dim
 constexpr int kChunk = 32;       // codes per packed chunk = tokens per block
 constexpr int kMetaBlockKivi = 512;   // bytes of KIVI metadata per block
 constexpr int kMetaBlockTok = 64;     // bytes of per-token metadata per block
+
+// Metadata bytes of one block of kind (0 = K, 1 = V) in a family.
+__host__ __device__ constexpr int meta_block_bytes(int family, int kind) {
+  return (family == RQ_KIVI || (family == RQ_KIVI_RTN && kind == 0)) ? kMetaBlockKivi
+                                                                     : kMetaBlockTok;
+}
+// Byte offset, inside one layer's metadata, of block 0 of unit (h, kind, b):
+// [h][kind][batch][block], a K block taking meta_block_bytes(family, 0)
+// bytes and a V block meta_block_bytes(family, 1).
+__host__ __device__ inline size_t meta_unit_offset(int family, int h, int kind, int b, int B,
+                                                   int nblk_cap) {
+  const size_t mk = meta_block_bytes(family, 0), mv = meta_block_bytes(family, 1);
+  return (size_t)h * B * nblk_cap * (mk + mv) + (size_t)kind * B * nblk_cap * mk +
+         (size_t)b * nblk_cap * (kind ? mv : mk);
+}
 constexpr int kAttnGroup = 16;        // streaming slots per merge group
 constexpr int kAttnResChunk = 32;     // window tokens per window workgroup
 constexpr int kAttnMaxDepth = 4;      // most blocks in flight per attention wave
@@ -41,6 +56,7 @@ struct QuantLaunch {
   uint16_t* resid;        // start of this layer's residual rings
   int B, H, n_new, n_past, cap, R;
   int blk0, nblk;         // blocks [blk0, blk0 + nblk) get quantized
+  int kind_lo, kind_n;    // kinds kind_lo .. kind_lo + kind_n - 1 (K = 0, V = 1)
   int is_bf16;
   int family;
   int n_cu;               // compute units of the device (grid sizing)

@@ -162,8 +162,8 @@ __device__ __forceinline__ BlockId block_id(const QuantLaunch& a, int it) {
   const int r = it / a.nblk;
   id.h = r % a.H;
   const int z = r / a.H;
-  id.b = z >> 1;
-  id.kind = z & 1;
+  id.b = z / a.kind_n;
+  id.kind = a.kind_lo + z % a.kind_n;
   return id;
 }
 
@@ -204,8 +204,8 @@ __device__ __forceinline__ void store_meta(const QuantLaunch& a, const KiviSmem&
   typedef uint32_t u2 __attribute__((ext_vector_type(2)));
   const int nblk_cap = a.cap / kChunk;
   RQ_GLOBAL u2* m = gptr(reinterpret_cast<u2*>(
-      a.meta + ((((size_t)id.h * 2 + id.kind) * a.B + id.b) * nblk_cap + id.blk) *
-                   kMetaBlockKivi));
+      a.meta + meta_unit_offset(a.family, id.h, id.kind, id.b, a.B, nblk_cap) +
+      (size_t)id.blk * kMetaBlockKivi));
   m[lane] = reinterpret_cast<const u2*>(sm.meta)[lane];
 }
 
@@ -381,7 +381,7 @@ kivi_quant_kernel(QuantLaunch a) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & (kWave - 1);
   KiviSmem& sm = smem[wave];
-  const int total = a.nblk * a.H * a.B * 2;
+  const int total = a.nblk * a.H * a.B * a.kind_n;
   const int stride = gridDim.x * kQWaves;
   int it = blockIdx.x * kQWaves + wave;
   if (it >= total) return;
@@ -551,7 +551,7 @@ sym_quant_kernel(QuantLaunch a) {
   __shared__ Smem sm;
   const int blk = a.blk0 + blockIdx.x;
   const int h = blockIdx.y;
-  const int b = blockIdx.z >> 1, kind = blockIdx.z & 1;
+  const int b = blockIdx.z / a.kind_n, kind = a.kind_lo + blockIdx.z % a.kind_n;
   const int lane = threadIdx.x;
   switch (a.tab.bits[h][kind]) {
     case 2: sym_block<ROT, BF16, 2>(a, sm, b, h, kind, blk, lane); break;
@@ -565,8 +565,8 @@ sym_quant_kernel(QuantLaunch a) {
   __syncthreads();
   // metadata of this block
   const int nblk_cap = a.cap / kChunk;
-  uint8_t* m = a.meta +
-               ((((size_t)h * 2 + kind) * a.B + b) * nblk_cap + blk) * kMetaBlockTok;
+  uint8_t* m = a.meta + meta_unit_offset(a.family, h, kind, b, a.B, nblk_cap) +
+               (size_t)blk * kMetaBlockTok;
   const uint32_t* src = reinterpret_cast<const uint32_t*>(sm.meta);
   if (lane < kMetaBlockTok / 4) reinterpret_cast<uint32_t*>(m)[lane] = src[lane];
 }
@@ -585,46 +585,66 @@ ring_kernel(RingLaunch a) {
   dst[threadIdx.x] = src[threadIdx.x];
 }
 
+// KIVI blocks of kinds q.kind_lo .. + q.kind_n - 1
+hipError_t launch_kivi(const QuantLaunch& q, hipStream_t s) {
+  int maxb = 1;
+  for (int h = 0; h < q.H; ++h)
+    for (int k = q.kind_lo; k < q.kind_lo + q.kind_n; ++k)
+      maxb = q.tab.bits[h][k] > maxb ? q.tab.bits[h][k] : maxb;
+  // persistent: as many workgroups of kQWaves waves as fit on the device
+  const long waves = (long)q.nblk * q.H * q.B * q.kind_n;
+  long wg = (waves + kQWaves - 1) / kQWaves;
+  const long cap = (long)(q.n_cu > 0 ? q.n_cu : 256) * quant_occupancy(maxb);
+  if (wg > cap) wg = cap;
+  dim3 grid((unsigned)wg), block(kQWaves * kWave);
+  if (maxb <= 4) {
+    if (q.is_bf16)
+      hipLaunchKernelGGL((kivi_quant_kernel<1, 4>), grid, block, 0, s, q);
+    else
+      hipLaunchKernelGGL((kivi_quant_kernel<0, 4>), grid, block, 0, s, q);
+  } else {
+    if (q.is_bf16)
+      hipLaunchKernelGGL((kivi_quant_kernel<1, 8>), grid, block, 0, s, q);
+    else
+      hipLaunchKernelGGL((kivi_quant_kernel<0, 8>), grid, block, 0, s, q);
+  }
+  return hipGetLastError();
+}
+
+// per-token symmetric blocks (QuaRot with the rotation, RTN without) of
+// kinds q.kind_lo .. + q.kind_n - 1
+hipError_t launch_sym(const QuantLaunch& q, bool rot, hipStream_t s) {
+  dim3 grid(q.nblk, q.H, q.B * q.kind_n);
+  // bit-widths of the symmetric quantizers are 2..8 (checked on the host)
+  if (rot && q.is_bf16)
+    hipLaunchKernelGGL((sym_quant_kernel<1, 1>), grid, dim3(kWave), 0, s, q);
+  else if (rot)
+    hipLaunchKernelGGL((sym_quant_kernel<1, 0>), grid, dim3(kWave), 0, s, q);
+  else if (q.is_bf16)
+    hipLaunchKernelGGL((sym_quant_kernel<0, 1>), grid, dim3(kWave), 0, s, q);
+  else
+    hipLaunchKernelGGL((sym_quant_kernel<0, 0>), grid, dim3(kWave), 0, s, q);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_quantize(const QuantLaunch& a, hipStream_t s) {
   if (a.nblk <= 0) return hipSuccess;
-  if (a.family == RQ_TURBO) return launch_quantize_turbo(a, s);
-  if (a.family == RQ_KIVI) {
-    int maxb = 1;
-    for (int h = 0; h < a.H; ++h)
-      for (int k = 0; k < 2; ++k) maxb = a.tab.bits[h][k] > maxb ? a.tab.bits[h][k] : maxb;
-    // persistent: as many workgroups of kQWaves waves as fit on the device
-    const long waves = (long)a.nblk * a.H * a.B * 2;
-    long wg = (waves + kQWaves - 1) / kQWaves;
-    const long cap = (long)(a.n_cu > 0 ? a.n_cu : 256) * quant_occupancy(maxb);
-    if (wg > cap) wg = cap;
-    dim3 grid((unsigned)wg), block(kQWaves * kWave);
-    if (maxb <= 4) {
-      if (a.is_bf16)
-        hipLaunchKernelGGL((kivi_quant_kernel<1, 4>), grid, block, 0, s, a);
-      else
-        hipLaunchKernelGGL((kivi_quant_kernel<0, 4>), grid, block, 0, s, a);
-    } else {
-      if (a.is_bf16)
-        hipLaunchKernelGGL((kivi_quant_kernel<1, 8>), grid, block, 0, s, a);
-      else
-        hipLaunchKernelGGL((kivi_quant_kernel<0, 8>), grid, block, 0, s, a);
-    }
-  } else {
-    dim3 grid(a.nblk, a.H, a.B * 2);
-    // bit-widths of the symmetric families are 2..8 (checked on the host)
-    const bool rot = a.family == RQ_QUAROT;
-    if (rot && a.is_bf16)
-      hipLaunchKernelGGL((sym_quant_kernel<1, 1>), grid, dim3(kWave), 0, s, a);
-    else if (rot)
-      hipLaunchKernelGGL((sym_quant_kernel<1, 0>), grid, dim3(kWave), 0, s, a);
-    else if (a.is_bf16)
-      hipLaunchKernelGGL((sym_quant_kernel<0, 1>), grid, dim3(kWave), 0, s, a);
-    else
-      hipLaunchKernelGGL((sym_quant_kernel<0, 0>), grid, dim3(kWave), 0, s, a);
+  QuantLaunch q = a;
+  q.kind_lo = 0;
+  q.kind_n = 2;
+  if (a.family == RQ_TURBO) return launch_quantize_turbo(q, s);
+  if (a.family == RQ_KIVI) return launch_kivi(q, s);
+  if (a.family == RQ_KIVI_RTN) {
+    // keys by KIVI, values by RTN
+    q.kind_n = 1;
+    hipError_t e = launch_kivi(q, s);
+    if (e != hipSuccess) return e;
+    q.kind_lo = 1;
+    return launch_sym(q, false, s);
   }
-  return hipGetLastError();
+  return launch_sym(q, a.family == RQ_QUAROT, s);
 }
 
 hipError_t launch_ring(const RingLaunch& a, hipStream_t s) {

@@ -7,7 +7,7 @@ import numpy as np
 import workloads
 from oracle import cache as ocache
 
-KIVI, QUAROT, TURBO, RTN = 0, 1, 2, 3
+KIVI, QUAROT, TURBO, RTN, KIVI_RTN = 0, 1, 2, 3, 4
 
 
 def dev(bits16, dtype, device="cuda"):
@@ -30,7 +30,9 @@ class Layout:
         self.family, self.L, self.B, self.H = family, n_layers, batch, H
         self.cap, self.R = cap, R
         self.bits = np.asarray(bits).reshape(n_layers, H, 2)
-        self.per_blk = 512 if family == KIVI else 64
+        # metadata bytes per block of each kind (KIVI-style 512, per-token 64)
+        self.mb = (512 if family in (KIVI, KIVI_RTN) else 64,
+                   512 if family == KIVI else 64)
 
     def region_off(self, l, h, kind):
         flat = self.bits.reshape(-1)
@@ -51,10 +53,12 @@ class Layout:
 
     def meta(self, meta_u8, l, b, h, kind, n_blk):
         nblk_cap = self.cap // 32
-        layer = self.H * 2 * self.B * nblk_cap * self.per_blk
-        base = l * layer + (((h * 2 + kind) * self.B + b) * nblk_cap) * self.per_blk
-        raw = meta_u8[base: base + n_blk * self.per_blk].view(np.float16)
-        if self.family == KIVI:
+        mk, mv = self.mb
+        layer = self.H * self.B * nblk_cap * (mk + mv)
+        base = (l * layer + h * self.B * nblk_cap * (mk + mv) + kind * self.B * nblk_cap * mk
+                + b * nblk_cap * self.mb[kind])
+        raw = meta_u8[base: base + n_blk * self.mb[kind]].view(np.float16)
+        if self.mb[kind] == 512:
             return raw.reshape(n_blk, 4, 2, 32)
         return raw.reshape(n_blk, 32)
 

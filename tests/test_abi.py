@@ -153,6 +153,13 @@ def test_descriptor_validation():
     r = rq.rq_cache_sizes(rq.make_cache(**dict(good, family=rq.RQ_RTN)))
     q = rq.rq_cache_sizes(rq.make_cache(**dict(good, family=rq.RQ_QUAROT)))
     assert r == q
+    # the mixed family: 512 metadata bytes per key block, 64 per value block
+    m = rq.rq_cache_sizes(rq.make_cache(**dict(good, family=rq.RQ_KIVI_RTN)))
+    k = rq.rq_cache_sizes(rq.make_cache(**good))
+    assert m[0] == k[0] and m[2] == k[2]
+    assert m[1] == 8 * 1 * (1024 // 32) * (512 + 64)
+    rq.rq_cache_sizes(rq.make_cache(**dict(
+        good, family=rq.RQ_KIVI_RTN, bits=np.array([[[1, 2]] * 8]))))
     cases = [
         (dict(capacity=1000), rq.RQ_EINVAL),
         (dict(n_q_heads=30), rq.RQ_EINVAL),
@@ -161,7 +168,9 @@ def test_descriptor_validation():
         (dict(bits=np.full((1, 8, 2), 0)), rq.RQ_EINVAL),
         (dict(family=rq.RQ_QUAROT, bits=np.full((1, 8, 2), 1)), rq.RQ_EINVAL),
         (dict(family=rq.RQ_RTN, bits=np.full((1, 8, 2), 1)), rq.RQ_EINVAL),
-        (dict(family=4), rq.RQ_EINVAL),
+        (dict(family=rq.RQ_KIVI_RTN, bits=np.array([[[2, 1]] * 8])),
+         rq.RQ_EINVAL),
+        (dict(family=5), rq.RQ_EINVAL),
         (dict(family=rq.RQ_TURBO), rq.RQ_EINVAL),   # no rotation/codebook
         (dict(dtype=7), rq.RQ_EINVAL),
         (dict(n_kv_heads=33, n_q_heads=66, bits=np.full((1, 33, 2), 2)),

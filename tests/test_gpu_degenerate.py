@@ -53,8 +53,9 @@ def _fill(family, dtype, bits, kf, vf, rotation=None):
 @pytest.mark.parametrize("family,bits", [
     (workloads.KIVI, [[1, 4], [2, 3], [3, 2], [8, 1]]),
     (workloads.QUAROT, [[2, 4], [3, 3], [4, 2], [8, 5]]),
-    (workloads.RTN, [[2, 4], [3, 3], [4, 2], [8, 5]])],
-    ids=["kivi", "quarot", "rtn"])
+    (workloads.RTN, [[2, 4], [3, 3], [4, 2], [8, 5]]),
+    (workloads.KIVI_RTN, [[1, 4], [2, 3], [3, 2], [8, 2]])],
+    ids=["kivi", "quarot", "rtn", "kivi_rtn"])
 @pytest.mark.parametrize("dtype", [workloads.F16, workloads.BF16])
 def test_degenerate_affine_families(family, bits, dtype):
     print(f"degenerate family {family} dtype {dtype}", flush=True)
@@ -65,7 +66,8 @@ def test_degenerate_affine_families(family, bits, dtype):
 
 
 @pytest.mark.parametrize("family", [workloads.KIVI, workloads.QUAROT,
-                                    workloads.RTN], ids=["kivi", "quarot", "rtn"])
+                                    workloads.RTN, workloads.KIVI_RTN],
+                         ids=["kivi", "quarot", "rtn", "kivi_rtn"])
 def test_saturated_metadata_bf16(family):
     # |x| up to ~1e7: scales and zero points saturate at the fp16 maximum
     print(f"saturated metadata family {family}", flush=True)
@@ -77,7 +79,8 @@ def test_saturated_metadata_bf16(family):
 
 @pytest.mark.parametrize("q_mult", [1.0e6, 1.0e-6], ids=["q1e6", "q1e-6"])
 @pytest.mark.parametrize("family", [workloads.KIVI, workloads.QUAROT,
-                                    workloads.RTN], ids=["kivi", "quarot", "rtn"])
+                                    workloads.RTN, workloads.KIVI_RTN],
+                         ids=["kivi", "quarot", "rtn", "kivi_rtn"])
 def test_large_values_and_queries(family, q_mult):
     # value scales near the fp16 maximum (probability x scale beyond the
     # fp16 range) and queries whose scaled elements leave it (q1e6) or

@@ -227,6 +227,24 @@ def test_kivi_two_level_merge_long_context(G):
     assert worst < ATOL
 
 
+@pytest.mark.parametrize("family,G", [(workloads.KIVI, 1), (workloads.KIVI, 3),
+                                      (workloads.KIVI, 6), (workloads.QUAROT, 3),
+                                      (workloads.RTN, 6)])
+def test_group_sizes_not_power_of_two(family, G):
+    """Query heads per kv-head that leave replicas of the query rows unused
+    (3 of 4, 6 of 8) or a single row; 1100 tokens so several streaming
+    workgroups merge.  KIVI's value side takes one (G <= 4) or two (G = 6)
+    A operands."""
+    lo = 1 if family == workloads.KIVI else 2
+    bits = np.array([[[lo, 3], [4, lo], [3, 4]]])
+    print(f"group size {G} family {family}", flush=True)
+    kvc, ks, vs, _ = _build(family, workloads.BF16, 3, G, 1100, 32, bits,
+                            batch=2)
+    units = _check_cache(family, workloads.BF16, kvc, ks, vs, bits, 32, 2, 3,
+                         1100)
+    _check_attention(kvc, units, workloads.BF16, 2, 3, G)
+
+
 def test_short_context_window_only():
     # fewer tokens than the window: nothing quantized, attention is exact
     bits = np.array([[[2, 2], [3, 3]]])

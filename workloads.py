@@ -29,7 +29,7 @@ import numpy as np
 HEAD_DIM = 128
 SEEDS = (42, 123, 2026)
 
-KIVI, QUAROT, TURBO, RTN = 0, 1, 2, 3
+KIVI, QUAROT, TURBO, RTN, KIVI_RTN = 0, 1, 2, 3, 4
 F16, BF16 = 0, 1
 
 
@@ -86,9 +86,15 @@ LLAMA3_70B = Workload("llama3-70b-kv-b4-t32768-turbo-3b", TURBO, BF16, 80, 4,
 # bits {1..4} at 2.0 average.
 QWEN3_32B = Workload("qwen3-32b-kv-b1-t131072-kivi-2b", KIVI, BF16, 64, 1, 8,
                      64, 131072, 128, (1, 2, 3, 4), 2.0, 0.81, (17.87, 4.65))
+# Llama-3-8B shaped KV with a base quantizer per side (K/V separation,
+# Sec. 3.4): KIVI keys, RTN per-token values, bits {2,3,4} at 3.0 average
+# (RTN needs two bits or more, so the set starts at 2 for both sides).
+LLAMA3_8B_MIXED = Workload("llama3-8b-kv-b16-t8192-kivi-rtn-3b", KIVI_RTN,
+                           BF16, 32, 16, 8, 32, 8192, 32, (2, 3, 4), 3.0, 0.5,
+                           (1.0, 1.0))
 
 WORKLOADS = {w.name: w for w in (SMALL, LLAMA3_8B, QWEN3_8B, LLAMA3_70B,
-                                 QWEN3_32B, QWEN3_8B_RTN)}
+                                 QWEN3_32B, QWEN3_8B_RTN, LLAMA3_8B_MIXED)}
 
 
 def _rng(seed, *stream):
