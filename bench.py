@@ -59,8 +59,13 @@ def parse():
     return p.parse_args()
 
 
-def meta_per_block(family):
-    return 512 if family == 0 else 64
+def meta_pair_bytes(family):
+    """Metadata bytes of one 32-token block of K plus one of V: 512 for a
+    KIVI-style side (scale and zero point per group), 64 for a per-token
+    side (one fp16 scale or norm per token)."""
+    k = 512 if family in (0, 4) else 64
+    v = 512 if family == 0 else 64
+    return k + v
 
 
 def n_quantized(T, R):
@@ -75,7 +80,7 @@ def attention_bytes(wl, bits_table, T):
     total = 0
     for l in range(bits_table.shape[0]):
         codes = sum(B * nq * 128 * int(b) // 8 for b in bits_table[l].reshape(-1))
-        meta = B * H * 2 * (nq // 32) * meta_per_block(wl.family)
+        meta = B * H * (nq // 32) * meta_pair_bytes(wl.family)
         resid = B * H * 2 * (T - nq) * 128 * 2
         qo = B * Hq * 128 * (2 + 4)
         total += codes + meta + resid + qo
@@ -91,60 +96,68 @@ def quantize_bytes(wl, bits_table, T):
     for l in range(bits_table.shape[0]):
         rd = 2 * B * H * T * 128 * 2
         codes = sum(B * nq * 128 * int(b) // 8 for b in bits_table[l].reshape(-1))
-        meta = B * H * 2 * (nq // 32) * meta_per_block(wl.family)
+        meta = B * H * (nq // 32) * meta_pair_bytes(wl.family)
         win = B * H * 2 * (T - nq) * 128 * 2
         total += rd + codes + meta + win
     return total
 
 
-def _oracle_unit(job):
-    """One (layer, batch entry, kv-head) unit through the oracle: quantize +
-    pack (its cache builder), then unpack + dequantize + fp64 decode
-    attention from the packed codes.  Returns (quantize s, attention s,
-    algorithmic attention bytes)."""
+def _oracle_units(job):
+    """The kv-heads of one (layer, batch entry) through the oracle, one unit
+    at a time: quantize + pack (its cache builder), then unpack + dequantize
+    + fp64 decode attention from the packed codes.  Inputs are generated
+    first and not timed.  Returns [(quantize s, attention s, algorithmic
+    attention bytes)] and the process id."""
     import workloads
     from oracle import attention as oatt
     from oracle import cache as ocache
     from oracle import fmt
     from oracle import quant as oq
-    wname, l, b, h, bk, bv = job
+    wname, l, b, heads = job
     wl = workloads.WORKLOADS[wname]
     T, R, G = wl.context, wl.residual, wl.group
     nq = n_quantized(T, R)
-    mb = meta_per_block(wl.family)
+    mb = meta_pair_bytes(wl.family)
     q16 = workloads.q_cpu(wl, l)
     k16, v16 = workloads.kv_cpu(wl, l, b, T)
-    k = workloads.u16_to_f32(k16[h], wl.dtype)
-    v = workloads.u16_to_f32(v16[h], wl.dtype)
-    q = workloads.u16_to_f32(q16[b, h * G:(h + 1) * G], wl.dtype)
-    rot = None
-    if wl.family == workloads.TURBO:
-        rot = workloads.u16_to_f32(workloads.turbo_rotation(42, l, h),
-                                   workloads.BF16).astype(np.float64)
-    t0 = time.perf_counter()
-    u = ocache.Unit(wl.family, k, v, bk, bv, R, rotation=rot)
-    t1 = time.perf_counter()
-    kc = ocache.unpack_keys(u.k_words, bk)
-    vc = ocache.unpack_values(u.v_words, bv)
-    if wl.family == workloads.KIVI:
-        kh = oq.kivi_dequant_keys(kc, *_kivi_meta_keys(u.k_meta))
-        vh = oq.kivi_dequant_values(vc, *_kivi_meta_values(u.v_meta))
-    else:
-        nk = fmt.from_pair_order(u.k_meta).reshape(-1)
-        nv = fmt.from_pair_order(u.v_meta).reshape(-1)
-        if wl.family == workloads.QUAROT:
-            kh, vh = oq.quarot_dequant(kc, nk, bk), oq.quarot_dequant(vc, nv, bv)
-        elif wl.family == workloads.RTN:
-            kh, vh = oq.rtn_dequant(kc, nk, bk), oq.rtn_dequant(vc, nv, bv)
+    out = []
+    for h, bk, bv in heads:
+        k = workloads.u16_to_f32(k16[h], wl.dtype)
+        v = workloads.u16_to_f32(v16[h], wl.dtype)
+        q = workloads.u16_to_f32(q16[b, h * G:(h + 1) * G], wl.dtype)
+        rot = None
+        if wl.family == workloads.TURBO:
+            rot = workloads.u16_to_f32(workloads.turbo_rotation(42, l, h),
+                                       workloads.BF16).astype(np.float64)
+        t0 = time.perf_counter()
+        u = ocache.Unit(wl.family, k, v, bk, bv, R, rotation=rot)
+        t1 = time.perf_counter()
+        kc = ocache.unpack_keys(u.k_words, bk)
+        vc = ocache.unpack_values(u.v_words, bv)
+        if wl.family == workloads.KIVI:
+            kh = oq.kivi_dequant_keys(kc, *_kivi_meta_keys(u.k_meta))
+            vh = oq.kivi_dequant_values(vc, *_kivi_meta_values(u.v_meta))
+        elif wl.family == workloads.KIVI_RTN:
+            kh = oq.kivi_dequant_keys(kc, *_kivi_meta_keys(u.k_meta))
+            nv = fmt.from_pair_order(u.v_meta).reshape(-1)
+            vh = oq.rtn_dequant(vc, nv, bv)
         else:
-            kh = oq.turbo_dequant(kc, nk, rot, bk)
-            vh = oq.turbo_dequant(vc, nv, rot, bv)
-    oatt.decode_attention(q, np.concatenate([kh, u.k_res]),
-                          np.concatenate([vh, u.v_res]))
-    t2 = time.perf_counter()
-    nbytes = (nq * 128 * (bk + bv) // 8 + 2 * (nq // 32) * mb
-              + 2 * (T - nq) * 256 + G * 128 * 6)
-    return t1 - t0, t2 - t1, nbytes
+            nk = fmt.from_pair_order(u.k_meta).reshape(-1)
+            nv = fmt.from_pair_order(u.v_meta).reshape(-1)
+            if wl.family == workloads.QUAROT:
+                kh, vh = oq.quarot_dequant(kc, nk, bk), oq.quarot_dequant(vc, nv, bv)
+            elif wl.family == workloads.RTN:
+                kh, vh = oq.rtn_dequant(kc, nk, bk), oq.rtn_dequant(vc, nv, bv)
+            else:
+                kh = oq.turbo_dequant(kc, nk, rot, bk)
+                vh = oq.turbo_dequant(vc, nv, rot, bv)
+        oatt.decode_attention(q, np.concatenate([kh, u.k_res]),
+                              np.concatenate([vh, u.v_res]))
+        t2 = time.perf_counter()
+        nbytes = (nq * 128 * (bk + bv) // 8 + (nq // 32) * mb
+                  + 2 * (T - nq) * 256 + G * 128 * 6)
+        out.append((t1 - t0, t2 - t1, nbytes))
+    return out, os.getpid()
 
 
 def _pool_init():
@@ -156,36 +169,30 @@ def _pool_init():
 def _cpu_jobs(wl, bits_table):
     for l in range(wl.n_layers):
         for b in range(wl.batch):
-            for h in range(wl.n_kv_heads):
-                yield (wl.name, l, b, h, int(bits_table[l, h, 0]),
-                       int(bits_table[l, h, 1]))
+            yield (wl.name, l, b, [(h, int(bits_table[l, h, 0]), int(bits_table[l, h, 1]))
+                                   for h in range(wl.n_kv_heads)])
 
 
-def _cpu_rates(res, wall, wl):
-    """Attention GB/s and whole-model quantize tok/s of a finished sample;
-    with wall set, rates over the wall time of all processes together."""
-    tq = sum(r[0] for r in res)
-    ta = sum(r[1] for r in res)
+def _cpu_rates(res, busy, wl):
+    """Attention GB/s and whole-model quantize tok/s: the sample's bytes
+    and tokens over the oracle time of the busiest process (busy: its
+    (quantize s, attention s); the sums themselves on one core)."""
     nb = sum(r[2] for r in res)
-    units = len(res)
-    if wall:
-        # each process spends its time in proportion: split the wall time
-        ta_w, tq_w = wall * ta / (ta + tq), wall * tq / (ta + tq)
-    else:
-        ta_w, tq_w = ta, tq
-    tok = units * wl.context / (wl.n_layers * wl.n_kv_heads)
-    return nb / ta_w / 1e9, tok / tq_w, tq, ta
+    tok = len(res) * wl.context / (wl.n_layers * wl.n_kv_heads)
+    return nb / busy[1] / 1e9, tok / busy[0]
 
 
 def cpu_baseline(wl, bits_table, seconds, workers):
     """The oracle (numpy), as it stands, on bounded samples of the same
     workload: whole (layer, batch entry, kv-head) units, first on one core
-    (units run one after another until the budget is spent), then on every
-    allowed core (one process per core, each single-threaded, for about the
-    same wall time).  Runs before the GPU is touched, so the worker
-    processes are plain forks.  Reports the attention rate in the metric's
-    unit (algorithmic bytes / oracle attention time) and the quantize rate
-    in whole-model tokens per second."""
+    (one (layer, batch) row of units after another until about `seconds`
+    of oracle time), then on every allowed core (one single-threaded
+    process per core, the sample about `seconds` per process).  Only the
+    oracle's work is timed, not the input generation.  Runs before the GPU
+    is touched, so the worker processes are plain forks.  Reports the
+    attention rate in the metric's unit (algorithmic bytes / oracle
+    attention time) and the quantize rate in whole-model tokens per
+    second."""
     import multiprocessing as mp
     import platform
     from threadpoolctl import threadpool_limits
@@ -201,36 +208,44 @@ def cpu_baseline(wl, bits_table, seconds, workers):
         pass
     allowed = len(os.sched_getaffinity(0))
     n = workers or min(16, allowed)
-    jobs = _cpu_jobs(wl, bits_table)
-    one = []
-    t0 = time.perf_counter()
+    one, spent = [], 0.0
     with threadpool_limits(limits=1):
-        for job in jobs:
-            one.append(_oracle_unit(job))
-            if time.perf_counter() - t0 >= seconds:
+        for job in _cpu_jobs(wl, bits_table):
+            res, _ = _oracle_units(job)
+            one += res
+            spent = sum(r[0] + r[1] for r in one)
+            if spent >= seconds:
                 break
-    a1, q1, tq1, ta1 = _cpu_rates(one, 0.0, wl)
-    # all cores: about `seconds` of wall time
-    per_unit = (time.perf_counter() - t0) / len(one)
-    n_units = max(n, int(seconds / per_unit) * n)
-    batch = [j for _, j in zip(range(n_units), _cpu_jobs(wl, bits_table))]
+    tq1, ta1 = sum(r[0] for r in one), sum(r[1] for r in one)
+    a1, q1 = _cpu_rates(one, (tq1, ta1), wl)
+    # all cores: about `seconds` of oracle work per process
+    per_row = spent / (len(one) / wl.n_kv_heads)
+    rows = max(n, int(round(seconds / per_row)) * n)
+    batch = [j for _, j in zip(range(rows), _cpu_jobs(wl, bits_table))]
     ctx = mp.get_context("fork")
     t1 = time.perf_counter()
     with ctx.Pool(n, initializer=_pool_init) as pool:
-        many = pool.map(_oracle_unit, batch, chunksize=1)
+        outs = pool.map(_oracle_units, batch, chunksize=1)
     wall = time.perf_counter() - t1
-    an, qn, tqn, tan = _cpu_rates(many, wall, wl)
-    return {"value": round(an, 4), "unit": "GB/s", "cores": n, "kind": "oracle",
-            "quantize_tok_s": round(qn, 1),
+    many = [r for res, _ in outs for r in res]
+    per_pid = {}
+    for res, pid in outs:
+        q, a = per_pid.get(pid, (0.0, 0.0))
+        per_pid[pid] = (q + sum(r[0] for r in res), a + sum(r[1] for r in res))
+    busy = (max(v[0] for v in per_pid.values()), max(v[1] for v in per_pid.values()))
+    an, qn = _cpu_rates(many, busy, wl)
+    return {"value": round(an, 4), "unit": "GB/s", "cores": len(per_pid),
+            "kind": "oracle", "quantize_tok_s": round(qn, 1),
             "single_core": {"value": round(a1, 4), "unit": "GB/s",
                             "quantize_tok_s": round(q1, 1), "units": len(one),
-                            "seconds": round(tq1 + ta1, 2)},
+                            "oracle_seconds": round(tq1 + ta1, 2)},
             "cpu_model": model, "nproc": os.cpu_count(), "allowed_cpus": allowed,
             "sample": f"{len(many)} (layer, batch, kv-head) units of "
-                      f"{wl.context} tokens on {n} processes ({wall:.1f} s wall; "
-                      f"single core: {len(one)} units, {tq1 + ta1:.1f} s): oracle "
-                      f"quantize + pack, then unpack + dequantize + fp64 decode "
-                      f"attention"}
+                      f"{wl.context} tokens on {len(per_pid)} processes (busiest "
+                      f"process {busy[0] + busy[1]:.1f} s of oracle time, {wall:.1f} s "
+                      f"wall with input generation); single core: {len(one)} units, "
+                      f"{tq1 + ta1:.1f} s: oracle quantize + pack, then unpack + "
+                      f"dequantize + fp64 decode attention"}
 
 
 def _kivi_meta_keys(m):
@@ -248,10 +263,13 @@ def _kivi_meta_values(m):
     return s, z
 
 
+# the mixed family quantizes its keys and its values with two kernels
 QUANT_KERNEL = {0: "kivi_quant_kernel", 1: "sym_quant_kernel",
-                2: "turbo_quant_kernel", 3: "sym_quant_kernel"}
+                2: "turbo_quant_kernel", 3: "sym_quant_kernel",
+                4: "kivi_quant_kernel+sym_quant_kernel"}
 KERNEL_SOURCES = {"kivi_quant_kernel": ["rq_quant.hip"],
                   "sym_quant_kernel": ["rq_quant.hip"],
+                  "kivi_quant_kernel+sym_quant_kernel": ["rq_quant.hip"],
                   "turbo_quant_kernel": ["rq_quant_turbo.hip"],
                   "attn_kernel": ["rq_attn*.hip", "rq_attn_impl.h"]}
 
@@ -575,7 +593,8 @@ def main():
                    "kv_heads": H, "q_heads": Hq, "head_dim": 128,
                    "context": T, "decode_steps": nsteps,
                    "residual_window": wl.residual,
-                   "family": ["kivi", "quarot", "turbo", "rtn"][wl.family],
+                   "family": ["kivi", "quarot", "turbo", "rtn",
+                              "kivi_rtn"][wl.family],
                    "avg_bits": wl.avg_bits, "bit_set": list(wl.bit_set),
                    "attention_bytes_per_step": att_bytes,
                    "quantize_bytes_per_step": q_bytes,
