@@ -157,7 +157,10 @@ int32_t rq_version(void);
 const char* rq_last_error(void);
 
 /* Validate a descriptor (device pointers may be NULL here) and report the
- * buffer sizes in bytes.  Any output pointer may be NULL.  Host only. */
+ * buffer sizes in bytes of the mixed-bit cache: codes at each kv-head's
+ * own K and V widths (the per-head bit table, Sec. 3.3; memory as in
+ * Appendix "Runtime Analysis"), metadata per the family, and the 16-bit
+ * window.  Any output pointer may be NULL.  Host only. */
 rq_status rq_cache_sizes(const rq_cache* c, uint64_t* codes_bytes,
                          uint64_t* meta_bytes, uint64_t* resid_bytes);
 
@@ -180,24 +183,36 @@ rq_status rq_quantize_kv(const rq_cache* c, int32_t layer, int32_t n_past,
                          rq_stream stream);
 
 /* Workspace bytes rq_decode_attention needs for n_tokens cached tokens
- * (it varies with n_tokens; size for the largest call, or re-query). */
+ * (it varies with n_tokens; size for the largest call, or re-query): the
+ * per-(batch, kv-head) counters and the partial results of the split
+ * decode of Appendix "Runtime Analysis" (the lookup-and-dequantize path).
+ * Host only. */
 rq_status rq_decode_workspace(const rq_cache* c, int32_t n_tokens,
                               uint64_t* bytes);
 
 /* Decode attention of one new query per sequence over the n_tokens cached
- * tokens of one layer (1 <= n_tokens <= capacity):
+ * tokens of one layer (1 <= n_tokens <= capacity), the inference path of
+ * Appendix "Runtime Analysis" (each kv-head's blocks dequantized at its own
+ * widths from the bit table, Sec. 3.3; the base quantizers of Sec. 3.4 /
+ * Appendix "Quantizer Implementation"):
  *   out[b][j] = softmax(scale * q[b][j] . K_hat^T) V_hat,
  * K_hat/V_hat the dequantized prefix plus the 16-bit window, query head j
  * reading kv-head j / (n_q_heads / n_kv_heads).  q: device
  * [batch][n_q_heads][128] in dtype; out: device fp32, same shape; ws:
  * device scratch of at least rq_decode_workspace bytes.  Its start holds
- * arrival counters (a fixed number per (batch, kv-head), set by the cache's
- * capacity) that must be zero before the first call on a workspace (zero
- * the whole buffer once); every call leaves them zero again.  The rest
- * holds per-call partial results.  Calls that share a workspace must not
- * overlap.  RQ_TURBO: handles kv-heads of 1..4 bits; a layer with a wider
- * head returns RQ_EUNSUPPORTED.  A layer whose K+V widths need more LDS
- * than the device offers returns RQ_EUNSUPPORTED.  Asynchronous. */
+ * counters (a fixed number per (batch, kv-head), set by the cache's
+ * capacity), each tagged with the number of the call counting in it: the
+ * library numbers the calls on each workspace (by its address), so a count
+ * left by an earlier call that did not finish is recognised and replaced;
+ * a zeroed buffer is always valid, and so is one left by earlier calls.
+ * The rest holds per-call partial results.  Calls that share a workspace
+ * must not overlap (they would race on the counters and partials).
+ * Accuracy: fp16 matrix-core operands with fp32 accumulation; the error is
+ * within 1e-2 max-abs for values of unit scale and grows in proportion to
+ * max|V_hat| beyond it; inputs must be finite, |scale * q| and the
+ * dequantized |K_hat|, |V_hat| below 2^56.  A layer whose K+V widths need
+ * more LDS than the device offers returns RQ_EUNSUPPORTED.
+ * Asynchronous. */
 rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
                               int32_t n_tokens, const void* q, float* out,
                               float scale, void* ws, uint64_t ws_bytes,

@@ -389,9 +389,9 @@ class KVCache:
         import torch
         need = rq_decode_workspace(self.desc, n_tokens)
         if self._ws is None or self._ws.numel() < need:
-            # zeroed once, on the stream of the call that first uses it: the
-            # arrival counters at its start must be zero before the first
-            # call (every call leaves them zero)
+            # zeroed once, on the stream of the call that first uses it (a
+            # zeroed counter is always read as stale, whatever the call's
+            # number on this workspace)
             s = torch.cuda.current_stream() if stream is None else stream
             with torch.cuda.stream(s):
                 self._ws = torch.zeros(need, dtype=torch.uint8,

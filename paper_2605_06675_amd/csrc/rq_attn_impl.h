@@ -790,23 +790,65 @@ __device__ __forceinline__ void wait_slot(int n) {
   else wait_vm_rt(n);
 }
 
+// Arrival and claim counters (agent scope, 64 bits): the upper half holds
+// the number of the call counting in it (the host numbers the calls on a
+// workspace 1, 2, ..), the lower half the count.  The last user of a
+// counter in a call leaves (next number, 0), so the next call on the
+// workspace finds its counters ready; a counter with another tag (a zeroed
+// workspace, or a count left by a call that did not finish) is stale, and
+// the first arrival of the call takes it over.
+__device__ __forceinline__ uint32_t next_epoch(uint32_t e) { return e + 1u == 0u ? 1u : e + 1u; }
+
+__device__ __forceinline__ uint64_t ctr_add(uint64_t* c) {
+  return __hip_atomic_fetch_add(c, (uint64_t)1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The count an arrival took, from its fetch-add result `old` (one lane).
+// With a stale tag the add does not count: the arrival installs
+// (epoch, 1), taking count 0, unless another arrival installed the tag
+// first, and then adds again.  Every turn of the loop returns or follows a
+// change of the counter by another arrival, and an arrival changes it at
+// most twice, so the loop ends.
+__device__ __forceinline__ uint32_t ctr_count(uint64_t* c, uint64_t old, uint32_t epoch) {
+  if ((uint32_t)(old >> 32) == epoch) return (uint32_t)old;
+  const uint64_t first = ((uint64_t)epoch << 32) | 1u;
+  for (;;) {
+    uint64_t cur = __hip_atomic_load(c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if ((uint32_t)(cur >> 32) == epoch) {
+      const uint64_t o = ctr_add(c);
+      if ((uint32_t)(o >> 32) == epoch) return (uint32_t)o;
+    } else if (__hip_atomic_compare_exchange_strong(c, &cur, first, __ATOMIC_RELAXED,
+                                                    __ATOMIC_RELAXED,
+                                                    __HIP_MEMORY_SCOPE_AGENT)) {
+      return 0;
+    }
+  }
+}
+
 // Block claims of a wave: the unit's blocks beyond the statically assigned
 // first ones go to whichever wave asks next (an agent-scope counter), so
 // that waves and workgroups that run faster take more of them.
 struct Claims {
-  uint32_t* ctr;       // the unit's claim counter (zero between calls)
+  uint64_t* ctr;       // the unit's claim counter
   int base;            // first dynamically assigned block
   int nblk;            // blocks of the unit
-  uint32_t pending;    // result of the claim in flight (lane 0)
+  uint32_t epoch;      // the call's tag
+  uint64_t pending;    // fetch-add result of the claim in flight (lane 0)
   bool live;           // a claim is in flight
 };
 
 // Lane 0 claims; its result is read -- and waited for -- only where the
-// caller takes lane 0's value.
-__device__ __forceinline__ uint32_t claim_issue(uint32_t* ctr, int lane) {
-  uint32_t r = 0;
-  if (lane == 0) r = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// caller takes lane 0's value (claim_take).
+__device__ __forceinline__ uint64_t claim_issue(uint64_t* ctr, int lane) {
+  uint64_t r = 0;
+  if (lane == 0) r = ctr_add(ctr);
   return r;
+}
+
+__device__ __forceinline__ int claim_take(Claims& cl, int lane) {
+  uint32_t v = 0;
+  if (lane == 0) v = ctr_count(cl.ctr, cl.pending, cl.epoch);
+  return __builtin_amdgcn_readfirstlane((int)v);
 }
 
 // The wave's blocks, up to `depth` (2 .. kMaxDepth) in flight in a ring of
@@ -851,7 +893,7 @@ __device__ __forceinline__ void stream_blocks(const Geo& g, int depth, int n_sta
       // pinned here: read before the block, the claim would be waited for
       // one block early
       asm volatile("" : "+v"(cl.pending) : : "memory");
-      const int v = __builtin_amdgcn_readfirstlane((int)cl.pending);
+      const int v = claim_take(cl, lo.lane);
       if (cl.base + v < cl.nblk) next = cl.base + v;
       else cl.live = false;
     }
@@ -1180,7 +1222,8 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int n
   int n_static = 0;
   for (int j = 0; j < depth; ++j) n_static += g_lo + wk + j * wstride < g_hi ? 1 : 0;
   Claims cl;
-  cl.ctr = a.counters + unit * a.cstride + a.claim_off + 32 * grp;
+  cl.ctr = a.counters + unit * a.cstride + a.claim_off + 16 * grp;
+  cl.epoch = a.epoch;
   cl.base = g_lo + depth * wstride;
   cl.nblk = g_hi;
   cl.live = cl.base < g_hi;
@@ -1558,19 +1601,20 @@ __device__ __forceinline__ void merge_slots(const AttnLaunch& a, size_t unit, fl
 
 // Arrival tickets on the unit's counters (agent scope); the caller's
 // partials are published (s_waitcnt 0) before.
-__device__ __forceinline__ uint32_t take_ticket(uint32_t* counter) {
+__device__ __forceinline__ uint32_t take_ticket(uint64_t* counter, uint32_t epoch) {
   __shared__ uint32_t ticket;
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  if (threadIdx.x == 0)
-    ticket = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (threadIdx.x == 0) ticket = ctr_count(counter, ctr_add(counter), epoch);
   __syncthreads();
   return ticket;
 }
 
-__device__ __forceinline__ void reset_counter(uint32_t* counter) {
+// A counter's last use in the call: ready it for the next call.
+__device__ __forceinline__ void reset_counter(uint64_t* counter, uint32_t epoch) {
   if (threadIdx.x == 0)
-    __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(counter, (uint64_t)next_epoch(epoch) << 32, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // FAM: quantizer family; NA: A operands of the KIVI value side (G <= 4: 1,
@@ -1632,14 +1676,15 @@ attn_kernel(AttnLaunch a) {
   // they report in groups of kGroup, the last of a group merges it into a
   // group partial; the group mergers then report on the final counter,
   // whose last arrival merges the group partials and the window.  Every
-  // counter is left at zero for the next call.
-  uint32_t* cnt = a.counters + unit * a.cstride;
+  // counter used is left ready for the next call.
+  uint64_t* cnt = a.counters + unit * a.cstride;
+  const uint32_t ep = a.epoch;
   const int ng = (nw + kGroup - 1) / kGroup;
   if (ng <= 1) {
-    if (take_ticket(cnt) == (uint32_t)(nx - 1)) {
+    if (take_ticket(cnt, ep) == (uint32_t)(nx - 1)) {
       merge_slots(a, unit, merge, 0, nw, nw, a.n_rw, nullptr);
-      reset_counter(cnt);
-      reset_counter(cnt + a.claim_off);
+      reset_counter(cnt, ep);
+      reset_counter(cnt + a.claim_off, ep);
     }
     return;
   }
@@ -1647,17 +1692,17 @@ attn_kernel(AttnLaunch a) {
     // two levels: every workgroup streams (nx = nw > kGroup)
     const int g = slot / kGroup;
     const int gsz = nw - g * kGroup < kGroup ? nw - g * kGroup : kGroup;
-    if (take_ticket(cnt + 1 + g) != (uint32_t)(gsz - 1)) return;
+    if (take_ticket(cnt + 1 + g, ep) != (uint32_t)(gsz - 1)) return;
     __syncthreads();   // the merge area is read until here
     merge_slots(a, unit, merge, g * kGroup, gsz, 0, 0,
                 part_ptr(a, unit, nw + a.n_rw + g));
-    reset_counter(cnt + 1 + g);
+    reset_counter(cnt + 1 + g, ep);
     // every wave of the group has stopped claiming
-    reset_counter(cnt + a.claim_off + 32 * g);
+    reset_counter(cnt + a.claim_off + 16 * g, ep);
   }
-  if (take_ticket(cnt) != (uint32_t)(ng - 1)) return;
+  if (take_ticket(cnt, ep) != (uint32_t)(ng - 1)) return;
   merge_slots(a, unit, merge, nw + a.n_rw, ng, nw, a.n_rw, nullptr);
-  reset_counter(cnt);
+  reset_counter(cnt, ep);
 }
 
 }  // namespace

@@ -9,8 +9,8 @@
 namespace rq {
 namespace {
 
-// Counters first (zero at load, and every call leaves the ones it used at
-// zero), then the partials.
+// Counters first (zero at load; each call tags them with its number), then
+// the partials.
 constexpr uint64_t kScratchCounterBytes = 1ull << 20;
 constexpr uint64_t kScratchBytes = 8ull << 20;
 static_assert(kScratchCounterBytes % 256 == 0, "partials stay 256-byte aligned");
@@ -55,7 +55,7 @@ rq_status rq_decode_attention_static(const rq_cache* c, int32_t layer, int32_t n
   if (st != RQ_OK) return st;
   uint8_t* base = static_cast<uint8_t*>(p);
   return rq::decode_attention(c, layer, n_tokens, q, out, scale,
-                              reinterpret_cast<uint32_t*>(base), rq::kScratchCounterBytes,
+                              base, rq::kScratchCounterBytes,
                               reinterpret_cast<float*>(base + rq::kScratchCounterBytes),
                               rq::kScratchBytes - rq::kScratchCounterBytes, stream);
 }

@@ -3,7 +3,9 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
+#include <mutex>
 #include <string>
+#include <unordered_map>
 #include <vector>
 
 #include "rq_host.h"
@@ -253,14 +255,28 @@ int max_groups(const rq_cache* c) {
   const int max_wg = (c->capacity / rq::kChunk + 3) / 4;
   return (max_wg + rq::kAttnGroup - 1) / rq::kAttnGroup;
 }
-int claim_offset(const rq_cache* c) { return 32 * ((1 + max_groups(c) + 31) / 32); }
-int counter_stride(const rq_cache* c) { return claim_offset(c) + 32 * max_groups(c); }
+// (64-bit counters: 16 per line)
+int claim_offset(const rq_cache* c) { return 16 * ((1 + max_groups(c) + 15) / 16); }
+int counter_stride(const rq_cache* c) { return claim_offset(c) + 16 * max_groups(c); }
 
-// Workspace: per-unit arrival counters (zero between calls), padded to 256
-// bytes, then the partials [B][H][n_wg + n_rw + groups][G][2 + 128] floats.
+// Workspace: per-unit arrival and claim counters, padded to 256 bytes, then
+// the partials [B][H][n_wg + n_rw + groups][G][2 + 128] floats.
 uint64_t attn_counter_bytes(const rq_cache* c) {
-  return ((uint64_t)c->batch * c->n_kv_heads * counter_stride(c) * sizeof(uint32_t) + 255) /
+  return ((uint64_t)c->batch * c->n_kv_heads * counter_stride(c) * sizeof(uint64_t) + 255) /
          256 * 256;
+}
+
+// The calls on one workspace (keyed by the address of its counters) are
+// numbered 1, 2, ..; the number tags the counters the call uses, so that a
+// count left by a call that did not finish is recognised as stale (0 never
+// numbers a call: a zeroed counter is always stale).
+uint32_t next_epoch(const void* counters) {
+  static std::mutex mu;
+  static std::unordered_map<const void*, uint32_t> epochs;
+  std::lock_guard<std::mutex> lock(mu);
+  uint32_t& e = epochs[counters];
+  e = e + 1u == 0u ? 1u : e + 1u;
+  return e;
 }
 
 int part_stride(const SplitPlan& p) { return p.pstride; }
@@ -278,7 +294,7 @@ namespace rq {
 uint64_t decode_counter_bytes(const rq_cache* c) { return attn_counter_bytes(c); }
 
 rq_status decode_attention(const rq_cache* c, int32_t layer, int32_t n_tokens, const void* q,
-                           float* out, float scale, uint32_t* counters, uint64_t counter_cap,
+                           float* out, float scale, void* counters, uint64_t counter_cap,
                            float* part, uint64_t part_cap, rq_stream stream) {
   rq_status st = check_cache(c);
   if (st != RQ_OK) return st;
@@ -314,7 +330,8 @@ rq_status decode_attention(const rq_cache* c, int32_t layer, int32_t n_tokens, c
   a.meta = static_cast<const uint8_t*>(c->meta) + meta_layer_bytes(c) * layer;
   a.resid = static_cast<const uint16_t*>(c->resid) + resid_layer_elems(c) * layer;
   a.out = out;
-  a.counters = counters;
+  a.counters = static_cast<uint64_t*>(counters);
+  a.epoch = next_epoch(counters);
   a.part = part;
   a.pstride = part_stride(p);
   a.cstride = counter_stride(c);
@@ -466,7 +483,7 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
   if (ws_bytes < cb)
     return fail(RQ_ESMALLWS, "workspace %llu bytes < %llu needed",
                 (unsigned long long)ws_bytes, (unsigned long long)cb);
-  return rq::decode_attention(c, layer, n_tokens, q, out, scale, static_cast<uint32_t*>(ws), cb,
+  return rq::decode_attention(c, layer, n_tokens, q, out, scale, ws, cb,
                               reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + cb),
                               ws_bytes - cb, stream);
 }

@@ -82,7 +82,9 @@ struct AttnLaunch {
   float* part;            // [B][H][pstride][G][2 + 128] (max, sum, acc);
                           // slots 0..n_wg-1 streaming, n_wg..n_wg+n_rw-1
                           // the residual window, then one per merge group
-  uint32_t* counters;     // [B][H][cstride] arrival counters, zero between calls
+  uint64_t* counters;     // [B][H][cstride] arrival and claim counters:
+                          // (epoch << 32) | count
+  uint32_t epoch;         // this call's number on the workspace (>= 1)
   int pstride;            // partial slots per unit
   int cstride;            // counters per unit: tickets (final, one per
                           // merge group) in the first 128-byte lines, then
@@ -140,11 +142,11 @@ struct SensLaunch {
 hipError_t launch_sensitivity(const SensLaunch& a, hipStream_t s);
 
 // Decode attention of one layer with the arrival counters (counter_cap
-// bytes, zero between calls) and the partial results (part_cap bytes) in
-// the given device buffers: the validation and launch shared by the entry
+// bytes, epoch-tagged) and the partial results (part_cap bytes) in the
+// given device buffers: the validation and launch shared by the entry
 // points with a caller's workspace and with the library's own scratch.
 rq_status decode_attention(const rq_cache* c, int32_t layer, int32_t n_tokens, const void* q,
-                           float* out, float scale, uint32_t* counters, uint64_t counter_cap,
+                           float* out, float scale, void* counters, uint64_t counter_cap,
                            float* part, uint64_t part_cap, rq_stream stream);
 // Bytes of arrival counters a cache's calls use.
 uint64_t decode_counter_bytes(const rq_cache* c);

@@ -196,7 +196,7 @@ def test_kivi_two_level_merge_long_context(G):
     """Two kv-heads, batch 1, 8000+ tokens: more than 16 workgroups per
     unit, so partials are merged in groups first.  Attention after the
     prefill and after appends that change the number of workgroups (the
-    counters must come back to zero every call)."""
+    counters must be ready for the next call every time)."""
     torch = _torch()
     H, R, T0 = 2, 128, 8000
     bits = np.array([[[2, 1], [3, 4]]])
@@ -243,6 +243,37 @@ def test_group_sizes_not_power_of_two(family, G):
     units = _check_cache(family, workloads.BF16, kvc, ks, vs, bits, 32, 2, 3,
                          1100)
     _check_attention(kvc, units, workloads.BF16, 2, 3, G)
+
+
+@pytest.mark.parametrize("fill", ["foreign_tags", "random_bytes"])
+def test_stale_workspace_counters(fill):
+    """A workspace whose counters hold counts of other calls (foreign tags,
+    arbitrary counts: what a call that did not finish leaves) or random
+    bytes: the call replaces the stale counts and matches the oracle, and
+    the call after it (on counters this call readied) does too.  4100
+    tokens over 2 x 4 units: two-level merges with claims in each group."""
+    torch = _torch()
+    H, G, T = 4, 4, 4100
+    bits = np.array([[[2, 3], [1, 4], [3, 2], [4, 1]]])
+    kvc, ks, vs, _ = _build(workloads.KIVI, workloads.BF16, H, G, T, 32, bits,
+                            batch=2)
+    units = _check_cache(workloads.KIVI, workloads.BF16, kvc, ks, vs, bits, 32,
+                         2, H, T)
+    ws = kvc.workspace(T)
+    rng = np.random.default_rng(17)
+    n8 = ws.numel() // 8
+    if fill == "foreign_tags":
+        tag = rng.integers(0x40000000, 0x7fffffff, size=n8, dtype=np.int64)
+        cnt = rng.integers(0, 1000, size=n8, dtype=np.int64)
+        stale = torch.from_numpy((tag << 32) | cnt).to(ws.device)
+        ws[:n8 * 8].view(torch.int64).copy_(stale)
+    else:
+        raw = rng.integers(0, 256, size=ws.numel(), dtype=np.uint8)
+        ws.copy_(torch.from_numpy(raw).to(ws.device))
+    torch.cuda.synchronize()
+    print(f"stale workspace ({fill})", flush=True)
+    for call in range(2):
+        _check_attention(kvc, units, workloads.BF16, 2, H, G, seed=11 + call)
 
 
 def test_short_context_window_only():
