@@ -4,6 +4,7 @@
 """
 import concurrent.futures
 import os
+import re
 import shutil
 import subprocess
 import sys
@@ -50,9 +51,36 @@ def _compile(src):
         if not asm:
             raise RuntimeError(f"{src}: device assembly not found")
         with open(os.path.join(BUILD, asm[0])) as f:
-            if "s_swappc" in f.read():
-                raise RuntimeError(f"{src}: device code contains a function call")
+            text = f.read()
+        if "s_swappc" in text:
+            raise RuntimeError(f"{src}: device code contains a function call")
+        if src.startswith("rq_attn"):
+            _check_claim_registers(src, text)
     return obj
+
+
+_VREG = re.compile(r"\bv(\d+)\b|\bv\[(\d+):(\d+)\]")
+_CLAIM_REGS = {166, 167}
+
+
+def _check_claim_registers(src, text):
+    """The attention kernels keep their block claims in v[166:167], written
+    and read only by inline assembly: reject code in which the compiler
+    itself uses one of those registers."""
+    in_asm = False
+    for line in text.split("\n"):
+        t = line.strip()
+        if t.startswith(";;#ASMSTART"):
+            in_asm = True
+        elif t.startswith(";;#ASMEND"):
+            in_asm = False
+        elif not in_asm and line.startswith("\t") and t and t[0] not in ".;":
+            for m in _VREG.finditer(t.split(";")[0]):
+                lo = int(m.group(1) or m.group(2))
+                hi = int(m.group(1) or m.group(3))
+                if _CLAIM_REGS & set(range(lo, hi + 1)):
+                    raise RuntimeError(f"{src}: compiler-generated use of a "
+                                       f"claim register: {t}")
 
 
 def build(verbose=False):

@@ -680,26 +680,39 @@ __device__ __forceinline__ void block_step(const uint8_t* slot, const LaneOps& l
 
 // A block's data is four contiguous byte ranges: K codes (512*BK), V codes
 // (512*BV), K metadata and V metadata (the family's metadata bytes of a
-// block of each kind).  A wave copies it
-// straight from global memory into one of its LDS slots with
-// global_load_lds_dwordx4: piece k of lane l covers bytes [16 l + 1024 k,
-// +16) of the concatenation, so every instruction moves 1 KB of contiguous
-// memory and no VGPR holds the data in flight.
+// block of each kind).  A wave copies it straight from global memory into
+// one of its LDS slots with buffer_load_dwordx4 .. lds: piece k of lane l
+// covers bytes [16 l + 1024 k, +16) of the concatenation, so every
+// instruction moves up to 1 KB of contiguous memory and no VGPR holds the
+// data in flight.  Two buffer resources per unit: its codes (K then V,
+// based at its K codes) and its metadata (based at its K metadata); the
+// piece that holds the end of the codes and the start of the metadata takes
+// one instruction for each.  (The flat-encoded global_load_lds would do
+// the same copies, but the compiler's wait insertion counts it as an LDS
+// access as well and then waits for every LDS read in flight before using
+// any of them.)
 template <int FAM, int BK, int BV> struct Slot {
   static constexpr int kb = 512 * BK;
   static constexpr int vb = 512 * BV;
+  static constexpr int cb = kb + vb;            // code bytes
   static constexpr int kmb = meta_block_bytes(FAM, 0);
   static constexpr int vmb = meta_block_bytes(FAM, 1);
-  static constexpr int bytes = kb + vb + kmb + vmb;
+  static constexpr int bytes = cb + kmb + vmb;
   static constexpr int pieces = (bytes + 1023) / 1024;
+  static constexpr int ops = pieces + (cb % 1024 != 0 ? 1 : 0);   // copy instructions
 };
 
 struct Geo {
-  const uint8_t* kreg;   // K codes of this unit
-  const uint8_t* vreg;   // V codes
-  const uint8_t* kmeta;  // K metadata
-  const uint8_t* vmeta;  // V metadata
+  __amdgpu_buffer_rsrc_t codes;  // this unit's K codes, then (at voff) its V codes
+  __amdgpu_buffer_rsrc_t meta;   // its K metadata, then (at vmoff) its V metadata
+  uint32_t voff, vmoff;
 };
+
+// Buffer resource over n bytes at p (raw 32-bit data format, no swizzle;
+// accesses at or beyond n read zeros).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_of(const void* p, uint32_t n) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, (int)n, 0x00020000);
+}
 
 typedef __attribute__((address_space(3))) void lds_void;
 
@@ -708,27 +721,35 @@ typedef __attribute__((address_space(3))) void lds_void;
 // the kernel's code and small shared data stay there across calls.
 constexpr int kStreamPolicy = 2;
 
+// Piece k of block blk into slot (lane: this lane's 16 bytes at o).
+__device__ __forceinline__ void copy_piece(const Geo& g, int blk, int o, int kb, int vb, int cb,
+                                           int kmb, int vmb, int bytes, bool has_codes,
+                                           bool has_meta, lds_void* dst) {
+  const uint32_t ub = (uint32_t)blk;
+  if (has_codes && o < cb) {
+    const uint32_t off = o < kb ? ub * kb + o : g.voff + ub * vb + (o - kb);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(g.codes, dst, 16, off, 0, 0, kStreamPolicy);
+  }
+  if (has_meta && o >= cb && o < bytes) {
+    const int m = o - cb;
+    const uint32_t off = m < kmb ? ub * kmb + m : g.vmoff + ub * vmb + (m - kmb);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(g.meta, dst, 16, off, 0, 0, kStreamPolicy);
+  }
+}
+
 template <int FAM, int BK, int BV>
 __device__ __forceinline__ void issue_block(const Geo& g, int blk, int lane, uint8_t* slot) {
   using S = Slot<FAM, BK, BV>;
 #pragma unroll
-  for (int k = 0; k < S::pieces; ++k) {
-    const int o = 16 * lane + 1024 * k;
-    if (o < S::bytes) {
-      const uint8_t* src;
-      if (o < S::kb) src = g.kreg + (size_t)blk * S::kb + o;
-      else if (o < S::kb + S::vb) src = g.vreg + (size_t)blk * S::vb + (o - S::kb);
-      else if (o < S::kb + S::vb + S::kmb) src = g.kmeta + (size_t)blk * S::kmb + (o - S::kb - S::vb);
-      else src = g.vmeta + (size_t)blk * S::vmb + (o - S::kb - S::vb - S::kmb);
-      __builtin_amdgcn_global_load_lds(src, (lds_void*)(slot + 1024 * k), 16, 0, kStreamPolicy);
-    }
-  }
+  for (int k = 0; k < S::pieces; ++k)
+    copy_piece(g, blk, 16 * lane + 1024 * k, S::kb, S::vb, S::cb, S::kmb, S::vmb, S::bytes,
+               1024 * k < S::cb, 1024 * (k + 1) > S::cb, (lds_void*)(slot + 1024 * k));
 }
 
 // Wait until at most N vector-memory operations of this wave are in flight
 // (gfx9 s_waitcnt encoding: vmcnt in bits 3:0 and 15:14, expcnt and lgkmcnt
-// at their maxima).  The compiler does not track LDS written by
-// global_load_lds, so the reads of a slot are fenced by hand.
+// at their maxima).  The compiler does not track LDS written by the
+// buffer-to-LDS copies, so the reads of a slot are fenced by hand.
 template <int N>
 __device__ __forceinline__ void wait_vm() {
   static_assert(N < 64, "vmcnt is 6 bits");
@@ -737,30 +758,23 @@ __device__ __forceinline__ void wait_vm() {
 }
 
 // Static blocks j0 .. j1-1 of a wave's ring (block blk0 + j stride, below
-// nblk, into slot j at j * bytes; bytes and pieces as in Slot<>, at run
-// time).  Returns the copy instructions issued.
+// nblk, into slot j at j * bytes; the layout of Slot<> at run time).
+// Returns the copy instructions issued.
 __device__ __forceinline__ int issue_first(const Geo& g, int bk, int bv, int mk, int mv, int j0,
                                            int j1, int blk0, int stride, int nblk, int lane,
                                            uint8_t* slots) {
-  const int kb = 512 * bk, vb = 512 * bv, bytes = kb + vb + mk + mv;
+  const int kb = 512 * bk, vb = 512 * bv, cb = kb + vb, bytes = cb + mk + mv;
   const int pieces = (bytes + 1023) / 1024;
+  const int ops = pieces + (cb % 1024 != 0 ? 1 : 0);
   int issued = 0;
   for (int j = j0; j < j1; ++j) {
     const int blk = blk0 + stride * j;
     if (blk >= nblk) break;
-    issued += pieces;
+    issued += ops;
     uint8_t* slot = slots + j * bytes;
-    for (int k = 0; k < pieces; ++k) {
-      const int o = 16 * lane + 1024 * k;
-      if (o < bytes) {
-        const uint8_t* src;
-        if (o < kb) src = g.kreg + (size_t)blk * kb + o;
-        else if (o < kb + vb) src = g.vreg + (size_t)blk * vb + (o - kb);
-        else if (o < kb + vb + mk) src = g.kmeta + (size_t)blk * mk + (o - kb - vb);
-        else src = g.vmeta + (size_t)blk * mv + (o - kb - vb - mk);
-        __builtin_amdgcn_global_load_lds(src, (lds_void*)(slot + 1024 * k), 16, 0, kStreamPolicy);
-      }
-    }
+    for (int k = 0; k < pieces; ++k)
+      copy_piece(g, blk, 16 * lane + 1024 * k, kb, vb, cb, mk, mv, bytes, 1024 * k < cb,
+                 1024 * (k + 1) > cb, (lds_void*)(slot + 1024 * k));
   }
   return issued;
 }
@@ -778,16 +792,30 @@ __device__ __forceinline__ void wait_vm_rt(int n) {
   }
 }
 
-// The wait before a block of P copy instructions: in steady state n, the
-// operations issued after its copies, is (depth - 1) (P + 1) (the later
-// slots' copies and claims), tested first so that the block loop usually
-// takes one compare; any other n goes through wait_vm_rt.
+// The wait before a block of P copy instructions, n the operations issued
+// after its copies: the largest multiple of P + 1 not above n (waiting for
+// fewer outstanding operations is always safe).  In steady state n is
+// (depth - 1) (P + 1) (the later slots' copies and claims) and the wait
+// exact; the other values occur while the ring fills, when the operations
+// it also waits for were issued right after the slot's.  Three compares at
+// most, so that the loop does not walk a search tree per block.
 template <int P>
 __device__ __forceinline__ void wait_slot(int n) {
-  if (n == 3 * (P + 1)) wait_vm<3 * (P + 1)>();
-  else if (n == 2 * (P + 1)) wait_vm<2 * (P + 1)>();
-  else if (n == P + 1) wait_vm<P + 1>();
-  else wait_vm_rt(n);
+  if (n >= 3 * (P + 1)) wait_vm<3 * (P + 1)>();
+  else if (n >= 2 * (P + 1)) wait_vm<2 * (P + 1)>();
+  else if (n >= P + 1) wait_vm<P + 1>();
+  else wait_vm<0>();
+}
+
+// The wait for a claim with n operations issued after it: the largest
+// multiple of P (the copies of one block) not above n.
+template <int P>
+__device__ __forceinline__ void wait_claim(int n) {
+  if (n >= 4 * P) wait_vm<4 * P>();
+  else if (n >= 3 * P) wait_vm<3 * P>();
+  else if (n >= 2 * P) wait_vm<2 * P>();
+  else if (n >= P) wait_vm<P>();
+  else wait_vm<0>();
 }
 
 // Arrival and claim counters (agent scope, 64 bits): the upper half holds
@@ -833,21 +861,35 @@ struct Claims {
   int base;            // first dynamically assigned block
   int nblk;            // blocks of the unit
   uint32_t epoch;      // the call's tag
-  uint64_t pending;    // fetch-add result of the claim in flight (lane 0)
+  int mark;            // the wave's operation count just after the claim
   bool live;           // a claim is in flight
 };
 
-// Lane 0 claims; its result is read -- and waited for -- only where the
-// caller takes lane 0's value (claim_take).
-__device__ __forceinline__ uint64_t claim_issue(uint64_t* ctr, int lane) {
-  uint64_t r = 0;
-  if (lane == 0) r = ctr_add(ctr);
-  return r;
+// The claim's fetch-add returns into v[166:167] of lane 0, registers
+// written and read only by these inline statements: the kernel leaves them
+// out of the compiler's allocation (and the build rejects attention code in
+// which the compiler uses them itself).
+// The compiler's wait insertion does not order the LDS-DMA block copies
+// with other loads, so a result in a register it tracks would be waited
+// for with every copy in flight; here the wave waits itself, for the claim
+// and what was issued before it (claim_take).
+#define RQ_CLAIM_REGS "memory", "v166", "v167"
+
+__device__ __forceinline__ void claim_issue(uint64_t* ctr, int lane) {
+  if (lane == 0)
+    asm volatile("global_atomic_add_x2 v[166:167], %0, %1, off sc0" ::"v"(ctr),
+                 "v"((uint64_t)1) : RQ_CLAIM_REGS);
 }
 
-__device__ __forceinline__ int claim_take(Claims& cl, int lane) {
+// The claimed index (relative to cl.base); n: the operations this wave
+// issued after the claim.
+template <int P>
+__device__ __forceinline__ int claim_take(const Claims& cl, int lane, int n) {
+  wait_claim<P>(n);
+  uint32_t lo, hi;
+  asm volatile("v_mov_b32 %0, v166\n\tv_mov_b32 %1, v167" : "=v"(lo), "=v"(hi) :: RQ_CLAIM_REGS);
   uint32_t v = 0;
-  if (lane == 0) v = ctr_count(cl.ctr, cl.pending, cl.epoch);
+  if (lane == 0) v = ctr_count(cl.ctr, ((uint64_t)hi << 32) | lo, cl.epoch);
   return __builtin_amdgcn_readfirstlane((int)v);
 }
 
@@ -875,25 +917,22 @@ __device__ __forceinline__ void stream_blocks(const Geo& g, int depth, int n_sta
   // m1.. those of the next slots in ring order (the first n0 slots were
   // issued back to back)
   const int n0 = n_static < n_up ? n_static : n_up;
-  int m0 = issued - (n0 - 1) * S::pieces;
-  int m1 = m0 + S::pieces;
-  int m2 = n0 > 2 ? m0 + 2 * S::pieces : m1;
-  int m3 = n0 > 3 ? m0 + 3 * S::pieces : m1;
+  int m0 = issued - (n0 - 1) * S::ops;
+  int m1 = m0 + S::ops;
+  int m2 = n0 > 2 ? m0 + 2 * S::ops : m1;
+  int m3 = n0 > 3 ? m0 + 3 * S::ops : m1;
   int inflight = n0;
   int ramp = n0;   // next static block (and slot), two ahead of the current
   int off = 0;
   const int ring = depth * S::bytes;
   while (inflight > 0) {
-    wait_slot<S::pieces>(issued - m0);
+    wait_slot<S::ops>(issued - m0);
     uint8_t* slot = slots + off;
     block_step<FAM, NA, BK, BV>(slot, lo, cst, ws);
     --inflight;
     int next = -1;
     if (cl.live) {
-      // pinned here: read before the block, the claim would be waited for
-      // one block early
-      asm volatile("" : "+v"(cl.pending) : : "memory");
-      const int v = claim_take(cl, lo.lane);
+      const int v = claim_take<S::ops>(cl, lo.lane, issued - cl.mark);
       if (cl.base + v < cl.nblk) next = cl.base + v;
       else cl.live = false;
     }
@@ -902,17 +941,18 @@ __device__ __forceinline__ void stream_blocks(const Geo& g, int depth, int n_sta
     asm volatile("" ::: "memory");
     if (ramp < n_static) {
       issue_block<FAM, BK, BV>(g, blk0 + ramp * stride, lo.lane, slots + ramp * S::bytes);
-      issued += S::pieces;
+      issued += S::ops;
       m2 = issued;
       ++ramp;
       ++inflight;
     }
     int mnew = m0;
     if (next >= 0) {
-      cl.pending = claim_issue(cl.ctr, lo.lane);
+      claim_issue(cl.ctr, lo.lane);
       issued += 1;
+      cl.mark = issued;
       issue_block<FAM, BK, BV>(g, next, lo.lane, slot);
-      issued += S::pieces;
+      issued += S::ops;
       mnew = issued;
       ++inflight;
     }
@@ -958,18 +998,18 @@ __device__ __forceinline__ u4 query_piece(const AttnLaunch& a, int b, int h) {
 }
 
 // Copy the 16-bit query rows of this kv-head (G x 256 bytes) into qraw with
-// global_load_lds: wave w moves bytes [1024 w, 1024 w + 1024).  Returns the
-// number of copy instructions this wave issued (0 or 1).
+// buffer_load_dwordx4 .. lds: wave w moves bytes [1024 w, 1024 w + 1024).
+// Returns the number of copy instructions this wave issued (0 or 1).
 __device__ __forceinline__ int issue_query(const AttnLaunch& a, int b, int h, int wave,
                                            int lane, uint16_t* qraw) {
   const int bytes = a.G * kD * 2;
   if (1024 * wave >= bytes) return 0;
-  const uint8_t* src = reinterpret_cast<const uint8_t*>(
-      a.q + ((size_t)b * a.H * a.G + (size_t)h * a.G) * kD);
+  const __amdgpu_buffer_rsrc_t src =
+      buffer_of(a.q + ((size_t)b * a.H * a.G + (size_t)h * a.G) * kD, (uint32_t)bytes);
   if (1024 * wave + 16 * lane < bytes)
-    __builtin_amdgcn_global_load_lds(src + 1024 * wave + 16 * lane,
-                                     (lds_void*)(reinterpret_cast<uint8_t*>(qraw) + 1024 * wave),
-                                     16, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        src, (lds_void*)(reinterpret_cast<uint8_t*>(qraw) + 1024 * wave), 16,
+        1024 * wave + 16 * lane, 0, 0, 0);
   return 1;
 }
 
@@ -1195,10 +1235,18 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int n
   const int nblk_cap = a.cap / kChunk;
   constexpr int mk = meta_block_bytes(FAM, 0), mv = meta_block_bytes(FAM, 1);
   Geo g;
-  g.kreg = a.codes + a.tab.code_off[h][0] + (size_t)b * a.cap * 16 * bk;
-  g.vreg = a.codes + a.tab.code_off[h][1] + (size_t)b * a.cap * 16 * bv;
-  g.kmeta = a.meta + meta_unit_offset(FAM, h, 0, b, a.B, nblk_cap);
-  g.vmeta = a.meta + meta_unit_offset(FAM, h, 1, b, a.B, nblk_cap);
+  {
+    // the unit's codes and metadata as two byte ranges (the host checks
+    // that each spans less than 4 GiB)
+    const size_t k0 = a.tab.code_off[h][0] + (size_t)b * a.cap * 16 * bk;
+    const size_t v0 = a.tab.code_off[h][1] + (size_t)b * a.cap * 16 * bv;
+    const size_t km0 = meta_unit_offset(FAM, h, 0, b, a.B, nblk_cap);
+    const size_t vm0 = meta_unit_offset(FAM, h, 1, b, a.B, nblk_cap);
+    g.voff = (uint32_t)(v0 - k0);
+    g.vmoff = (uint32_t)(vm0 - km0);
+    g.codes = buffer_of(a.codes + k0, g.voff + (uint32_t)a.cap * 16 * bv);
+    g.meta = buffer_of(a.meta + km0, g.vmoff + (uint32_t)nblk_cap * mv);
+  }
   const int nblk = a.nq / kChunk;
   // this unit's ring: as many whole blocks as the wave's region holds
   const int blk_bytes = 512 * (bk + bv) + mk + mv;
@@ -1227,12 +1275,13 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int n
   cl.base = g_lo + depth * wstride;
   cl.nblk = g_hi;
   cl.live = cl.base < g_hi;
-  cl.pending = 0;
+  cl.mark = 0;
   const int nq_ops = issue_query(a, b, h, wave, lane, qraw);
   int issued = 0;
   if (cl.live) {
-    cl.pending = claim_issue(cl.ctr, lane);
+    claim_issue(cl.ctr, lane);
     issued += 1;
+    cl.mark = issued;
   }
   const int nb_ops = issue_first(g, bk, bv, mk, mv, 0, 1, g_lo + wk, wstride, g_hi, lane,
                                  my_slots);
@@ -1619,8 +1668,12 @@ __device__ __forceinline__ void reset_counter(uint64_t* counter, uint32_t epoch)
 
 // FAM: quantizer family; NA: A operands of the KIVI value side (G <= 4: 1,
 // G <= 8: 2, else 4); MAXB: largest bit-width handled (4 or 8).
+// The compiler allocates v0..v165 (the attribute's value is doubled for the
+// unified vector register file of this architecture: 83 -> 166);
+// v[166:167], the rest of the 168 that three workgroups per CU leave a
+// lane, hold the block claims.
 template <int FAM, int NA, int MAXB>
-__global__ void __launch_bounds__(kThreads, kAttnOcc)
+__global__ void __launch_bounds__(kThreads, kAttnOcc) __attribute__((amdgpu_num_vgpr(83)))
 attn_kernel(AttnLaunch a) {
   __shared__ u4 cst4[2];             // fp16 ones (4 dwords), zeros (4 dwords)
   uint32_t* cst = reinterpret_cast<uint32_t*>(cst4);

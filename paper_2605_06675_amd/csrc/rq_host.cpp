@@ -311,6 +311,24 @@ rq_status decode_attention(const rq_cache* c, int32_t layer, int32_t n_tokens, c
     const int bb = 512 * (tab.bits[h][0] + tab.bits[h][1]) + meta_pair_bytes(c);
     max_blk = bb > max_blk ? bb : max_blk;
   }
+  // each unit's K and V codes, and its K and V metadata, are read through
+  // one 32-bit-addressed buffer each
+  {
+    const uint64_t nc = c->capacity / rq::kChunk, cap16 = (uint64_t)c->capacity * 16;
+    const uint64_t mk = rq::meta_block_bytes(c->family, 0), mv = rq::meta_block_bytes(c->family, 1);
+    const uint64_t B = c->batch;
+    for (int h = 0; h < c->n_kv_heads; ++h) {
+      const uint64_t bk = tab.bits[h][0], bv = tab.bits[h][1];
+      for (uint64_t b : {(uint64_t)0, B - 1}) {
+        const uint64_t codes = cap16 * ((B - b) * bk + b * bv) + cap16 * bv;
+        const uint64_t meta = nc * ((B - b) * mk + b * mv) + nc * mv;
+        if (codes > 0xffffffffull || meta > 0xffffffffull)
+          return fail(RQ_EUNSUPPORTED,
+                      "layer %d head %d: the codes of one (batch, kv-head) unit span more "
+                      "than 4 GiB", layer, h);
+      }
+    }
+  }
   AttnShape shape;
   if (!attn_shape(c, max_blk, &shape))
     return fail(RQ_EUNSUPPORTED,
