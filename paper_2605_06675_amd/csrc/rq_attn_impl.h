@@ -1231,7 +1231,8 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int n
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid / kWave), lane = tid & (kWave - 1);
   const size_t unit = (size_t)b * a.H + h;
   const int G = a.G;
-  const int bk = a.tab.bits[h][0], bv = a.tab.bits[h][1];
+  const int bk = kernarg_byte(&a.tab.bits[0][0], 2 * h),
+            bv = kernarg_byte(&a.tab.bits[0][0], 2 * h + 1);
   const int nblk_cap = a.cap / kChunk;
   constexpr int mk = meta_block_bytes(FAM, 0), mv = meta_block_bytes(FAM, 1);
   Geo g;

@@ -150,6 +150,16 @@ __device__ __forceinline__ uint32_t pair_or(const uint32_t* wds, int I, uint32_t
   return acc;
 }
 
+// Entry i (wave-uniform) of a byte table held in the kernel arguments
+// (4-byte aligned), read through its dword: gfx9 has no scalar byte loads,
+// and a vector byte load would be waited for together with every load in
+// flight before it.
+__device__ __forceinline__ int kernarg_byte(const uint8_t* table, int i) {
+  i = __builtin_amdgcn_readfirstlane(i);
+  const uint32_t w = reinterpret_cast<const uint32_t*>(table)[i >> 2];
+  return (int)((w >> (8 * (i & 3))) & 0xffu);
+}
+
 __device__ __forceinline__ h2 as_h2(uint32_t x) {
   return __builtin_bit_cast(h2, x);
 }

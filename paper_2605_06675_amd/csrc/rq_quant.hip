@@ -57,9 +57,11 @@ struct Smem {
 // Persistent kernel: every wave loops over blocks (block, kv-head, batch,
 // K|V in that order), with the next block's 8 KB already loading into
 // registers while the current one is quantized from the wave's own LDS
-// area.  The waves of a workgroup share nothing, so no workgroup barrier is
-// needed: a wave's LDS operations complete in issue order.
+// area.  The waves of a workgroup share nothing, so no
+// workgroup barrier is needed: a wave's LDS operations complete in issue
+// order.
 constexpr int kQWaves = 4;                // waves per workgroup
+constexpr int kQBuf = 1;                  // register buffers per wave
 // workgroups per CU: three when every width of the layer is at most 4 bits
 // (the code paths then fit 168 registers), else two
 __host__ __device__ constexpr int quant_occupancy(int maxb) { return maxb <= 4 ? 3 : 2; }
@@ -169,23 +171,21 @@ __device__ __forceinline__ BlockId block_id(const QuantLaunch& a, int it) {
 
 // Global -> registers: the block's 32 token rows, 16 bytes per lane and
 // step (step j, lane l: token 4 j + l / 16, bytes 16 (l % 16) of the row).
+// Branch-free: each row's address selects between the new input and the
+// residual window, so that every block issues the same eight loads.  The
+// loads are non-temporal: every byte is read once.
 __device__ __forceinline__ void load_block(const QuantLaunch& a, const BlockId& id,
                                            u4 v[8], int lane) {
   const int t0 = id.blk * kChunk;
-  if (t0 >= a.n_past) {
-    // the whole block is new input: 8 KB contiguous
-    const RQ_GLOBAL u4* src = gptr(reinterpret_cast<const u4*>(
-        (id.kind ? a.v : a.k) +
-        ((size_t)(id.b * a.H + id.h) * a.n_new + (t0 - a.n_past)) * kD));
+  const uint16_t* in = (id.kind ? a.v : a.k) + (size_t)(id.b * a.H + id.h) * a.n_new * kD;
+  const int cap = a.R + kChunk;
+  const uint16_t* ring = a.resid + (((size_t)id.b * a.H + id.h) * 2 + id.kind) * cap * kD;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) v[j] = src[j * kWave + lane];
-  } else {
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int c = j * kWave + lane, t = c >> 4, p = c & 15;
-      v[j] = gptr(reinterpret_cast<const u4*>(
-          token_src(a, id.b, id.h, id.kind, t0 + t)))[p];
-    }
+  for (int j = 0; j < 8; ++j) {
+    const int c = j * kWave + lane, t = t0 + (c >> 4), p = c & 15;
+    const uint16_t* row = t >= a.n_past ? in + (size_t)(t - a.n_past) * kD
+                                        : ring + (size_t)(t % cap) * kD;
+    v[j] = __builtin_nontemporal_load(gptr(reinterpret_cast<const u4*>(row)) + p);
   }
 }
 
@@ -349,7 +349,7 @@ __device__ __forceinline__ void kivi_values_lds(const QuantLaunch& a, KiviSmem& 
 template <int BF16, int MAXB>
 __device__ __forceinline__ void kivi_block(const QuantLaunch& a, KiviSmem& sm,
                                            const BlockId& id, int lane) {
-  const int bits = a.tab.bits[id.h][id.kind];
+  const int bits = kernarg_byte(&a.tab.bits[0][0], 2 * id.h + id.kind);
 #define RQ_KIVI_CASE(NB)                                          \
   case NB:                                                        \
     if (NB <= MAXB) {                                             \
@@ -373,6 +373,21 @@ __device__ __forceinline__ void kivi_block(const QuantLaunch& a, KiviSmem& sm,
 #undef RQ_KIVI_CASE
 }
 
+// Block cur from the buffer v, whose registers then start loading the
+// wave's next block.  Every step issues the same loads (past the last
+// block, a copy of the last one, never used), so that the compiler's wait
+// before a buffer's staging counts the younger buffers' loads on every path
+// and leaves them in flight.
+template <int BF16, int MAXB>
+__device__ __forceinline__ void kivi_step(const QuantLaunch& a, KiviSmem& sm, int cur,
+                                          int stride, int total, u4 v[8], int lane) {
+  stage_block(sm, v, lane);
+  const int nxt = cur + kQBuf * stride;
+  load_block(a, block_id(a, nxt < total ? nxt : total - 1), v, lane);
+  kivi_block<BF16, MAXB>(a, sm, block_id(a, cur), lane);
+  __builtin_amdgcn_wave_barrier();
+}
+
 // MAXB: the widest bit-width of the layer (4 or 8)
 template <int BF16, int MAXB>
 __global__ void __launch_bounds__(kQWaves * kWave, quant_occupancy(MAXB))
@@ -387,13 +402,7 @@ kivi_quant_kernel(QuantLaunch a) {
   if (it >= total) return;
   u4 v[8];
   load_block(a, block_id(a, it), v, lane);
-  for (; it < total; it += stride) {
-    const BlockId id = block_id(a, it);
-    stage_block(sm, v, lane);
-    if (it + stride < total) load_block(a, block_id(a, it + stride), v, lane);
-    kivi_block<BF16, MAXB>(a, sm, id, lane);
-    __builtin_amdgcn_wave_barrier();
-  }
+  for (; it < total; it += stride) kivi_step<BF16, MAXB>(a, sm, it, stride, total, v, lane);
 }
 
 // ------------------------------------------------------- QuaRot and RTN
@@ -553,7 +562,7 @@ sym_quant_kernel(QuantLaunch a) {
   const int h = blockIdx.y;
   const int b = blockIdx.z / a.kind_n, kind = a.kind_lo + blockIdx.z % a.kind_n;
   const int lane = threadIdx.x;
-  switch (a.tab.bits[h][kind]) {
+  switch (kernarg_byte(&a.tab.bits[0][0], 2 * h + kind)) {
     case 2: sym_block<ROT, BF16, 2>(a, sm, b, h, kind, blk, lane); break;
     case 3: sym_block<ROT, BF16, 3>(a, sm, b, h, kind, blk, lane); break;
     case 4: sym_block<ROT, BF16, 4>(a, sm, b, h, kind, blk, lane); break;

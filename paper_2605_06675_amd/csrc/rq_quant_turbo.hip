@@ -251,7 +251,7 @@ template <int BF16>
 __device__ __forceinline__ void turbo_dispatch(const QuantLaunch& a, const uint16_t* Rs,
                                                uint32_t* cbuf, int h, const TBlock& id,
                                                const u4 x[8], int lane) {
-  switch (a.tab.bits[h][id.kind]) {
+  switch (kernarg_byte(&a.tab.bits[0][0], 2 * h + id.kind)) {
     case 1: turbo_block_codes<BF16, 1>(a, Rs, cbuf, h, id, x, lane); break;
     case 2: turbo_block_codes<BF16, 2>(a, Rs, cbuf, h, id, x, lane); break;
     case 3: turbo_block_codes<BF16, 3>(a, Rs, cbuf, h, id, x, lane); break;
