@@ -361,6 +361,55 @@ def stream_ceiling(dev, gib=4, reps=10):
             "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4)}
 
 
+def fused_comparison(wl, kvc, prefill, Q, outs, table, T0, dev, D=8, reps=5):
+    """Decode steps through rq_decode_step (per layer and step: the flush
+    launch when a block leaves the window, then one launch that appends the
+    token and attends) against rq_quantize_kv + rq_decode_attention per
+    layer, over D steps after a prefill of T0 - D tokens (the decode tokens
+    are the prefill's last D), all layers in model order; ms per decode
+    step, median of `reps` runs of each."""
+    import torch
+
+    import paper_2605_06675_amd as rq
+    L = table.shape[0]
+    Tp = T0 - D
+    toks = [[(prefill[l][0][:, :, Tp + s:Tp + s + 1].contiguous(),
+              prefill[l][1][:, :, Tp + s:Tp + s + 1].contiguous()) for s in range(D)]
+            for l in range(L)]
+    # the window, and with it the workspace, varies over the steps
+    ws = torch.zeros(max(rq.rq_decode_workspace(kvc.desc, Tp + s + 1) for s in range(D)),
+                     dtype=torch.uint8, device=dev)
+
+    def run(fused):
+        for l in range(L):
+            rq.rq_quantize_kv(kvc.desc, l, 0, prefill[l][0][:, :, :Tp].contiguous(),
+                              prefill[l][1][:, :, :Tp].contiguous())
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for s in range(D):
+            for l in range(L):
+                k, v = toks[l][s]
+                if fused:
+                    rq.rq_decode_step(kvc.desc, l, Tp + s, k, v, Q[l][0], outs[l], ws)
+                else:
+                    rq.rq_quantize_kv(kvc.desc, l, Tp + s, k, v)
+                    rq.rq_decode_attention(kvc.desc, l, Tp + s + 1, Q[l][0], outs[l], ws)
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / D
+
+    t_sep, t_fus = [], []
+    for _ in range(reps):
+        t_sep.append(run(False))
+        t_fus.append(run(True))
+    sep, fus = float(np.median(t_sep)), float(np.median(t_fus))
+    return {"steps": D, "layers": L, "separate_ms_per_step": round(sep, 3),
+            "fused_ms_per_step": round(fus, 3), "speedup": round(sep / fus, 4),
+            "calls": "rq_quantize_kv + rq_decode_attention vs rq_decode_step, "
+                     "per layer in model order"}
+
+
 def uniform_comparison(wl, kvc, prefill, dec, Q, outs, table, T0, nsteps,
                        rot, dev, reps=10):
     """The paper's zero-overhead claim (Appendix "Runtime Analysis"): decode
@@ -534,6 +583,8 @@ def main():
     ceiling = stream_ceiling(dev)
     uniform = uniform_comparison(wl, kvc, prefill, dec, Q, outs, table, T0,
                                  nsteps, rot, dev)
+    fused = fused_comparison(wl, kvc, prefill, Q, outs, table, T0, dev,
+                             D=max(8, nsteps))
 
     # stage times: medians over the timed steps
     el = lambda p: p[0].elapsed_time(p[1])
@@ -603,6 +654,7 @@ def main():
         "roofline_by_kernel": rooflines,
         "stream_ceiling": ceiling,
         "uniform_vs_mixed": uniform,
+        "decode_step_fused": fused,
         "sensitivity": sens,
     }
     for name, r in rooflines.items():

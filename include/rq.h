@@ -218,6 +218,24 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
                               float scale, void* ws, uint64_t ws_bytes,
                               rq_stream stream);
 
+/* One decode step of one layer: append one token (k, v: device
+ * [batch][n_kv_heads][1][128] in dtype, contiguous) to the n_past cached
+ * ones (0 <= n_past < capacity) and attend over the n_past + 1 tokens with
+ * q, as rq_quantize_kv(n_past, k, v, 1) followed by
+ * rq_decode_attention(n_past + 1) would, with the same cache contents
+ * afterwards and outputs to the same accuracy.  Fused (the per-step path of
+ * Appendix "Runtime Analysis": each layer's append, flush and lookup-and-
+ * dequantize attention in as few launches as possible): the block that
+ * leaves the residual window, if any, is quantized first (one launch),
+ * then one attention launch also writes the new token to the window.
+ * Everything is validated before the first launch: an error leaves the
+ * cache unchanged.  Workspace and overlap rules as rq_decode_attention.
+ * Asynchronous. */
+rq_status rq_decode_step(const rq_cache* c, int32_t layer, int32_t n_past,
+                         const void* k, const void* v, const void* q,
+                         float* out, float scale, void* ws, uint64_t ws_bytes,
+                         rq_stream stream);
+
 /* For callers that cannot allocate device memory (code under stream
  * capture, serving loops, harnesses that forbid allocation):
  * rq_decode_attention with the workspace replaced by the library's own

@@ -27,7 +27,7 @@ EXPORTS = ("rq_version", "rq_last_error", "rq_cache_sizes", "rq_region_offset",
            "rq_fit_distortion", "rq_allocate_bits", "rq_turbo_codebook",
            "rq_sensitivity_workspace", "rq_sensitivity", "rq_cap_weights",
            "rq_fallback_beta", "rq_decode_static_bytes",
-           "rq_decode_attention_static", "rq_read_probe")
+           "rq_decode_attention_static", "rq_read_probe", "rq_decode_step")
 RQ_TURBO_TABLE_FLOATS = 8 * 2 * 256
 
 
@@ -90,6 +90,8 @@ def lib():
             "rq_read_probe": (i32, [vp, u64, vp, i32, vp]),
             "rq_decode_attention_static": (i32, [pc, i32, i32, vp, vp,
                                                  C.c_float, vp]),
+            "rq_decode_step": (i32, [pc, i32, i32, vp, vp, vp, vp, C.c_float,
+                                     vp, u64, vp]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)
@@ -260,6 +262,25 @@ def rq_decode_attention(cache, layer, n_tokens, q, out, ws, scale=None,
         _tptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
+def rq_decode_step(cache, layer, n_past, k, v, q, out, ws, scale=None,
+                   stream=None):
+    """Append one token (k, v: [batch][n_kv_heads][1][128]) after n_past and
+    attend over n_past + 1 tokens with q in one fused call; out, ws as for
+    rq_decode_attention (ws sized for n_past + 1 tokens)."""
+    if scale is None:
+        scale = 1.0 / np.sqrt(128.0)
+    shape = (cache.batch, cache.n_kv_heads, 1, 128)
+    _need_device(k, "k", shape, 2)
+    _need_device(v, "v", shape, 2)
+    _check_attention_args(cache, q, out)
+    if not ws.is_cuda or not ws.is_contiguous():
+        raise ValueError("ws must be a contiguous device tensor")
+    _check(lib().rq_decode_step(
+        C.byref(cache), layer, n_past, _tptr(k), _tptr(v), _tptr(q), _tptr(out),
+        float(scale), _tptr(ws), ws.numel() * ws.element_size(),
+        _stream(stream)))
+
+
 def rq_decode_attention_static(cache, layer, n_tokens, q, out, scale=None,
                                stream=None):
     """rq_decode_attention with the library's own scratch: allocates
@@ -405,6 +426,18 @@ class KVCache:
         n = self.n_tokens[layer]
         rq_decode_attention(self.desc, layer, n, q, out,
                             self.workspace(n, stream), scale, stream)
+        return out
+
+    def decode_step(self, layer, k, v, q, out=None, scale=None, stream=None):
+        """Append one token to `layer` and attend over the cache with q
+        (rq_decode_step)."""
+        import torch
+        if out is None:
+            out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+        n = self.n_tokens[layer]
+        rq_decode_step(self.desc, layer, n, k, v, q, out,
+                       self.workspace(n + 1, stream), scale, stream)
+        self.n_tokens[layer] = n + 1
         return out
 
     def attention_static(self, layer, q, out, scale=None, stream=None):

@@ -1120,6 +1120,11 @@ __device__ __forceinline__ void residual_slot_t(const AttnLaunch& a, int b, int 
   const int cap = a.R + kChunk;
   const uint16_t* kb = a.resid + (((size_t)b * a.H + h) * 2 + 0) * cap * kD;
   const uint16_t* vb = a.resid + (((size_t)b * a.H + h) * 2 + 1) * cap * kD;
+  // a token appended by this call is read from the new input (its window
+  // slot is written below, by the one workgroup whose range holds it)
+  const size_t unit_row = ((size_t)b * a.H + h) * kD;
+  const uint16_t* kn = a.t_new >= 0 ? a.k_new + unit_row : kb;
+  const uint16_t* vn = a.t_new >= 0 ? a.v_new + unit_row : vb;
   uint16_t* ks = stage;
   uint16_t* vs = stage + kResTok * kResRow;
   // a chunk is 64 tokens x 16 pieces of 16 bytes: four pieces per thread
@@ -1130,9 +1135,10 @@ __device__ __forceinline__ void residual_slot_t(const AttnLaunch& a, int b, int 
     for (int i = 0; i < 4; ++i) {
       const int e = tid + i * kThreads, t = e >> 4, piece = e & 15;
       if (t < n) {
-        const size_t row = (size_t)((t0 + t) % cap) * kD + piece * 8;
-        kr[i] = *reinterpret_cast<const u4*>(kb + row);
-        vr[i] = *reinterpret_cast<const u4*>(vb + row);
+        const bool fresh = t0 + t == a.t_new;
+        const size_t row = fresh ? (size_t)piece * 8 : (size_t)((t0 + t) % cap) * kD + piece * 8;
+        kr[i] = *reinterpret_cast<const u4*>((fresh ? kn : kb) + row);
+        vr[i] = *reinterpret_cast<const u4*>((fresh ? vn : vb) + row);
       }
     }
   };
@@ -1155,6 +1161,11 @@ __device__ __forceinline__ void residual_slot_t(const AttnLaunch& a, int b, int 
       if (t < n) {
         *reinterpret_cast<u4*>(ks + t * kResRow + piece * 8) = kr[i];
         *reinterpret_cast<u4*>(vs + t * kResRow + piece * 8) = vr[i];
+        if (t0 + t == a.t_new) {
+          uint16_t* w = a.resid_w + (size_t)(a.t_new % cap) * kD + piece * 8;
+          *reinterpret_cast<u4*>(w + (((size_t)b * a.H + h) * 2 + 0) * cap * kD) = kr[i];
+          *reinterpret_cast<u4*>(w + (((size_t)b * a.H + h) * 2 + 1) * cap * kD) = vr[i];
+        }
       }
     }
     __syncthreads();

@@ -295,7 +295,8 @@ uint64_t decode_counter_bytes(const rq_cache* c) { return attn_counter_bytes(c);
 
 rq_status decode_attention(const rq_cache* c, int32_t layer, int32_t n_tokens, const void* q,
                            float* out, float scale, void* counters, uint64_t counter_cap,
-                           float* part, uint64_t part_cap, rq_stream stream) {
+                           float* part, uint64_t part_cap, rq_stream stream,
+                           const void* k_new, const void* v_new, bool launch) {
   rq_status st = check_cache(c);
   if (st != RQ_OK) return st;
   if (layer < 0 || layer >= c->n_layers)
@@ -348,8 +349,11 @@ rq_status decode_attention(const rq_cache* c, int32_t layer, int32_t n_tokens, c
   a.meta = static_cast<const uint8_t*>(c->meta) + meta_layer_bytes(c) * layer;
   a.resid = static_cast<const uint16_t*>(c->resid) + resid_layer_elems(c) * layer;
   a.out = out;
+  a.t_new = k_new ? n_tokens - 1 : -1;
+  a.k_new = static_cast<const uint16_t*>(k_new);
+  a.v_new = static_cast<const uint16_t*>(v_new);
+  a.resid_w = static_cast<uint16_t*>(c->resid) + resid_layer_elems(c) * layer;
   a.counters = static_cast<uint64_t*>(counters);
-  a.epoch = next_epoch(counters);
   a.part = part;
   a.pstride = part_stride(p);
   a.cstride = counter_stride(c);
@@ -377,6 +381,8 @@ rq_status decode_attention(const rq_cache* c, int32_t layer, int32_t n_tokens, c
   a.tab = tab;
   a.wave_bytes = shape.wave_bytes;
   a.area_bytes = (int)rq::attention_area_bytes(G, a.wave_bytes, c->family);
+  if (!launch) return ok();
+  a.epoch = next_epoch(counters);
   hipError_t e = rq::launch_attention(a, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "attention launch");
   return ok();
@@ -414,23 +420,14 @@ rq_status rq_region_offset(const rq_cache* c, int32_t layer, int32_t head,
   return ok();
 }
 
-rq_status rq_quantize_kv(const rq_cache* c, int32_t layer, int32_t n_past,
-                         const void* k, const void* v, int32_t n_new,
-                         rq_stream stream) {
-  rq_status st = check_cache(c);
-  if (st != RQ_OK) return st;
-  if (layer < 0 || layer >= c->n_layers)
-    return fail(RQ_EINVAL, "layer %d out of range", layer);
-  if (n_past < 0 || n_new < 1 || (int64_t)n_past + n_new > c->capacity)
-    return fail(RQ_EINVAL, "tokens %d + %d exceed capacity %d", n_past, n_new,
-                c->capacity);
-  if (!k || !v || !c->codes || !c->meta || !c->resid)
-    return fail(RQ_EINVAL, "NULL device pointer");
-  const int T_new = n_past + n_new;
-  const int nq_old = n_quantized(n_past, c->residual);
-  const int nq_new = n_quantized(T_new, c->residual);
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+namespace {
 
+// Quantize launch of the blocks that leave the residual window when n_new
+// tokens (k, v: [batch][n_kv_heads][n_new][128]) follow n_past cached ones.
+rq::QuantLaunch quant_launch(const rq_cache* c, int layer, int n_past, const void* k,
+                             const void* v, int n_new) {
+  const int nq_old = n_quantized(n_past, c->residual);
+  const int nq_new = n_quantized(n_past + n_new, c->residual);
   rq::QuantLaunch q{};
   q.k = static_cast<const uint16_t*>(k);
   q.v = static_cast<const uint16_t*>(v);
@@ -454,6 +451,27 @@ rq_status rq_quantize_kv(const rq_cache* c, int32_t layer, int32_t n_past,
     q.cb = c->codebook;
   }
   q.tab = layer_table(c, layer);
+  return q;
+}
+
+}  // namespace
+
+rq_status rq_quantize_kv(const rq_cache* c, int32_t layer, int32_t n_past,
+                         const void* k, const void* v, int32_t n_new,
+                         rq_stream stream) {
+  rq_status st = check_cache(c);
+  if (st != RQ_OK) return st;
+  if (layer < 0 || layer >= c->n_layers)
+    return fail(RQ_EINVAL, "layer %d out of range", layer);
+  if (n_past < 0 || n_new < 1 || (int64_t)n_past + n_new > c->capacity)
+    return fail(RQ_EINVAL, "tokens %d + %d exceed capacity %d", n_past, n_new,
+                c->capacity);
+  if (!k || !v || !c->codes || !c->meta || !c->resid)
+    return fail(RQ_EINVAL, "NULL device pointer");
+  const int T_new = n_past + n_new;
+  const int nq_new = n_quantized(T_new, c->residual);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const rq::QuantLaunch q = quant_launch(c, layer, n_past, k, v, n_new);
   hipError_t e = rq::launch_quantize(q, s);
   if (e != hipSuccess) return hip_fail(e, "quantize launch");
 
@@ -504,6 +522,33 @@ rq_status rq_decode_attention(const rq_cache* c, int32_t layer,
   return rq::decode_attention(c, layer, n_tokens, q, out, scale, ws, cb,
                               reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + cb),
                               ws_bytes - cb, stream);
+}
+
+rq_status rq_decode_step(const rq_cache* c, int32_t layer, int32_t n_past, const void* k,
+                         const void* v, const void* q, float* out, float scale, void* ws,
+                         uint64_t ws_bytes, rq_stream stream) {
+  rq_status st = check_cache(c);
+  if (st != RQ_OK) return st;
+  if (n_past < 0 || n_past >= c->capacity)
+    return fail(RQ_EINVAL, "n_past %d outside 0..%d", n_past, c->capacity - 1);
+  if (!k || !v) return fail(RQ_EINVAL, "NULL new token");
+  if (!ws) return fail(RQ_EINVAL, "NULL workspace");
+  const uint64_t cb = rq::decode_counter_bytes(c);
+  if (ws_bytes < cb)
+    return fail(RQ_ESMALLWS, "workspace of %llu bytes holds no counters (%llu)",
+                (unsigned long long)ws_bytes, (unsigned long long)cb);
+  float* part = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + cb);
+  // everything is checked before the first launch
+  st = rq::decode_attention(c, layer, n_past + 1, q, out, scale, ws, cb, part, ws_bytes - cb,
+                            stream, k, v, false);
+  if (st != RQ_OK) return st;
+  // the block that leaves the window (if any) is quantized first; the new
+  // token itself goes to the window inside the attention kernel
+  const rq::QuantLaunch ql = quant_launch(c, layer, n_past, k, v, 1);
+  hipError_t e = rq::launch_quantize(ql, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "quantize launch");
+  return rq::decode_attention(c, layer, n_past + 1, q, out, scale, ws, cb, part, ws_bytes - cb,
+                              stream, k, v, true);
 }
 
 rq_status rq_calibrate_workspace(int32_t n_comp, int32_t n_tokens,

@@ -79,6 +79,13 @@ struct AttnLaunch {
   const uint8_t* meta;    // this layer
   const uint16_t* resid;  // this layer
   float* out;             // [B][Hq][128]
+  // the token this call appends (fused decode step; t_new < 0: none):
+  // [B][H][128] rows of K and V, read for the attention and written to
+  // window slot t_new mod (R + 32) of this layer's residual window
+  const uint16_t* k_new;
+  const uint16_t* v_new;
+  uint16_t* resid_w;      // this layer's window, writable
+  int t_new;
   float* part;            // [B][H][pstride][G][2 + 128] (max, sum, acc);
                           // slots 0..n_wg-1 streaming, n_wg..n_wg+n_rw-1
                           // the residual window, then one per merge group
@@ -145,9 +152,14 @@ hipError_t launch_sensitivity(const SensLaunch& a, hipStream_t s);
 // bytes, epoch-tagged) and the partial results (part_cap bytes) in the
 // given device buffers: the validation and launch shared by the entry
 // points with a caller's workspace and with the library's own scratch.
+// k_new, v_new: the token this call appends at position n_tokens - 1 (a
+// fused decode step whose flush, if any, has been launched), or NULL.
+// launch = false: validate only.
 rq_status decode_attention(const rq_cache* c, int32_t layer, int32_t n_tokens, const void* q,
                            float* out, float scale, void* counters, uint64_t counter_cap,
-                           float* part, uint64_t part_cap, rq_stream stream);
+                           float* part, uint64_t part_cap, rq_stream stream,
+                           const void* k_new = nullptr, const void* v_new = nullptr,
+                           bool launch = true);
 // Bytes of arrival counters a cache's calls use.
 uint64_t decode_counter_bytes(const rq_cache* c);
 // Record an error message for rq_last_error and return code.
