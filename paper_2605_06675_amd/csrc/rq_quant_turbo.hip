@@ -9,7 +9,9 @@
 // 16-bit rows are loaded straight into matrix-core operands:
 //   keys   D[coord][token] = R . X^T   (the chunk of a token is 32 coords)
 //   values D[token][coord] = X . R^T   (the chunk of a coord is 32 tokens)
-// on v_mfma_f32_16x16x32 (bf16 inputs, or fp16 with R converted exactly).
+// on v_mfma_f32_16x16x32 (bf16 inputs; fp16 inputs with R converted to
+// fp16, exact for the entries of magnitude 2^-17 and above, about one entry
+// of a Haar matrix rounding to the fp16 subnormal grid, by at most 2^-25).
 // Norms are summed in fp64 from the same registers.  Codes count the
 // positive thresholds below |t| (the codebook is symmetric, with the middle
 // threshold at 0) and go, as bytes, through a small LDS buffer from which
@@ -46,8 +48,9 @@ __device__ __forceinline__ float wid(uint32_t w16) {
   return (float)__builtin_bit_cast(_Float16, (uint16_t)w16);
 }
 
-// bf16 -> fp16 bit pattern (exact for the entries of an orthogonal matrix
-// above 2^-24 in magnitude; smaller ones round to the fp16 subnormal grid)
+// bf16 -> fp16 bit pattern: exact for |r| >= 2^-17 (the 8 significant bits
+// of a bf16 value fit the fp16 grid there); smaller entries round to the
+// fp16 subnormal grid (spacing 2^-24)
 __device__ __forceinline__ uint32_t bf16_to_f16(uint32_t b) {
   return __builtin_bit_cast(uint16_t, (_Float16)__uint_as_float(b << 16));
 }
