@@ -471,10 +471,7 @@ rq_status rq_quantize_kv(const rq_cache* c, int32_t layer, int32_t n_past,
   const int T_new = n_past + n_new;
   const int nq_new = n_quantized(T_new, c->residual);
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  const rq::QuantLaunch q = quant_launch(c, layer, n_past, k, v, n_new);
-  hipError_t e = rq::launch_quantize(q, s);
-  if (e != hipSuccess) return hip_fail(e, "quantize launch");
-
+  rq::QuantLaunch q = quant_launch(c, layer, n_past, k, v, n_new);
   rq::RingLaunch r{};
   r.k = q.k;
   r.v = q.v;
@@ -486,8 +483,21 @@ rq_status rq_quantize_kv(const rq_cache* c, int32_t layer, int32_t n_past,
   r.R = c->residual;
   r.t_lo = nq_new > n_past ? nq_new : n_past;
   r.t_hi = T_new;
-  e = rq::launch_ring(r, s);
-  if (e != hipSuccess) return hip_fail(e, "window launch");
+  // The quantize launch also copies the window rows unless a row it writes
+  // could take the ring slot of a token a flushed block still reads there
+  // (tokens [nq_old, min(nq_new, n_past)) are read from the ring): then the
+  // window waits for its own launch.
+  const int nq_old = n_quantized(n_past, c->residual);
+  const int read_hi = nq_new < n_past ? nq_new : n_past;
+  const bool reads_ring = nq_old < read_hi;
+  q.ring = r;
+  q.ring_fused = q.nblk > 0 && (!reads_ring || T_new - 1 - nq_old < c->residual + rq::kChunk);
+  hipError_t e = rq::launch_quantize(q, s);
+  if (e != hipSuccess) return hip_fail(e, "quantize launch");
+  if (!q.ring_fused) {
+    e = rq::launch_ring(r, s);
+    if (e != hipSuccess) return hip_fail(e, "window launch");
+  }
   return ok();
 }
 

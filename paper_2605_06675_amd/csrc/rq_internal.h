@@ -48,6 +48,14 @@ struct FieldPosTab {
   int8_t v[9][4];
 };
 
+struct RingLaunch {
+  const uint16_t* k;
+  const uint16_t* v;
+  uint16_t* resid;        // this layer's rings
+  int B, H, n_new, n_past, R;
+  int t_lo, t_hi;         // tokens [t_lo, t_hi) go to the window
+};
+
 struct QuantLaunch {
   const uint16_t* k;      // [B][H][n_new][128]
   const uint16_t* v;
@@ -57,20 +65,14 @@ struct QuantLaunch {
   int B, H, n_new, n_past, cap, R;
   int blk0, nblk;         // blocks [blk0, blk0 + nblk) get quantized
   int kind_lo, kind_n;    // kinds kind_lo .. kind_lo + kind_n - 1 (K = 0, V = 1)
+  RingLaunch ring;        // window rows this launch also copies
+  int ring_fused;         // (when set; else the window has its own launch)
   int is_bf16;
   int family;
   int n_cu;               // compute units of the device (grid sizing)
   const uint16_t* rot;    // TurboQuant: this layer's rotations [H][128][128] bf16
   const float* cb;        // TurboQuant: codebook table (rq_turbo_codebook)
   LayerTable tab;
-};
-
-struct RingLaunch {
-  const uint16_t* k;
-  const uint16_t* v;
-  uint16_t* resid;        // this layer's rings
-  int B, H, n_new, n_past, R;
-  int t_lo, t_hi;         // tokens [t_lo, t_hi) go to the window
 };
 
 struct AttnLaunch {

@@ -10,26 +10,13 @@
 // every code goes straight into its packed word.
 #include "rq_device.h"
 #include "rq_internal.h"
+#include "rq_ring.h"
 
 namespace rq {
 
 namespace {
 
 constexpr int kWave = 64;
-
-// Source of token t of a unit: the new input for t >= n_past, else the
-// residual window.
-__device__ __forceinline__ const uint16_t* token_src(const QuantLaunch& a,
-                                                     int b, int h, int kind,
-                                                     int t) {
-  if (t >= a.n_past) {
-    const uint16_t* base = kind ? a.v : a.k;
-    return base + ((size_t)(b * a.H + h) * a.n_new + (t - a.n_past)) * kD;
-  }
-  const int cap = a.R + kChunk;
-  return a.resid +
-         ((((size_t)b * a.H + h) * 2 + kind) * cap + (t % cap)) * kD;
-}
 
 __device__ __forceinline__ int pair_pos(int j) {
   return j < 16 ? 2 * j : 2 * (j - 16) + 1;
@@ -38,7 +25,7 @@ __device__ __forceinline__ int pair_pos(int j) {
 template <int B>
 __device__ __forceinline__ void store_words(uint32_t* dst, const uint32_t w[B]) {
 #pragma unroll
-  for (int i = 0; i < B; ++i) dst[i] = w[i];
+  for (int i = 0; i < B; ++i) __builtin_nontemporal_store(w[i], dst + i);
 }
 
 template <int B>
@@ -147,11 +134,14 @@ template <int B> struct ChunkAcc {
   }
 };
 
+// Code and metadata stores are non-temporal: written once per call and
+// read by later calls, they need not stay in the L2 (whose dirty lines the
+// end of the launch would otherwise write back).
 template <int B>
 __device__ __forceinline__ void store_chunk(uint32_t* dst, const uint32_t* w) {
   RQ_GLOBAL uint32_t* g = gptr(dst);
 #pragma unroll
-  for (int i = 0; i < B; ++i) g[i] = w[i];
+  for (int i = 0; i < B; ++i) __builtin_nontemporal_store(w[i], g + i);
 }
 
 struct BlockId {
@@ -206,7 +196,7 @@ __device__ __forceinline__ void store_meta(const QuantLaunch& a, const KiviSmem&
   RQ_GLOBAL u2* m = gptr(reinterpret_cast<u2*>(
       a.meta + meta_unit_offset(a.family, id.h, id.kind, id.b, a.B, nblk_cap) +
       (size_t)id.blk * kMetaBlockKivi));
-  m[lane] = reinterpret_cast<const u2*>(sm.meta)[lane];
+  __builtin_nontemporal_store(reinterpret_cast<const u2*>(sm.meta)[lane], m + lane);
 }
 
 // Keys: scale and zero per channel over the block's 32 tokens; chunk q of
@@ -399,6 +389,7 @@ kivi_quant_kernel(QuantLaunch a) {
   const int total = a.nblk * a.H * a.B * a.kind_n;
   const int stride = gridDim.x * kQWaves;
   int it = blockIdx.x * kQWaves + wave;
+  if (a.ring_fused) copy_window(a.ring, it, stride, lane);
   if (it >= total) return;
   u4 v[8];
   load_block(a, block_id(a, it), v, lane);
@@ -424,10 +415,17 @@ __device__ __forceinline__ float dpp_xor2(float v) {
 }
 
 // One quarter of token t (channels 32 q .. 32 q + 31) into registers.
+// The row address selects between the new input and the residual window
+// without a branch around the loads (a divergent branch there would read
+// the input pointers with vector loads and wait for every load in flight).
 __device__ __forceinline__ void load_quarter(const QuantLaunch& a, int b, int h,
                                              int kind, int t, int q, u4 raw[4]) {
-  const RQ_GLOBAL u4* s = gptr(reinterpret_cast<const u4*>(
-      token_src(a, b, h, kind, t) + 32 * q));
+  const uint16_t* in = (kind ? a.v : a.k) + (size_t)(b * a.H + h) * a.n_new * kD;
+  const int cap = a.R + kChunk;
+  const uint16_t* ring = a.resid + (((size_t)b * a.H + h) * 2 + kind) * cap * kD;
+  const uint16_t* row = t >= a.n_past ? in + (size_t)(t - a.n_past) * kD
+                                      : ring + (size_t)(t % cap) * kD;
+  const RQ_GLOBAL u4* s = gptr(reinterpret_cast<const u4*>(row + 32 * q));
 #pragma unroll
   for (int i = 0; i < 4; ++i) raw[i] = s[i];
 }
@@ -562,6 +560,9 @@ sym_quant_kernel(QuantLaunch a) {
   const int h = blockIdx.y;
   const int b = blockIdx.z / a.kind_n, kind = a.kind_lo + blockIdx.z % a.kind_n;
   const int lane = threadIdx.x;
+  if (a.ring_fused)
+    copy_window(a.ring, (blockIdx.z * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x,
+                gridDim.x * gridDim.y * gridDim.z, lane);
   switch (kernarg_byte(&a.tab.bits[0][0], 2 * h + kind)) {
     case 2: sym_block<ROT, BF16, 2>(a, sm, b, h, kind, blk, lane); break;
     case 3: sym_block<ROT, BF16, 3>(a, sm, b, h, kind, blk, lane); break;
@@ -577,7 +578,8 @@ sym_quant_kernel(QuantLaunch a) {
   uint8_t* m = a.meta + meta_unit_offset(a.family, h, kind, b, a.B, nblk_cap) +
                (size_t)blk * kMetaBlockTok;
   const uint32_t* src = reinterpret_cast<const uint32_t*>(sm.meta);
-  if (lane < kMetaBlockTok / 4) reinterpret_cast<uint32_t*>(m)[lane] = src[lane];
+  if (lane < kMetaBlockTok / 4)
+    __builtin_nontemporal_store(src[lane], reinterpret_cast<uint32_t*>(m) + lane);
 }
 
 __global__ void __launch_bounds__(kWave)
@@ -651,6 +653,7 @@ hipError_t launch_quantize(const QuantLaunch& a, hipStream_t s) {
     hipError_t e = launch_kivi(q, s);
     if (e != hipSuccess) return e;
     q.kind_lo = 1;
+    q.ring_fused = 0;   // copied by the keys' launch
     return launch_sym(q, false, s);
   }
   return launch_sym(q, a.family == RQ_QUAROT, s);

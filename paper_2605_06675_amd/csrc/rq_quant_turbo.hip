@@ -18,6 +18,7 @@
 // each lane packs whole chunks.
 #include "rq_device.h"
 #include "rq_internal.h"
+#include "rq_ring.h"
 
 namespace rq {
 
@@ -245,7 +246,7 @@ __device__ __forceinline__ void turbo_block_codes(const QuantLaunch& a, const ui
     pack_chunk<B>(c, w);
     RQ_GLOBAL uint32_t* dst = gptr(base + (size_t)unit * B);
 #pragma unroll
-    for (int i = 0; i < B; ++i) dst[i] = w[i];
+    for (int i = 0; i < B; ++i) __builtin_nontemporal_store(w[i], dst + i);
   }
   __builtin_amdgcn_wave_barrier();
 }
@@ -295,17 +296,22 @@ turbo_quant_kernel(QuantLaunch a) {
   const int per_head = a.nblk * a.B * 2;
   const int stride = gridDim.x * kTWaves;
   int it = blockIdx.x * kTWaves + wave;
-  if (it >= per_head) return;
-  u4 nx[8];
-  load_x(a, h, turbo_block(a, it), nx, lane);
-  for (; it < per_head; it += stride) {
-    const TBlock id = turbo_block(a, it);
-    u4 x[8];
+  if (it < per_head) {
+    u4 nx[8];
+    load_x(a, h, turbo_block(a, it), nx, lane);
+    for (; it < per_head; it += stride) {
+      const TBlock id = turbo_block(a, it);
+      u4 x[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) x[i] = nx[i];
-    if (it + stride < per_head) load_x(a, h, turbo_block(a, it + stride), nx, lane);
-    turbo_dispatch<BF16>(a, Rs, cbuf, h, id, x, lane);
+      for (int i = 0; i < 8; ++i) x[i] = nx[i];
+      if (it + stride < per_head) load_x(a, h, turbo_block(a, it + stride), nx, lane);
+      turbo_dispatch<BF16>(a, Rs, cbuf, h, id, x, lane);
+    }
   }
+  // the window rows of the append, after the blocks (fewer live registers)
+  if (a.ring_fused)
+    copy_window(a.ring, (blockIdx.y * gridDim.x + blockIdx.x) * kTWaves + wave,
+                gridDim.x * gridDim.y * kTWaves, lane);
 }
 
 }  // namespace
