@@ -365,41 +365,6 @@ def stream_ceiling(dev, gib=4, reps=10):
             "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4)}
 
 
-def launch_times(kvc, prefill, dec, Q, outs, L, T0, nsteps, ws, reps=5):
-    """Average duration of one launch of the dominant kernels, from HIP
-    events around each call (so the gaps between launches are left out):
-    the prefill quantize of each layer (one launch: the quantize kernel also
-    writes the window) and the decode attention of each layer after the
-    decode tokens; median over `reps` passes.  Leaves the cache as the timed
-    steps do."""
-    import torch
-
-    import paper_2605_06675_amd as rq
-    ev = lambda: torch.cuda.Event(enable_timing=True)
-    q_us, a_us = [], []
-    for _ in range(reps):
-        eq, ea = [], []
-        for l in range(L):
-            a, b = ev(), ev()
-            a.record()
-            rq.rq_quantize_kv(kvc.desc, l, 0, prefill[l][0], prefill[l][1])
-            b.record()
-            eq.append((a, b))
-        for l in range(L):
-            for s in range(nsteps):
-                rq.rq_quantize_kv(kvc.desc, l, T0 + s, dec[l][0][s], dec[l][1][s])
-        for l in range(L):
-            a, b = ev(), ev()
-            a.record()
-            rq.rq_decode_attention(kvc.desc, l, T0 + nsteps, Q[l][nsteps - 1], outs[l], ws)
-            b.record()
-            ea.append((a, b))
-        torch.cuda.synchronize()
-        q_us.append(1e3 * float(np.mean([a.elapsed_time(b) for a, b in eq])))
-        a_us.append(1e3 * float(np.mean([a.elapsed_time(b) for a, b in ea])))
-    return float(np.median(q_us)), float(np.median(a_us))
-
-
 def fused_comparison(wl, kvc, prefill, Q, outs, table, T0, dev, D=8, reps=5):
     """Decode steps through rq_decode_step (per layer and step: the flush
     launch when a block leaves the window, then one launch that appends the
@@ -624,8 +589,6 @@ def main():
         ceiling = stream_ceiling(dev)
         uniform = uniform_comparison(wl, kvc, prefill, dec, Q, outs, table, T0,
                                      nsteps, rot, dev)
-    q_launch_us, a_launch_us = launch_times(kvc, prefill, dec, Q, outs, L, T0,
-                                            nsteps, ws)
     if not args.no_extras:
         fused = fused_comparison(wl, kvc, prefill, Q, outs, table, T0, dev,
                                  D=max(8, nsteps))
@@ -644,15 +607,16 @@ def main():
     q_tok_s = B * T0 / (ms["quantize"] * 1e-3)
     q_gbs = q_bytes / (ms["quantize"] * 1e-3) / 1e9
     qk = QUANT_KERNEL[wl.family]
-    # per launch: bytes of one launch over its own duration (events around
-    # each call); the phase rates above include the gaps between launches
+    # per launch: the phase time over its launches (back to back on the
+    # stream, one kernel per call; events around single calls would add the
+    # dispatch and drain of each launch, which back-to-back launches overlap)
     kernels = {
         qk: {"call": f"rq_quantize_kv prefill of one layer ({T0} tokens; the "
                      "launch also writes the window)",
-             "bytes": q_bytes / L, "us": q_launch_us},
-        "attn_kernel": {"call": f"rq_decode_attention of one layer ({T0 + nsteps} tokens)",
-                        "bytes": attention_bytes(wl, table, T0 + nsteps) / L,
-                        "us": a_launch_us},
+             "bytes": q_bytes / L, "us": ms["quantize"] * 1e3 / L},
+        "attn_kernel": {"call": "rq_decode_attention of one layer",
+                        "bytes": att_bytes / (L * nsteps),
+                        "us": ms["attention"] * 1e3 / (L * nsteps)},
     }
     rooflines = {}
     for name, k in kernels.items():
