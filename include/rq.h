@@ -47,12 +47,16 @@
  *             summed in fp32 on the matrix cores, so a coordinate whose t
  *             lies within the rounding of that sum of a threshold may take
  *             the neighbouring code; everything else is exact.
- *  - Packed chunk: 32 codes of one stream in exactly b uint32 words.  The
- *    code bits are split into planes of widths equal to the binary digits
- *    of b, widest first (3 -> 2+1, 5 -> 4+1, 6 -> 4+2, 7 -> 4+2+1); plane
- *    width w occupies w words, and its word d holds the field of code
- *    d*16/w + k at bit k*w and that of code 16 + d*16/w + k at bit
- *    16 + k*w, for k = 0 .. 16/w - 1.
+ *  - Packed chunk: 32 codes of one stream in exactly b uint32 words.
+ *    b = 3: one 3-bit field per code.  The three words form a 96-bit
+ *    stream (stream bit 32k + j = bit j of word k) of four 24-bit
+ *    quarters; quarter q holds code 4q + i at stream bit 24q + 3i and
+ *    code 16 + 4q + i at stream bit 24q + 12 + 3i (i = 0..3).
+ *    Other widths: the code bits are split into planes of widths equal
+ *    to the binary digits of b, widest first (5 -> 4+1, 6 -> 4+2,
+ *    7 -> 4+2+1); plane width w occupies w words, and its word d holds
+ *    the field of code d*16/w + k at bit k*w and that of code
+ *    16 + d*16/w + k at bit 16 + k*w, for k = 0 .. 16/w - 1.
  *  - Pair order of 32 entries: 0,16,1,17,...,15,31.
  *
  * Cache layout (one buffer each; the caller allocates the sizes reported by

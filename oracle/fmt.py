@@ -7,14 +7,25 @@ Footprint").  It does not fix a byte layout; the one below is this
 library's, and packed codes are compared bit for bit against it.
 
 Chunk: 32 codes of one b-bit stream (b = 1..8) occupy exactly b 32-bit
-words.  The code bits are split into planes whose widths are the binary
-digits of b, widest first (b=3 -> 2,1; b=5 -> 4,1; b=6 -> 4,2; b=7 -> 4,2,1;
+words.  Words are little-endian uint32.
+
+b = 3: every code is one 3-bit field.  The three words form one 96-bit
+stream (stream bit 32k + j is bit j of word k), cut into four quarters of
+24 bits; quarter q (0..3) holds, for i = 0..3,
+    code  4q + i       at stream bit  24q + 3i,
+    code  16 + 4q + i  at stream bit  24q + 12 + 3i,
+so that moving the upper 12 bits of a quarter up by 4 puts codes
+(4q + i, 16 + 4q + i) at bits (3i, 16 + 3i) of one word.  Two fields cross
+a word boundary (codes 6 and 25).
+
+Other widths: the code bits are split into planes whose widths are the
+binary digits of b, widest first (b=5 -> 4,1; b=6 -> 4,2; b=7 -> 4,2,1;
 b=1,2,4,8 -> one plane); plane p holds code bits [o_p, o_p + w_p).  A plane
 of width w is w words; word d of it holds, for k = 0 .. 16/w - 1,
     the field of code  d*16/w + k       at bit  k*w,
     the field of code  16 + d*16/w + k  at bit  16 + k*w,
 so that every 16-bit half-word pair (bit k*w, bit 16 + k*w) carries codes
-(i, i + 16).  Words are little-endian uint32.
+(i, i + 16).
 
 Pair order of a 32-entry sequence s[0..31]: s[0], s[16], s[1], s[17], ...,
 s[15], s[31].  Per-group metadata is stored in pair order.
@@ -26,10 +37,41 @@ F16_MAX = 65504.0
 
 
 def planes(b):
-    """Plane widths of a b-bit code, widest first."""
+    """Plane widths of a b-bit code, widest first (b = 3: one field)."""
     if not 1 <= b <= 8:
         raise ValueError("bits must be in 1..8")
+    if b == 3:
+        return [3]
     return [w for w in (8, 4, 2, 1) if b & w]
+
+
+def stream3_bit(i):
+    """Stream bit of code i (0..31) of a three-bit chunk."""
+    j = i % 16
+    return 24 * (j // 4) + 3 * (j % 4) + (12 if i >= 16 else 0)
+
+
+def _pack3(codes, out):
+    for i in range(CHUNK):
+        pos = stream3_bit(i)
+        word, bit = divmod(pos, 32)
+        c = codes[..., i]
+        out[..., word] |= (c << np.uint32(bit)) & np.uint32(0xFFFFFFFF)
+        if bit + 3 > 32:
+            out[..., word + 1] |= c >> np.uint32(32 - bit)
+    return out
+
+
+def _unpack3(words, codes):
+    x = [words[..., k].astype(np.int64) for k in range(3)]
+    for i in range(CHUNK):
+        pos = stream3_bit(i)
+        word, bit = divmod(pos, 32)
+        v = x[word] >> bit
+        if bit + 3 > 32:
+            v = v | (x[word + 1] << (32 - bit))
+        codes[..., i] = v & 7
+    return codes
 
 
 def pack_chunks(codes, b):
@@ -39,6 +81,8 @@ def pack_chunks(codes, b):
     if np.any(codes >> b):
         raise ValueError("code out of range")
     out = np.zeros(codes.shape[:-1] + (b,), dtype=np.uint32)
+    if b == 3:
+        return _pack3(codes, out)
     word = 0
     shift = 0
     for w in planes(b):
@@ -62,6 +106,8 @@ def unpack_chunks(words, b):
     words = np.asarray(words, dtype=np.uint32)
     assert words.shape[-1] == b
     codes = np.zeros(words.shape[:-1] + (CHUNK,), dtype=np.int64)
+    if b == 3:
+        return _unpack3(words, codes)
     word = 0
     shift = 0
     for w in planes(b):

@@ -32,9 +32,9 @@ size_t attention_area_bytes(int G, int wave_bytes, int family) {
 }
 
 size_t attention_tail_bytes(int G, int family) {
-  // TurboQuant: the rotated query rows and two fp16 centroid tables
+  // TurboQuant: the rotated query rows and the K and V code tables
   return (size_t)G * kD * sizeof(uint16_t) +
-         (family == RQ_TURBO ? (size_t)G * kD * sizeof(float) + 2 * 256 * sizeof(uint16_t) : 0);
+         (family == RQ_TURBO ? (size_t)G * kD * sizeof(float) + 2 * kTqTabBytes : 0);
 }
 
 size_t attention_lds_bytes(int G, int wave_bytes, int family) {

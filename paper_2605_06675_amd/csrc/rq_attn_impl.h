@@ -121,6 +121,7 @@ __host__ __device__ __forceinline__ constexpr int kshift(int b, int i) {
   return cur;
 }
 __host__ __device__ __forceinline__ constexpr int kpos(int b, int i) {
+  if (b == 3) return (i & 3) < 3 ? 3 * (i & 3) : 0;   // see kpair<3>
   const int w = plane_w(b, 0);
   return (i % (16 / w)) * w - kshift(b, i);
 }
@@ -136,6 +137,7 @@ __host__ __device__ __forceinline__ constexpr int vshift(int b, int i) {
   return cur;
 }
 __host__ __device__ __forceinline__ constexpr int vpos(int b, int i) {
+  if (b == 3) return i < 3 ? 3 * i : 0;               // see vpairs<3>
   const int w = plane_w(b, 0);
   return (w == 8 ? 8 * (i & 1) : i * w) - vshift(b, i);
 }
@@ -221,8 +223,37 @@ __device__ __forceinline__ uint32_t pk_fms(uint32_t a, uint32_t b, uint32_t c) {
 // fp16 pair (u_i 2^(P-24), u_{i+16} 2^(P-24)) of key pair i of a chunk (its
 // B words), P = kpos(B, i): the fields masked into the mantissa of a zero
 // exponent, exact subnormals.
+// Three-bit chunks (single fields in four 24-bit quarters of the 96-bit
+// stream of the chunk's words): quarter x (at bits 0..23 of x) with its
+// upper 12 bits moved up by 4, so that slot s (codes 4q+s, 16+4q+s) sits
+// at bits (3s, 16+3s).  Bits above 27 are left over from the neighbouring
+// quarter and never selected.
+__device__ __forceinline__ uint32_t spread3(uint32_t x) {
+  return insert(x, 0xffffu, x << 4);
+}
+// quarter q (a constant after unrolling) of a chunk's three words, spread
+__device__ __forceinline__ uint32_t quarter3(const uint32_t* wds, int q) {
+  if (q == 0) return spread3(wds[0]);
+  if (q == 1) return spread3(__builtin_amdgcn_alignbit(wds[1], wds[0], 24));
+  if (q == 2) return spread3(__builtin_amdgcn_alignbit(wds[2], wds[1], 16));
+  return spread3(wds[2] >> 8);
+}
+// quarter r (per lane) of the chunk at ch, spread: one aligned funnel
+// shift of words (24r / 32, 24r / 32 + 1).  For r = 3 the second word is
+// the one after the chunk; the bits taken from it land above bit 27.
+__device__ __forceinline__ uint32_t lane_quarter3(const uint32_t* ch, int r) {
+  const int w = (24 * r) >> 5;
+  return spread3(__builtin_amdgcn_alignbit(ch[w + 1], ch[w], (24 * r) & 31));
+}
+// slot s of a spread quarter as a pair of fields at bits (P, 16+P), P =
+// 3s for s < 3 and 0 for s = 3 (a field at bit 9 would reach the exponent)
+__device__ __forceinline__ uint32_t slot3(uint32_t z, int s) {
+  return s < 3 ? z & (pair_mask(3) << (3 * s)) : (z >> 9) & pair_mask(3);
+}
+
 template <int B>
 __device__ __forceinline__ uint32_t kpair(const uint32_t* wds, int i) {
+  if constexpr (B == 3) return slot3(quarter3(wds, i >> 2), i & 3);
   constexpr int w0 = plane_w(B, 0);
   const int P = kpos(B, i);
   uint32_t acc = (wds[i / (16 / w0)] >> kshift(B, i)) & (pair_mask(w0) << P);
@@ -240,7 +271,11 @@ __device__ __forceinline__ uint32_t kpair(const uint32_t* wds, int i) {
 template <int B>
 __device__ __forceinline__ void vpairs(const uint32_t* ch, int r, uint32_t out[4]) {
   constexpr int w0 = plane_w(B, 0);
-  if constexpr (w0 == 8) {
+  if constexpr (B == 3) {
+    const uint32_t z = lane_quarter3(ch, r);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) out[i] = slot3(z, i);
+  } else if constexpr (w0 == 8) {
     const uint32_t x = ch[2 * r], y = ch[2 * r + 1];
     out[0] = x & pair_mask(8);
     out[1] = (x >> 8) & pair_mask(8);
@@ -267,9 +302,13 @@ __device__ __forceinline__ void vpairs(const uint32_t* ch, int r, uint32_t out[4
 
 // ------------------------------------------------------------- TurboQuant
 // Codes (i, i + 16) of a chunk as integers at bits 0 and 16 (i < 16 after
-// unrolling, or a per-lane quarter base plus a constant).
+// unrolling, or, for widths other than three, a per-lane quarter base plus
+// a constant).
 template <int B>
 __device__ __forceinline__ uint32_t tq_code_pair(const uint32_t* wds, int i) {
+  // three bits: the fields at bits (0, 16), other bits not cleared (the
+  // three-bit table lookup reads only bits 0..2 and 16..18)
+  if constexpr (B == 3) return quarter3(wds, i >> 2) >> (3 * (i & 3));
   uint32_t f = 0;
 #pragma unroll
   for (int p = 0; p < plane_n(B); ++p) {
@@ -280,46 +319,26 @@ __device__ __forceinline__ uint32_t tq_code_pair(const uint32_t* wds, int i) {
   return f;
 }
 
-// fp16 centroid pair of a code pair f (codes at bits 0 and 16).  lut: the
-// centroids as fp16 pairs -- b <= 2: all of them in order; b = 3, 4: the
-// positive half (codes 2^(b-1) ..), the negative half being its mirror
-// image (centroid 2^b - 1 - u = -centroid u).
+// fp16 centroid pair of a code pair f (codes at bits 0 and 16, widths 1
+// and 2).  lut: the 2^b centroids as fp16 pairs in code order.
 template <int B>
 __device__ __forceinline__ uint32_t tq_lut(uint32_t f, const uint32_t* lut) {
-  if constexpr (B == 1) {
-    return lut[0] | ((~f & 0x00010001u) << 15);
-  } else if constexpr (B == 2) {
-    return __builtin_amdgcn_perm(lut[1], lut[0], f * 0x202u + 0x01000100u);
-  } else if constexpr (B == 3) {
-    const uint32_t neg = (~f >> 2) & 0x00010001u;
-    const uint32_t m = (f ^ (neg * 3u)) & 0x00030003u;
-    return __builtin_amdgcn_perm(lut[1], lut[0], m * 0x202u + 0x01000100u) | (neg << 15);
-  } else {
-    const uint32_t neg = (~f >> 3) & 0x00010001u;
-    const uint32_t m = (f ^ (neg * 7u)) & 0x00070007u;
-    const uint32_t sel = (m & 0x00030003u) * 0x202u + 0x01000100u;
-    const uint32_t lo = __builtin_amdgcn_perm(lut[1], lut[0], sel);
-    const uint32_t hi = __builtin_amdgcn_perm(lut[3], lut[2], sel);
-    const uint32_t pick = ((m >> 2) & 0x00010001u) * 0xFFFFu;
-    return ((hi & pick) | (lo & ~pick)) | (neg << 15);
-  }
+  static_assert(B <= 2, "register tables hold widths 1 and 2");
+  if constexpr (B == 1) return lut[0] | ((~f & 0x00010001u) << 15);
+  else return __builtin_amdgcn_perm(lut[1], lut[0], f * 0x202u + 0x01000100u);
 }
 
-// fp16 lookup table of the b-bit codebook (layout of tq_lut) from the fp32
-// centroid table
-__device__ __forceinline__ void tq_make_lut(const float* cb, int b, uint32_t lut[4]) {
+// fp16 lookup table of the b-bit codebook (b <= 2, layout of tq_lut) from
+// the fp32 centroid table
+__device__ __forceinline__ void tq_make_lut(const float* cb, int b, uint32_t lut[2]) {
   const float* c = cb + (b - 1) * 512 + 256;
-  const int first = b <= 2 ? 0 : (1 << (b - 1));
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const int e0 = first + 2 * k, e1 = e0 + 1;
-    const float c0 = e0 < (1 << b) ? c[e0] : 0.0f, c1 = e1 < (1 << b) ? c[e1] : 0.0f;
-    const h2 v = {(_Float16)c0, (_Float16)c1};
-    lut[k] = as_u32(v);
-  }
   if (b == 1) {
     const h2 v = {(_Float16)c[1], (_Float16)c[1]};
-    lut[0] = as_u32(v);
+    lut[0] = lut[1] = as_u32(v);
+  } else {
+    const h2 v0 = {(_Float16)c[0], (_Float16)c[1]}, v1 = {(_Float16)c[2], (_Float16)c[3]};
+    lut[0] = as_u32(v0);
+    lut[1] = as_u32(v1);
   }
 }
 
@@ -337,6 +356,25 @@ __device__ __forceinline__ uint32_t tq_code2_pair(const uint32_t* wds, int i) {
 }
 
 typedef __attribute__((address_space(3))) const _Float16 lds_h;
+typedef __attribute__((address_space(3))) const uint32_t lds_u32;
+typedef uint16_t us2v __attribute__((ext_vector_type(2)));
+
+// LDS tables of a TurboQuant width, one 1 KiB area per side (K, V):
+// widths 3 and 4 hold every code pair (u, v) as the fp16 pair
+// (centroid u, centroid v) at entry u + 2^b v; widths 5..8 hold the 2^b
+// fp16 centroids.
+constexpr int kTqTabBytes = 1024;
+
+// fp16 centroid pair of code pair f (codes at bits 0 and 16, nothing else
+// set; widths 3 and 4) from the pair table: the byte offset 4 u + 2^(b+2) v
+// is one two-way dot product of f's halves
+template <int B>
+__device__ __forceinline__ uint32_t tq_tab(uint32_t f, lds_h* tab) {
+  const uint32_t base = (uint32_t)(uintptr_t)tab;
+  const us2v w = {4, (uint16_t)(4 << B)};
+  const uint32_t off = __builtin_amdgcn_udot2(__builtin_bit_cast(us2v, f), w, base, false);
+  return *(lds_u32*)(uintptr_t)off;
+}
 
 // fp16 centroid pair of a doubled code pair f from an LDS table of 2^b fp16
 // centroids (widths 5..8; two 16-bit LDS reads straight into the halves)
@@ -352,7 +390,8 @@ __device__ __forceinline__ uint32_t tq_lds(uint32_t f, lds_h* tab) {
 template <int B>
 __device__ __forceinline__ uint32_t tq_pair(const uint32_t* wds, int i, const uint32_t* lut,
                                             lds_h* tab) {
-  if constexpr (B <= 4) return tq_lut<B>(tq_code_pair<B>(wds, i), lut);
+  if constexpr (B <= 2) return tq_lut<B>(tq_code_pair<B>(wds, i), lut);
+  else if constexpr (B <= 4) return tq_tab<B>(tq_code_pair<B>(wds, i) & pair_mask(B), tab);
   else return tq_lds(tq_code2_pair<B>(wds, i), tab);
 }
 
@@ -388,10 +427,10 @@ struct LaneOps {
   float cK;         // qscale 2^(24+e) (codes as subnormals) or qscale 2^e
                     // (TurboQuant), qscale = scale * log2(e)
   float eK;         // KIVI: qscale 2^e (the zero-point sum)
-  uint32_t lutk[4]; // TurboQuant: fp16 centroid tables of the K and V widths
-  uint32_t lutv[4]; //   (widths <= 4)
-  lds_h* tabk;      // TurboQuant: fp16 centroids of the K and V widths in LDS
-  lds_h* tabv;      //   (widths >= 5)
+  uint32_t lutk[2]; // TurboQuant: fp16 centroid tables of the K and V widths
+  uint32_t lutv[2]; //   (widths <= 2)
+  lds_h* tabk;      // TurboQuant: LDS tables of the K and V widths (pairs
+  lds_h* tabv;      //   for widths 3, 4; centroids for widths >= 5)
   int r, col, lane;
   int gsub;         // col / GP
   int GP;           // queries per replica (power of two >= G)
@@ -561,8 +600,14 @@ __device__ __forceinline__ void vpart(const SlotPtrs& sp, const LaneOps& lo,
     uint32_t pr[4];
     if constexpr (FAM == RQ_TURBO) {
       const uint32_t* ch = sp.vc + (16 * nt + col) * BV;
+      if constexpr (BV == 3) {
+        const uint32_t z = lane_quarter3(ch, r);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) pr[i] = tq_pair<BV>(ch, 4 * r + i, lo.lutv, lo.tabv);
+        for (int i = 0; i < 4; ++i) pr[i] = tq_tab<3>((z >> (3 * i)) & pair_mask(3), lo.tabv);
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) pr[i] = tq_pair<BV>(ch, 4 * r + i, lo.lutv, lo.tabv);
+      }
     } else {
       vpairs<BV>(sp.vc + (16 * nt + col) * BV, r, pr);
     }
@@ -1314,18 +1359,22 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int n
     const int j = lo.col & (a.GP - 1);
     float qv[32];
     if (FAM == RQ_TURBO) {
-      if (MAXB > 4) {
-        // fp16 centroid tables of the unit's K and V widths (above 4 bits
-        // they are looked up in LDS); rotate_queries ends with a barrier
-        _Float16* tab = reinterpret_cast<_Float16*>(reinterpret_cast<uint8_t*>(qs) +
-                                                    (size_t)G * kD * sizeof(float));
-        for (int e = tid; e < 512; e += kThreads) {
-          const int side = e >> 8, k = e & 255, bb = side ? bv : bk;
-          if (k < (1 << bb)) tab[e] = (_Float16)a.cb[(bb - 1) * 512 + 256 + k];
+      // LDS tables of the unit's K and V widths (pairs for 3 and 4 bits,
+      // centroids above); rotate_queries ends with a barrier
+      uint8_t* tab = reinterpret_cast<uint8_t*>(qs) + (size_t)G * kD * sizeof(float);
+      for (int e = tid; e < 512; e += kThreads) {
+        const int side = e >> 8, k = e & 255, bb = side ? bv : bk;
+        const float* c = a.cb + (bb - 1) * 512 + 256;
+        uint8_t* area = tab + side * kTqTabBytes;
+        if (bb >= 5) {
+          if (k < (1 << bb)) reinterpret_cast<_Float16*>(area)[k] = (_Float16)c[k];
+        } else if (bb >= 3 && k < (1 << (2 * bb))) {
+          const h2 v = {(_Float16)c[k & ((1 << bb) - 1)], (_Float16)c[k >> bb]};
+          reinterpret_cast<uint32_t*>(area)[k] = as_u32(v);
         }
-        lo.tabk = (lds_h*)tab;
-        lo.tabv = (lds_h*)(tab + 256);
       }
+      lo.tabk = (lds_h*)tab;
+      lo.tabv = (lds_h*)(tab + kTqTabBytes);
       rotate_queries(a, h, qraw, qs);
 #pragma unroll
       for (int i = 0; i < 32; ++i) qv[i] = j < G ? qs[j][32 * lo.r + i] : 0.0f;

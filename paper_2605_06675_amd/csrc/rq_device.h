@@ -1,7 +1,8 @@
 // Device helpers: number conversions, the quantizer arithmetic that decides
-// codes, and the packed-chunk format (32 codes in b words, bit planes whose
-// widths are the binary digits of b, codes i and i+16 sharing the two
-// half-words of a word).
+// codes, and the packed-chunk format (32 codes in b words; three-bit codes
+// as single fields in four 24-bit quarters of a 96-bit stream, other widths
+// as bit planes whose widths are the binary digits of b, codes i and i+16
+// sharing the two half-words of a word).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -78,76 +79,67 @@ __device__ __forceinline__ int asym_code(float x, const AsymParams& p,
   return rint_i(r);
 }
 
-// Bit planes of a b-bit code, widest first.
+// Bit planes of a b-bit code, widest first (three-bit codes are single
+// fields and do not use planes).
 template <int B> struct Planes;
 template <> struct Planes<1> { static constexpr int n = 1; static constexpr int w[1] = {1}; };
 template <> struct Planes<2> { static constexpr int n = 1; static constexpr int w[1] = {2}; };
-template <> struct Planes<3> { static constexpr int n = 2; static constexpr int w[2] = {2, 1}; };
 template <> struct Planes<4> { static constexpr int n = 1; static constexpr int w[1] = {4}; };
 template <> struct Planes<5> { static constexpr int n = 2; static constexpr int w[2] = {4, 1}; };
 template <> struct Planes<6> { static constexpr int n = 2; static constexpr int w[2] = {4, 2}; };
 template <> struct Planes<7> { static constexpr int n = 3; static constexpr int w[3] = {4, 2, 1}; };
 template <> struct Planes<8> { static constexpr int n = 1; static constexpr int w[1] = {8}; };
 
+// Three-bit chunk: the three words are one 96-bit stream (bit 32k + j =
+// bit j of word k) of four 24-bit quarters; quarter q holds codes 4q + i
+// at stream bit 24q + 3i and codes 16 + 4q + i at 24q + 12 + 3i (i = 0..3).
+// Codes 6 and 25 cross a word boundary.
+__host__ __device__ __forceinline__ constexpr int stream3_pos(int i) {
+  return 24 * ((i & 15) >> 2) + 3 * (i & 3) + (i >= 16 ? 12 : 0);
+}
+
 // Pack 32 codes (bytes, code i = byte i of c[i/4]) into B words.
 template <int B>
 __device__ __forceinline__ void pack_chunk(const uint32_t c[8], uint32_t out[B]) {
-  int word = 0, shift = 0;
+  if constexpr (B == 3) {
+    out[0] = out[1] = out[2] = 0;
 #pragma unroll
-  for (int p = 0; p < Planes<B>::n; ++p) {
-    const int w = Planes<B>::w[p];
-    const int per = 16 / w;
-    const uint32_t m = (1u << w) - 1u;
-#pragma unroll
-    for (int d = 0; d < w; ++d) {
-      uint32_t acc = 0;
-#pragma unroll
-      for (int k = 0; k < per; ++k) {
-        const int i0 = d * per + k, i1 = 16 + d * per + k;
-        uint32_t c0 = (c[i0 >> 2] >> (8 * (i0 & 3))) & 0xffu;
-        uint32_t c1 = (c[i1 >> 2] >> (8 * (i1 & 3))) & 0xffu;
-        acc |= ((c0 >> shift) & m) << (k * w);
-        acc |= ((c1 >> shift) & m) << (16 + k * w);
-      }
-      out[word++] = acc;
+    for (int i = 0; i < 32; ++i) {
+      const uint32_t code = (c[i >> 2] >> (8 * (i & 3))) & 7u;
+      const int pos = stream3_pos(i), word = pos >> 5, bit = pos & 31;
+      out[word] |= code << bit;
+      if (bit > 29) out[word + 1] |= code >> (32 - bit);
     }
-    shift += w;
+    return;
+  } else {
+    int word = 0, shift = 0;
+#pragma unroll
+    for (int p = 0; p < Planes<B>::n; ++p) {
+      const int w = Planes<B>::w[p];
+      const int per = 16 / w;
+      const uint32_t m = (1u << w) - 1u;
+#pragma unroll
+      for (int d = 0; d < w; ++d) {
+        uint32_t acc = 0;
+#pragma unroll
+        for (int k = 0; k < per; ++k) {
+          const int i0 = d * per + k, i1 = 16 + d * per + k;
+          uint32_t c0 = (c[i0 >> 2] >> (8 * (i0 & 3))) & 0xffu;
+          uint32_t c1 = (c[i1 >> 2] >> (8 * (i1 & 3))) & 0xffu;
+          acc |= ((c0 >> shift) & m) << (k * w);
+          acc |= ((c1 >> shift) & m) << (16 + k * w);
+        }
+        out[word++] = acc;
+      }
+      shift += w;
+    }
   }
-}
-
-// 0x64006400 (the fp16 pair 1024, 1024) in a register the compiler cannot
-// see through, so that "(x & mask) | magic" becomes one v_and_or_b32 with
-// the mask in an SGPR (VOP3 has no literal operand on this target).
-__device__ __forceinline__ uint32_t opaque_magic() {
-  uint32_t m = 0x64006400u;
-  asm volatile("" : "+v"(m));
-  return m;
 }
 
 // x shifted right by s bits (left when s < 0); s is a constant after
 // unrolling.
 __device__ __forceinline__ uint32_t shr_signed(uint32_t x, int s) {
   return s > 0 ? (x >> s) : (s < 0 ? (x << -s) : x);
-}
-
-// Codes i and i+16 of a chunk (0 <= i < 16) placed into the two fp16
-// mantissas of `acc` (which carries the 1024 exponent pattern): returns
-// acc | code_i | code_{i+16} << 16, read from the chunk's B words (i must
-// fold to a constant after unrolling).
-template <int B>
-__device__ __forceinline__ uint32_t pair_or(const uint32_t* wds, int I, uint32_t acc) {
-  int word = 0, shift = 0;
-#pragma unroll
-  for (int p = 0; p < Planes<B>::n; ++p) {
-    const int w = Planes<B>::w[p];
-    const int per = 16 / w;
-    const uint32_t m = ((1u << w) - 1u) * 0x00010001u;
-    const int d = I / per, k = I % per;
-    acc = (shr_signed(wds[word + d], k * w - shift) & (m << shift)) | acc;
-    word += w;
-    shift += w;
-  }
-  return acc;
 }
 
 // Entry i (wave-uniform) of a byte table held in the kernel arguments
@@ -165,11 +157,6 @@ __device__ __forceinline__ h2 as_h2(uint32_t x) {
 }
 __device__ __forceinline__ uint32_t as_u32(h2 x) {
   return __builtin_bit_cast(uint32_t, x);
-}
-
-// fp16 pair (1024 + code0, 1024 + code1) minus off, exactly.
-__device__ __forceinline__ h2 magic_to_h2(uint32_t magic_pair, h2 off) {
-  return as_h2(magic_pair) - off;
 }
 
 }  // namespace rq

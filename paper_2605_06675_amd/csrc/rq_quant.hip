@@ -100,7 +100,10 @@ __device__ __forceinline__ uint32_t kivi_code_bits(float x, float zf, float inv)
 // that reaches the top bit are added as (bits >> shift), which carries the
 // constant kMagicBits >> shift along, and lower planes are extracted
 // exactly.  Fields never overlap, so the sum equals the OR of the fields
-// plus a compile-time constant per word, removed by finish().
+// plus a compile-time constant per word, removed by finish().  A three-bit
+// code is one field; its part that crosses into the next word is
+// (bits >> k), k <= 2, which is (kMagicBits >> k) + (code >> k) because the
+// low 24 bits of kMagicBits are zero.
 template <int B> struct ChunkAcc {
   uint32_t w[B];
   uint32_t bias[B];
@@ -111,21 +114,32 @@ template <int B> struct ChunkAcc {
   }
   // code i of the chunk (0..31, constant after unrolling)
   __device__ __forceinline__ void add(int i, uint32_t cb) {
-    int word = 0, shift = 0;
-#pragma unroll
-    for (int p = 0; p < Planes<B>::n; ++p) {
-      const int wd = Planes<B>::w[p];
-      const int per = 16 / wd;
-      const int j = i & 15, d = j / per, k = j % per;
-      const int pos = k * wd + (i >= 16 ? 16 : 0);
-      if (shift + wd == B) {
-        w[word + d] += (cb >> shift) << pos;
-        bias[word + d] += (kMagicBits >> shift) << pos;
-      } else {
-        w[word + d] += __builtin_amdgcn_ubfe(cb, shift, wd) << pos;
+    if constexpr (B == 3) {
+      const int pos = stream3_pos(i), word = pos >> 5, bit = pos & 31;
+      w[word] += cb << bit;
+      bias[word] += kMagicBits << bit;
+      if (bit > 29) {
+        w[word + 1] += cb >> (32 - bit);
+        bias[word + 1] += kMagicBits >> (32 - bit);
       }
-      word += wd;
-      shift += wd;
+      return;
+    } else {
+      int word = 0, shift = 0;
+#pragma unroll
+      for (int p = 0; p < Planes<B>::n; ++p) {
+        const int wd = Planes<B>::w[p];
+        const int per = 16 / wd;
+        const int j = i & 15, d = j / per, k = j % per;
+        const int pos = k * wd + (i >= 16 ? 16 : 0);
+        if (shift + wd == B) {
+          w[word + d] += (cb >> shift) << pos;
+          bias[word + d] += (kMagicBits >> shift) << pos;
+        } else {
+          w[word + d] += __builtin_amdgcn_ubfe(cb, shift, wd) << pos;
+        }
+        word += wd;
+        shift += wd;
+      }
     }
   }
   __device__ __forceinline__ void finish() {

@@ -32,16 +32,40 @@ def test_pack_hand_examples():
     c = np.zeros(32, dtype=int)                             # b = 1
     c[0], c[15], c[16], c[31] = 1, 1, 1, 1
     assert [int(x) for x in fmt.pack_chunks(c, 1)] == [0x80018001]
-    c = np.zeros(32, dtype=int)                             # b = 3: planes 2,1
+    c = np.zeros(32, dtype=int)                             # b = 3: one field
     c[0], c[16], c[9] = 7, 5, 2
     w = [int(x) for x in fmt.pack_chunks(c, 3)]
-    # 2-bit plane word 0 holds codes 0..7 | 16..23, word 1 codes 8..15 | 24..31
-    assert w == [0x00010003, 0x00000008, 0x00010001]
+    # code 0 at stream bit 0, code 16 at bit 12 (quarter 0), code 9 =
+    # quarter 2 slot 1 at bit 48 + 3 = word 1 bit 19
+    assert w == [0x00005007, 0x00100000, 0x00000000]
+    c = np.zeros(32, dtype=int)
+    c[6], c[25], c[31] = 7, 5, 6
+    w = [int(x) for x in fmt.pack_chunks(c, 3)]
+    # code 6 = quarter 1 slot 2 at bits 30..32 (crosses into word 1),
+    # code 25 = quarter 2 upper slot 1 at bits 63..65 (crosses into word 2),
+    # code 31 = quarter 3 upper slot 3 at bits 93..95
+    assert w == [0xC0000000, 0x80000001, 0xC0000002]
+
+
+def test_pack3_pairs_after_spreading():
+    # The property the layout is built for: quarter q's 24 bits, the upper
+    # 12 moved up by 4, hold codes (4q + i, 16 + 4q + i) at bits (3i, 16 + 3i).
+    rng = np.random.default_rng(3)
+    c = rng.integers(0, 8, size=32)
+    w = [int(x) for x in fmt.pack_chunks(c, 3)]
+    stream = w[0] | (w[1] << 32) | (w[2] << 64)
+    for q in range(4):
+        x = (stream >> (24 * q)) & 0xFFFFFF
+        z = (x & 0xFFF) | ((x >> 12) << 16)
+        for i in range(4):
+            assert (z >> (3 * i)) & 7 == c[4 * q + i]
+            assert (z >> (16 + 3 * i)) & 7 == c[16 + 4 * q + i]
 
 
 def test_plane_widths():
     assert [sum(fmt.planes(b)) for b in range(1, 9)] == list(range(1, 9))
     assert fmt.planes(7) == [4, 2, 1] and fmt.planes(6) == [4, 2]
+    assert fmt.planes(3) == [3]
 
 
 def test_pair_order():
