@@ -319,27 +319,17 @@ __device__ __forceinline__ uint32_t tq_code_pair(const uint32_t* wds, int i) {
   return f;
 }
 
-// fp16 centroid pair of a code pair f (codes at bits 0 and 16, widths 1
-// and 2).  lut: the 2^b centroids as fp16 pairs in code order.
-template <int B>
-__device__ __forceinline__ uint32_t tq_lut(uint32_t f, const uint32_t* lut) {
-  static_assert(B <= 2, "register tables hold widths 1 and 2");
-  if constexpr (B == 1) return lut[0] | ((~f & 0x00010001u) << 15);
-  else return __builtin_amdgcn_perm(lut[1], lut[0], f * 0x202u + 0x01000100u);
+// fp16 centroid pair of a one-bit code pair f (codes at bits 0 and 16):
+// the codebook is +-c, so the pair is (c, c) with the sign bits of the
+// zero codes set.  lut: the fp16 pair (c, c).
+__device__ __forceinline__ uint32_t tq_lut1(uint32_t f, uint32_t lut) {
+  return lut | ((~f & 0x00010001u) << 15);
 }
 
-// fp16 lookup table of the b-bit codebook (b <= 2, layout of tq_lut) from
-// the fp32 centroid table
-__device__ __forceinline__ void tq_make_lut(const float* cb, int b, uint32_t lut[2]) {
-  const float* c = cb + (b - 1) * 512 + 256;
-  if (b == 1) {
-    const h2 v = {(_Float16)c[1], (_Float16)c[1]};
-    lut[0] = lut[1] = as_u32(v);
-  } else {
-    const h2 v0 = {(_Float16)c[0], (_Float16)c[1]}, v1 = {(_Float16)c[2], (_Float16)c[3]};
-    lut[0] = as_u32(v0);
-    lut[1] = as_u32(v1);
-  }
+// the fp16 pair (c, c) of the one-bit codebook from the fp32 centroid table
+__device__ __forceinline__ uint32_t tq_make_lut1(const float* cb) {
+  const h2 v = {(_Float16)cb[256 + 1], (_Float16)cb[256 + 1]};
+  return as_u32(v);
 }
 
 // Codes (i, i + 16) of a chunk times two, at bits 1 and 17: the byte offsets
@@ -360,13 +350,13 @@ typedef __attribute__((address_space(3))) const uint32_t lds_u32;
 typedef uint16_t us2v __attribute__((ext_vector_type(2)));
 
 // LDS tables of a TurboQuant width, one 1 KiB area per side (K, V):
-// widths 3 and 4 hold every code pair (u, v) as the fp16 pair
+// widths 2..4 hold every code pair (u, v) as the fp16 pair
 // (centroid u, centroid v) at entry u + 2^b v; widths 5..8 hold the 2^b
 // fp16 centroids.
 constexpr int kTqTabBytes = 1024;
 
 // fp16 centroid pair of code pair f (codes at bits 0 and 16, nothing else
-// set; widths 3 and 4) from the pair table: the byte offset 4 u + 2^(b+2) v
+// set; widths 2..4) from the pair table: the byte offset 4 u + 2^(b+2) v
 // is one two-way dot product of f's halves
 template <int B>
 __device__ __forceinline__ uint32_t tq_tab(uint32_t f, lds_h* tab) {
@@ -388,9 +378,8 @@ __device__ __forceinline__ uint32_t tq_lds(uint32_t f, lds_h* tab) {
 
 // fp16 centroid pair of codes (i, i+16) of a chunk of width B
 template <int B>
-__device__ __forceinline__ uint32_t tq_pair(const uint32_t* wds, int i, const uint32_t* lut,
-                                            lds_h* tab) {
-  if constexpr (B <= 2) return tq_lut<B>(tq_code_pair<B>(wds, i), lut);
+__device__ __forceinline__ uint32_t tq_pair(const uint32_t* wds, int i, uint32_t lut, lds_h* tab) {
+  if constexpr (B == 1) return tq_lut1(tq_code_pair<B>(wds, i), lut);
   else if constexpr (B <= 4) return tq_tab<B>(tq_code_pair<B>(wds, i) & pair_mask(B), tab);
   else return tq_lds(tq_code2_pair<B>(wds, i), tab);
 }
@@ -427,10 +416,10 @@ struct LaneOps {
   float cK;         // qscale 2^(24+e) (codes as subnormals) or qscale 2^e
                     // (TurboQuant), qscale = scale * log2(e)
   float eK;         // KIVI: qscale 2^e (the zero-point sum)
-  uint32_t lutk[2]; // TurboQuant: fp16 centroid tables of the K and V widths
-  uint32_t lutv[2]; //   (widths <= 2)
+  uint32_t lut1;    // TurboQuant: the fp16 pair (c, c) of the one-bit
+                    //   codebook +-c
   lds_h* tabk;      // TurboQuant: LDS tables of the K and V widths (pairs
-  lds_h* tabv;      //   for widths 3, 4; centroids for widths >= 5)
+  lds_h* tabv;      //   for widths 2..4; centroids for widths >= 5)
   int r, col, lane;
   int gsub;         // col / GP
   int GP;           // queries per replica (power of two >= G)
@@ -502,15 +491,15 @@ __device__ __forceinline__ void kpart(const SlotPtrs& sp, const LaneOps& lo, flo
       const h8 Bk = make_h8(lo.qh[4 * kb], lo.qh[4 * kb + 1], lo.qh[4 * kb + 2],
                             lo.qh[4 * kb + 3]);
       if constexpr (FAM == RQ_TURBO) {
-        S0 = mfma(make_h8(tq_pair<BK>(kw[0], 4 * kb, lo.lutk, lo.tabk),
-                          tq_pair<BK>(kw[0], 4 * kb + 1, lo.lutk, lo.tabk),
-                          tq_pair<BK>(kw[0], 4 * kb + 2, lo.lutk, lo.tabk),
-                          tq_pair<BK>(kw[0], 4 * kb + 3, lo.lutk, lo.tabk)),
+        S0 = mfma(make_h8(tq_pair<BK>(kw[0], 4 * kb, lo.lut1, lo.tabk),
+                          tq_pair<BK>(kw[0], 4 * kb + 1, lo.lut1, lo.tabk),
+                          tq_pair<BK>(kw[0], 4 * kb + 2, lo.lut1, lo.tabk),
+                          tq_pair<BK>(kw[0], 4 * kb + 3, lo.lut1, lo.tabk)),
                   Bk, S0);
-        S1 = mfma(make_h8(tq_pair<BK>(kw[1], 4 * kb, lo.lutk, lo.tabk),
-                          tq_pair<BK>(kw[1], 4 * kb + 1, lo.lutk, lo.tabk),
-                          tq_pair<BK>(kw[1], 4 * kb + 2, lo.lutk, lo.tabk),
-                          tq_pair<BK>(kw[1], 4 * kb + 3, lo.lutk, lo.tabk)),
+        S1 = mfma(make_h8(tq_pair<BK>(kw[1], 4 * kb, lo.lut1, lo.tabk),
+                          tq_pair<BK>(kw[1], 4 * kb + 1, lo.lut1, lo.tabk),
+                          tq_pair<BK>(kw[1], 4 * kb + 2, lo.lut1, lo.tabk),
+                          tq_pair<BK>(kw[1], 4 * kb + 3, lo.lut1, lo.tabk)),
                   Bk, S1);
       } else {
         S0 = mfma(make_h8(kpair<BK>(kw[0], 4 * kb), kpair<BK>(kw[0], 4 * kb + 1),
@@ -606,7 +595,7 @@ __device__ __forceinline__ void vpart(const SlotPtrs& sp, const LaneOps& lo,
         for (int i = 0; i < 4; ++i) pr[i] = tq_tab<3>((z >> (3 * i)) & pair_mask(3), lo.tabv);
       } else {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) pr[i] = tq_pair<BV>(ch, 4 * r + i, lo.lutv, lo.tabv);
+        for (int i = 0; i < 4; ++i) pr[i] = tq_pair<BV>(ch, 4 * r + i, lo.lut1, lo.tabv);
       }
     } else {
       vpairs<BV>(sp.vc + (16 * nt + col) * BV, r, pr);
@@ -1098,11 +1087,41 @@ __device__ __forceinline__ void store_queries(const AttnLaunch& a, u4 piece, boo
 // fp16 for fp16 queries) as B.  Wave w computes coordinate tiles 2w, 2w+1.
 typedef __bf16 abf8 __attribute__((ext_vector_type(8)));
 
-__device__ __forceinline__ void rotate_queries(const AttnLaunch& a, int h, const uint16_t* qraw,
-                                               float (*qs)[kD]) {
+// What the TurboQuant set-up reads from global memory, loaded before the
+// query and the first block copies (so that waiting for it never waits
+// for a copy): this lane's B operands of the query rotation (rows of R)
+// and the codebook entries of its LDS table entries.
+struct TurboPrefetch {
+  u4 rb[2][4];      // [tile t][k-step]: R row 16 (2 wave + t) + r, 8 entries
+  float c[2][2];    // [side][lo, hi]: centroids of table entry tid of the side
+};
+
+__device__ __forceinline__ void turbo_prefetch(const AttnLaunch& a, int h, int bk, int bv,
+                                               TurboPrefetch& p) {
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid / kWave), lane = tid & (kWave - 1);
   const int r = lane & 15, g = lane >> 4;
-  const uint16_t* Rh = a.rot + (size_t)h * kD * kD;
+  const RQ_GLOBAL u4* Rh = gptr(reinterpret_cast<const u4*>(a.rot + (size_t)h * kD * kD));
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+      p.rb[t][ks] = Rh[((16 * (2 * wave + t) + r) * kD + 32 * ks + 8 * g) / 8];
+  // table entry k = tid of each side: centroid k (widths >= 5) or the pair
+  // (k mod 2^b, k / 2^b) (widths 2..4); indices < 256 stay inside the
+  // width's 512-entry row of the codebook table
+#pragma unroll
+  for (int side = 0; side < 2; ++side) {
+    const int bb = side ? bv : bk;
+    const RQ_GLOBAL float* c = gptr(a.cb + (bb - 1) * 512 + 256);
+    p.c[side][0] = c[bb >= 5 ? tid : (tid & ((1 << bb) - 1))];
+    p.c[side][1] = c[(tid >> bb) & 255];
+  }
+}
+
+__device__ __forceinline__ void rotate_queries(const AttnLaunch& a, const TurboPrefetch& p,
+                                               const uint16_t* qraw, float (*qs)[kD]) {
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid / kWave), lane = tid & (kWave - 1);
+  const int r = lane & 15, g = lane >> 4;
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
     const int nt = 2 * wave + t;
@@ -1111,7 +1130,7 @@ __device__ __forceinline__ void rotate_queries(const AttnLaunch& a, int h, const
     for (int ks = 0; ks < 4; ++ks) {
       // rows >= G (outputs unused) read row 0: qraw holds G rows
       const u4 qa = *reinterpret_cast<const u4*>(&qraw[(r < a.G ? r : 0) * kD + 32 * ks + 8 * g]);
-      u4 rb = gptr(reinterpret_cast<const u4*>(&Rh[(16 * nt + r) * kD + 32 * ks + 8 * g]))[0];
+      u4 rb = p.rb[t][ks];
       if (a.is_bf16) {
         d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(abf8, qa),
                                                     __builtin_bit_cast(abf8, rb), d, 0, 0, 0);
@@ -1333,6 +1352,8 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int n
   cl.nblk = g_hi;
   cl.live = cl.base < g_hi;
   cl.mark = 0;
+  TurboPrefetch tp;
+  if (FAM == RQ_TURBO) turbo_prefetch(a, h, bk, bv, tp);
   const int nq_ops = issue_query(a, b, h, wave, lane, qraw);
   int issued = 0;
   if (cl.live) {
@@ -1359,23 +1380,24 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int n
     const int j = lo.col & (a.GP - 1);
     float qv[32];
     if (FAM == RQ_TURBO) {
-      // LDS tables of the unit's K and V widths (pairs for 3 and 4 bits,
+      // LDS tables of the unit's K and V widths (pairs for 2..4 bits,
       // centroids above); rotate_queries ends with a barrier
       uint8_t* tab = reinterpret_cast<uint8_t*>(qs) + (size_t)G * kD * sizeof(float);
-      for (int e = tid; e < 512; e += kThreads) {
-        const int side = e >> 8, k = e & 255, bb = side ? bv : bk;
-        const float* c = a.cb + (bb - 1) * 512 + 256;
+      static_assert(kThreads == 256, "one table entry of each side per thread");
+#pragma unroll
+      for (int side = 0; side < 2; ++side) {
+        const int k = tid, bb = side ? bv : bk;
         uint8_t* area = tab + side * kTqTabBytes;
         if (bb >= 5) {
-          if (k < (1 << bb)) reinterpret_cast<_Float16*>(area)[k] = (_Float16)c[k];
-        } else if (bb >= 3 && k < (1 << (2 * bb))) {
-          const h2 v = {(_Float16)c[k & ((1 << bb) - 1)], (_Float16)c[k >> bb]};
+          if (k < (1 << bb)) reinterpret_cast<_Float16*>(area)[k] = (_Float16)tp.c[side][0];
+        } else if (bb >= 2 && k < (1 << (2 * bb))) {
+          const h2 v = {(_Float16)tp.c[side][0], (_Float16)tp.c[side][1]};
           reinterpret_cast<uint32_t*>(area)[k] = as_u32(v);
         }
       }
       lo.tabk = (lds_h*)tab;
       lo.tabv = (lds_h*)(tab + kTqTabBytes);
-      rotate_queries(a, h, qraw, qs);
+      rotate_queries(a, tp, qraw, qs);
 #pragma unroll
       for (int i = 0; i < 32; ++i) qv[i] = j < G ? qs[j][32 * lo.r + i] : 0.0f;
     } else {
@@ -1449,8 +1471,7 @@ __device__ __forceinline__ void stream_slot(const AttnLaunch& a, int slot, int n
     for (int i = 0; i < 4; ++i) lo.vq[i] = h_pair((uint32_t)(15 + vp[i]) << 10);
     lo.corrK = (f4){0.f, 0.f, 0.f, 0.f};
     if (FAM == RQ_TURBO) {
-      tq_make_lut(a.cb, bk, lo.lutk);
-      tq_make_lut(a.cb, bv, lo.lutv);
+      lo.lut1 = tq_make_lut1(a.cb);
     }
     if (key_fam(FAM) == RQ_QUAROT) {
       // the symmetric offset of the key codes, -2^(b-1) at the codes'
@@ -1589,6 +1610,17 @@ __device__ __forceinline__ void merge_rows(const AttnLaunch& a, size_t unit, flo
   const int ns = count + nwin;
   const float* base = part_ptr(a, unit, 0) + (size_t)j * (2 + kD);
   const size_t stride = (size_t)G * (2 + kD);
+  // TurboQuant output: the unit's rotation (32 KB) is loaded now, in flight
+  // with the partials, and staged in LDS after them
+  constexpr int kRotLoads = kD * kD / 8 / kThreads;
+  const bool turbo_out = !dst && a.family == RQ_TURBO;
+  u4 rtmp[kRotLoads];
+  if (turbo_out) {
+    const RQ_GLOBAL u4* src = gptr(reinterpret_cast<const u4*>(
+        a.rot + (size_t)(unit % a.H) * kD * kD));
+#pragma unroll
+    for (int k = 0; k < kRotLoads; ++k) rtmp[k] = src[tid + k * kThreads];
+  }
   float M = -INFINITY, den = 0.0f, num[E], tail[E];
 #pragma unroll
   for (int k = 0; k < E; ++k) num[k] = tail[k] = 0.0f;
@@ -1674,12 +1706,8 @@ __device__ __forceinline__ void merge_rows(const AttnLaunch& a, size_t unit, flo
   }
   // TurboQuant: x = R^T y, R staged in LDS (row-major, as stored)
   uint16_t* Rs = reinterpret_cast<uint16_t*>(lds + G * kD);
-  {
-    const RQ_GLOBAL u4* src = gptr(reinterpret_cast<const u4*>(
-        a.rot + (size_t)(unit % a.H) * kD * kD));
-    for (int i = tid; i < kD * kD / 8; i += kThreads)
-      reinterpret_cast<u4*>(Rs)[i] = src[i];
-  }
+#pragma unroll
+  for (int k = 0; k < kRotLoads; ++k) reinterpret_cast<u4*>(Rs)[tid + k * kThreads] = rtmp[k];
   __syncthreads();
   if (own) {
     float acc[E];
@@ -1785,25 +1813,26 @@ attn_kernel(AttnLaunch a) {
   // window's partial stores complete first
   if (slot < a.n_rw) wait_vm<0>();
   if (slot < nw) stream_slot<FAM, NA, MAXB>(a, slot, nw, h, b, qs, qraw, cst, slots, merge);
-  // publish this workgroup's partials and take a ticket.  Up to kGroup
-  // workgroups: the last to arrive merges every slot and the window.  More:
-  // they report in groups of kGroup, the last of a group merges it into a
-  // group partial; the group mergers then report on the final counter,
-  // whose last arrival merges the group partials and the window.  Every
-  // counter used is left ready for the next call.
+  // publish this workgroup's partials and take a ticket.  Up to
+  // kAttnMergeFlat workgroups: the last to arrive merges every slot and the
+  // window.  More: they report in groups of kGroup, the last of a group
+  // merges it into a group partial; the group mergers then report on the
+  // final counter, whose last arrival merges the group partials and the
+  // window.  Every counter used is left ready for the next call.
   uint64_t* cnt = a.counters + unit * a.cstride;
   const uint32_t ep = a.epoch;
   const int ng = (nw + kGroup - 1) / kGroup;
-  if (ng <= 1) {
+  if (nw <= kAttnMergeFlat) {
     if (take_ticket(cnt, ep) == (uint32_t)(nx - 1)) {
       merge_slots(a, unit, merge, 0, nw, nw, a.n_rw, nullptr);
       reset_counter(cnt, ep);
-      reset_counter(cnt + a.claim_off, ep);
+      // every claim group's line (the last arrival: nobody claims now)
+      for (int g = 0; g < (ng > 1 ? ng : 1); ++g) reset_counter(cnt + a.claim_off + 16 * g, ep);
     }
     return;
   }
   {
-    // two levels: every workgroup streams (nx = nw > kGroup)
+    // two levels: every workgroup streams (nx = nw > kAttnMergeFlat)
     const int g = slot / kGroup;
     const int gsz = nw - g * kGroup < kGroup ? nw - g * kGroup : kGroup;
     if (take_ticket(cnt + 1 + g, ep) != (uint32_t)(gsz - 1)) return;

@@ -208,11 +208,11 @@ int cu_count() {
   return n;
 }
 
-// Merge groups of a unit's workgroups (the two-level merge starts above one
-// group).
+// Merge groups of a unit's workgroups (the two-level merge starts above
+// kAttnMergeFlat workgroups, in groups of kAttnGroup).
 int merge_groups(int n_wg) {
-  const int ng = (n_wg + rq::kAttnGroup - 1) / rq::kAttnGroup;
-  return ng <= 1 ? 0 : ng;
+  if (n_wg <= rq::kAttnMergeFlat) return 0;
+  return (n_wg + rq::kAttnGroup - 1) / rq::kAttnGroup;
 }
 
 // Workgroups (four waves each) per (batch, kv-head) unit.  The grid is sized

@@ -28,6 +28,7 @@ __host__ __device__ inline size_t meta_unit_offset(int family, int h, int kind, 
          (size_t)b * nblk_cap * (kind ? mv : mk);
 }
 constexpr int kAttnGroup = 16;        // streaming slots per merge group
+constexpr int kAttnMergeFlat = 16;    // at most this many: one merge level
 constexpr int kAttnResChunk = 32;     // window tokens per window workgroup
 constexpr int kAttnMaxDepth = 4;      // most blocks in flight per attention wave
 constexpr int kAttnWaves = 4;         // waves per attention workgroup
