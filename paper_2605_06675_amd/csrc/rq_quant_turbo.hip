@@ -14,8 +14,9 @@
 // of a Haar matrix rounding to the fp16 subnormal grid, by at most 2^-25).
 // Norms are summed in fp64 from the same registers.  Codes count the
 // positive thresholds below |t| (the codebook is symmetric, with the middle
-// threshold at 0) and go, as bytes, through a small LDS buffer from which
-// each lane packs whole chunks.
+// threshold at 0).  Codes go through a small LDS buffer from which each
+// lane packs whole chunks: three-bit codes as quarters of a chunk already
+// in stream order, other widths as bytes.
 #include "rq_device.h"
 #include "rq_internal.h"
 #include "rq_ring.h"
@@ -114,15 +115,34 @@ __device__ __forceinline__ u4 r_op(const uint16_t* Rs, int ct, int ks, int lane)
 
 // Code of t: the number of thresholds below t.  th[] holds the P positive
 // thresholds (ascending); the L - 1 thresholds are -th reversed, 0, th.
+// cnt = #{j : th[j] < |t|}, found by bisection for b = 3 and 4 (the same
+// count: the thresholds are sorted).
 template <int B>
 __device__ __forceinline__ uint32_t turbo_code(float t, const float* th) {
   constexpr int L = 1 << B, P = L / 2 - 1;
   const float m = __builtin_fabsf(t);
-  int cnt = 0;
+  uint32_t cnt = 0;
+  if constexpr (B == 3) {
+    const bool c1 = th[1] < m;
+    cnt = (c1 ? 2u : 0u) + ((c1 ? th[2] : th[0]) < m ? 1u : 0u);
+  } else if constexpr (B == 4) {
+    const bool c1 = th[3] < m;
+    const bool c2 = (c1 ? th[5] : th[1]) < m;
+    const float t3 = c1 ? (c2 ? th[6] : th[4]) : (c2 ? th[2] : th[0]);
+    cnt = (c1 ? 4u : 0u) + (c2 ? 2u : 0u) + (t3 < m ? 1u : 0u);
+  } else {
 #pragma unroll
-  for (int j = 0; j < P; ++j) cnt += th[j] < m ? 1 : 0;
-  return (uint32_t)(t > 0.0f ? L / 2 + cnt : L / 2 - 1 - cnt);
+    for (int j = 0; j < P; ++j) cnt += th[j] < m ? 1u : 0u;
+  }
+  return t > 0.0f ? (uint32_t)(L / 2) + cnt : (uint32_t)(L / 2 - 1) - cnt;
 }
+
+// Three-bit codes: in both operand layouts a lane holds quarter g = lane /
+// 16 of one chunk (codes 4g + i and 16 + 4g + i, i = 0..3), which it
+// assembles as the chunk's stream bits 24g .. 24g + 23 and stages as one
+// dword (kQ3W dwords per chunk, padded against bank conflicts); the pack
+// step joins a chunk's four quarters into its three words.
+constexpr int kQ3W = 5;
 
 __device__ __forceinline__ uint32_t bytes4(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3) {
   return c0 | (c1 << 8) | (c2 << 16) | (c3 << 24);
@@ -195,12 +215,22 @@ __device__ __forceinline__ void turbo_block_codes(const QuantLaunch& a, const ui
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt) {
         // lane: token 16 tt + j, coords 32q + 16c + 4g + i -> code 16c + 4g + i
-        uint32_t* u = cbuf + ((16 * tt + j) * 4 + q) * kUnitW;
+        if constexpr (B == 3) {
+          uint32_t qb = 0;
 #pragma unroll
-        for (int c = 0; c < 2; ++c) {
-          const f4 y = d[c][tt];
-          u[4 * c + g] = bytes4(turbo_code<B>(y[0] * f[tt], th), turbo_code<B>(y[1] * f[tt], th),
-                                turbo_code<B>(y[2] * f[tt], th), turbo_code<B>(y[3] * f[tt], th));
+          for (int c = 0; c < 2; ++c)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              qb |= turbo_code<3>(d[c][tt][i] * f[tt], th) << (12 * c + 3 * i);
+          cbuf[((16 * tt + j) * 4 + q) * kQ3W + g] = qb;
+        } else {
+          uint32_t* u = cbuf + ((16 * tt + j) * 4 + q) * kUnitW;
+#pragma unroll
+          for (int c = 0; c < 2; ++c) {
+            const f4 y = d[c][tt];
+            u[4 * c + g] = bytes4(turbo_code<B>(y[0] * f[tt], th), turbo_code<B>(y[1] * f[tt], th),
+                                  turbo_code<B>(y[2] * f[tt], th), turbo_code<B>(y[3] * f[tt], th));
+          }
         }
       }
     }
@@ -220,12 +250,23 @@ __device__ __forceinline__ void turbo_block_codes(const QuantLaunch& a, const ui
 #pragma unroll
         for (int tt = 0; tt < 2; ++tt) d[tt] = mma<BF16>(x[4 * tt + ks], r, d[tt]);
       }
-      uint32_t* u = cbuf + (16 * ct + j) * kUnitW;
+      if constexpr (B == 3) {
+        // lane: coord 16 ct + j, tokens 16 tt + 4g + i -> code 16 tt + 4g + i
+        uint32_t qb = 0;
 #pragma unroll
-      for (int tt = 0; tt < 2; ++tt) {
-        const f4 y = d[tt];
-        u[4 * tt + g] = bytes4(turbo_code<B>(y[0] * fr[tt][0], th), turbo_code<B>(y[1] * fr[tt][1], th),
-                               turbo_code<B>(y[2] * fr[tt][2], th), turbo_code<B>(y[3] * fr[tt][3], th));
+        for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            qb |= turbo_code<3>(d[tt][i] * fr[tt][i], th) << (12 * tt + 3 * i);
+        cbuf[(16 * ct + j) * kQ3W + g] = qb;
+      } else {
+        uint32_t* u = cbuf + (16 * ct + j) * kUnitW;
+#pragma unroll
+        for (int tt = 0; tt < 2; ++tt) {
+          const f4 y = d[tt];
+          u[4 * tt + g] = bytes4(turbo_code<B>(y[0] * fr[tt][0], th), turbo_code<B>(y[1] * fr[tt][1], th),
+                                 turbo_code<B>(y[2] * fr[tt][2], th), turbo_code<B>(y[3] * fr[tt][3], th));
+        }
       }
     }
   }
@@ -236,6 +277,21 @@ __device__ __forceinline__ void turbo_block_codes(const QuantLaunch& a, const ui
   uint32_t* region = reinterpret_cast<uint32_t*>(a.codes + a.tab.code_off[h][id.kind]);
   uint32_t* base = id.kind == 0 ? region + ((size_t)id.b * a.cap + t0) * 4 * B
                                 : region + ((size_t)id.b * nblk_cap + id.blk) * kD * B;
+  if constexpr (B == 3) {
+#pragma unroll
+    for (int rep = 0; rep < 2; ++rep) {
+      const int unit = lane + rep * kWave;
+      const uint32_t* src = cbuf + unit * kQ3W;
+      const uint32_t q0 = src[0], q1 = src[1], q2 = src[2], q3 = src[3];
+      // words 0..2 = stream bits 0..31, 32..63, 64..95
+      RQ_GLOBAL uint32_t* dst = gptr(base + (size_t)unit * 3);
+      __builtin_nontemporal_store(q0 | (q1 << 24), dst);
+      __builtin_nontemporal_store(__builtin_amdgcn_alignbit(q2, q1 << 8, 16), dst + 1);
+      __builtin_nontemporal_store(__builtin_amdgcn_alignbit(q3, q2 << 8, 24), dst + 2);
+    }
+    __builtin_amdgcn_wave_barrier();
+    return;
+  }
 #pragma unroll
   for (int rep = 0; rep < 2; ++rep) {
     const int unit = lane + rep * kWave;
