@@ -220,9 +220,6 @@ __device__ __forceinline__ uint32_t pk_fms(uint32_t a, uint32_t b, uint32_t c) {
   return as_u32(__builtin_elementwise_fma(as_h2(a), as_h2(b), -as_h2(c)));
 }
 
-// fp16 pair (u_i 2^(P-24), u_{i+16} 2^(P-24)) of key pair i of a chunk (its
-// B words), P = kpos(B, i): the fields masked into the mantissa of a zero
-// exponent, exact subnormals.
 // Three-bit chunks (single fields in four 24-bit quarters of the 96-bit
 // stream of the chunk's words): quarter x (at bits 0..23 of x) with its
 // upper 12 bits moved up by 4, so that slot s (codes 4q+s, 16+4q+s) sits
@@ -251,6 +248,9 @@ __device__ __forceinline__ uint32_t slot3(uint32_t z, int s) {
   return s < 3 ? z & (pair_mask(3) << (3 * s)) : (z >> 9) & pair_mask(3);
 }
 
+// fp16 pair (u_i 2^(P-24), u_{i+16} 2^(P-24)) of key pair i of a chunk (its
+// B words), P = kpos(B, i): the fields masked into the mantissa of a zero
+// exponent, exact subnormals.
 template <int B>
 __device__ __forceinline__ uint32_t kpair(const uint32_t* wds, int i) {
   if constexpr (B == 3) return slot3(quarter3(wds, i >> 2), i & 3);
@@ -306,8 +306,8 @@ __device__ __forceinline__ void vpairs(const uint32_t* ch, int r, uint32_t out[4
 // a constant).
 template <int B>
 __device__ __forceinline__ uint32_t tq_code_pair(const uint32_t* wds, int i) {
-  // three bits: the fields at bits (0, 16), other bits not cleared (the
-  // three-bit table lookup reads only bits 0..2 and 16..18)
+  // three bits: the fields at bits (0, 16); the bits above them are not
+  // cleared (the caller masks)
   if constexpr (B == 3) return quarter3(wds, i >> 2) >> (3 * (i & 3));
   uint32_t f = 0;
 #pragma unroll
