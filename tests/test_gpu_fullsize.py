@@ -1,8 +1,8 @@
 """GPU parity at full size: one layer of each long-context workload, filled
 the way the benchmark fills it (prefill of T - s tokens, then s single-token
 appends, s = 64 for the long-context KIVI workload and 1 otherwise), then
-decode attention over all T tokens; sampled (batch, kv-head) units checked
-against the oracle (codes, metadata and window bit-exact, TurboQuant codes by
+decode attention over all T tokens; sampled (batch, kv-head) units, one of
+every width pair of the layer among them, checked against the oracle (codes, metadata and window bit-exact, TurboQuant codes by
 its near-threshold rule; attention within 1e-2 max-abs)."""
 import numpy as np
 import pytest
@@ -81,7 +81,14 @@ def test_full_size_layer_sampled(wl):
     bufs = gh.read_buffers(kvc)
     G = wl.group
     worst, mism, total = 0.0, 0, 0
-    for (b, h) in sorted({(0, 0), (B // 2, 3), (B - 1, H - 1)}):
+    # three fixed units, plus one unit of every (K, V) width pair the
+    # allocation gave this layer
+    first_of_pair = {}
+    for h in range(H):
+        first_of_pair.setdefault(tuple(int(x) for x in bits[0, h]), h)
+    units = {(0, 0), (B // 2, 3), (B - 1, H - 1)}
+    units |= {(h % B, h) for h in first_of_pair.values()}
+    for (b, h) in sorted(units):
         k16, v16 = gh.host_bits(K[b, h]), gh.host_bits(V[b, h])
         k = workloads.u16_to_f32(k16, wl.dtype)
         v = workloads.u16_to_f32(v16, wl.dtype)

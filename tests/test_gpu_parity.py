@@ -361,7 +361,8 @@ def test_calibration_sweep(family, bits):
 def test_llama3_8b_layer_sampled():
     """One full layer of the Llama-3-8B shaped workload (batch 16, 8192
     tokens, bf16, KIVI g32, window 32, bits from the allocator at 2.5
-    average), checked on sampled units."""
+    average), checked on sampled units, one of every width pair of the layer
+    among them."""
     torch = _torch()
     wl = workloads.LLAMA3_8B
     w, a, be = workloads.allocation_inputs(wl)
@@ -382,7 +383,13 @@ def test_llama3_8b_layer_sampled():
     bufs = gh.read_buffers(kvc)
     G = wl.group
     worst = 0.0
-    for (b, h) in [(0, 0), (7, 3), (15, 7)]:
+    # three fixed units, plus one unit of every (K, V) width pair of the layer
+    first_of_pair = {}
+    for h in range(wl.n_kv_heads):
+        first_of_pair.setdefault(tuple(int(x) for x in bits[0, h]), h)
+    units = {(0, 0), (7, 3), (15, 7)}
+    units |= {((5 * h) % wl.batch, h) for h in first_of_pair.values()}
+    for (b, h) in sorted(units):
         k16 = gh.host_bits(K[b, h])
         v16 = gh.host_bits(V[b, h])
         u = ocache.Unit(wl.family, workloads.u16_to_f32(k16, wl.dtype),
