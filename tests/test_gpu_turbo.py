@@ -163,6 +163,18 @@ def test_turbo_attention_eight_queries_per_head_no_window():
     _attention(kvc, units, workloads.BF16, 2, 8, 8)
 
 
+@pytest.mark.parametrize("G", [3, 6])
+def test_turbo_attention_group_sizes_not_power_of_two(G):
+    # query heads per kv-head that leave rotated query rows unused (3 of 4,
+    # 6 of 8); pair-table widths 2..4 and a centroid-table width; 1100
+    # tokens so several streaming workgroups merge
+    bits = np.array([[[2, 3], [4, 2], [3, 5]]])
+    print(f"turbo group size {G}", flush=True)
+    kvc, ks, vs, Rf = _build(workloads.BF16, 3, 1100, 32, bits, 2, G=G)
+    units = _check(workloads.BF16, kvc, ks, vs, Rf, bits, 32, 2, 3)
+    _attention(kvc, units, workloads.BF16, 2, 3, G)
+
+
 @pytest.mark.parametrize("dtype", [workloads.BF16, workloads.F16])
 def test_turbo_attention_wide_widths(dtype):
     # widths 5..8 look their centroids up in LDS; mixed with narrow ones
