@@ -29,10 +29,11 @@
 //                against constants (values).
 //   RTN          QuaRot's path with no rotation of the query or the output.
 //   TurboQuant   codes index the Lloyd-Max centroids, which are not affine
-//                in the code: each pair of codes is looked up in a table of
-//                fp16 centroids held in two to four registers (v_perm_b32,
-//                using the symmetry of the codebook for b >= 3) or, above 4
-//                bits, in LDS; the per-token norm scales the scores and
+//                in the code: each pair of codes is looked up in LDS, in a
+//                table of every code pair as an fp16 pair (widths 2..4, one
+//                read per pair) or of the fp16 centroids (wider codes, two
+//                16-bit reads); the one-bit codebook +-c is a sign OR on
+//                (c, c); the per-token norm scales the scores and
 //                probabilities.  The query is rotated by R on entry; the
 //                merge rotates the quantized part of the output back by R^T.
 // With G query heads per kv-head the sixteen MFMA columns carry the G
