@@ -87,7 +87,8 @@ constexpr int kMaxDepth = kAttnMaxDepth;
 constexpr int kAttnOcc = 3;
 
 // ---------------------------------------------------------- field positions
-// Plane widths of a b-bit code are the binary digits of b, widest first.
+// Plane widths of a b-bit code are the binary digits of b, widest first
+// (three-bit codes are single fields instead: see kpair<3>).
 __host__ __device__ __forceinline__ constexpr int plane_w(int b, int p) {
   int n = 0;
   for (int w = 8; w >= 1; w >>= 1)
